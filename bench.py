@@ -1,0 +1,193 @@
+"""Benchmark of the batched text-encoder prefill on one MI355X.
+
+One step = one pass of the whole hot path over one batch: device-side
+position build (mte_build_positions) + the 28-layer encoder forward
+(mte_encode), inputs resident in HBM. Prints ONE JSON line.
+
+Default workload: 16 frames x 96 tokens (8x8 merged image grid + 32
+instruction tokens), 28 layers of the Qwen3-VL-2B-class decoder, bf16
+weights, synthetic seeded weights and embeddings. The batch-1 frame
+(96 tokens) is timed as well and reported in the same line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def gemm_flops(dims, T):
+    """Algorithmic flops of the four projection GEMMs for T tokens, per layer."""
+    D, F, d = dims.hidden, dims.ffn, dims.head_dim
+    nqkv = (dims.n_q_heads + 2 * dims.n_kv_heads) * d
+    return {"qkv": 2 * T * nqkv * D, "o": 2 * T * D * dims.n_q_heads * d,
+            "gate_up": 2 * T * 2 * F * D, "down": 2 * T * D * F}
+
+
+def step_flops(dims, lens):
+    g = sum(gemm_flops(dims, sum(lens)).values())
+    att = sum(4 * dims.n_q_heads * dims.head_dim * L * (L + 1) // 2 for L in lens)
+    return dims.n_layers * (g + att)
+
+
+def run_workload(torch, name, steps, warmup, timing_class=None):
+    from paper_2606_05981_amd import binding as B
+    from paper_2606_05981_amd.encoder import TextEncoder, build_positions
+    from synth import workloads as W
+
+    wl = W.workload(name)
+    dims = wl.dims
+    lens = W.seq_lens(wl.layouts)
+    T = sum(lens)
+    cfg = B.make_config(dims.n_layers, dims.hidden, dims.n_q_heads, dims.n_kv_heads,
+                        dims.head_dim, dims.ffn, rms_eps=dims.rms_eps, rope_theta=dims.rope_theta,
+                        mrope_section=dims.mrope_section, mrope_layout=dims.mrope_layout,
+                        qk_norm=dims.qk_norm, dtype=B.MTE_BF16, out_dtype=B.MTE_F32, max_tokens=T,
+                        max_batch=len(lens), max_seq=max(lens))
+    enc = TextEncoder.from_host(cfg, (W.layer_weights(dims, l) for l in range(dims.n_layers)),
+                                W.final_norm_gain(dims))
+    emb = torch.from_numpy(W.embeddings(dims, wl.layouts)).to("cuda", torch.bfloat16)
+    layouts = [(s.n_text_before, s.grid_t, s.grid_h, s.grid_w, s.n_text_after) for s in wl.layouts]
+    out = torch.empty((T, dims.hidden), dtype=torch.float32, device="cuda")
+    pos = torch.empty((3, T), dtype=torch.int32, device="cuda")
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+
+    def step():
+        B.mte_build_positions(layouts, pos.data_ptr(), sh)
+        B.mte_encode(enc.handle, emb.data_ptr(), pos.data_ptr(), lens, len(lens), out.data_ptr(), sh)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    if timing_class is not None:
+        B.mte_timing_enable(enc.handle, timing_class, steps * dims.n_layers)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    kern = None
+    if timing_class is not None:
+        n, ms = B.mte_timing_read(enc.handle)
+        B.mte_timing_disable(enc.handle)
+        kern = (n, ms)
+    enc.close()
+    return dict(name=name, dims=dims, lens=lens, T=T, wall_s=wall, gpu_ms=gpu_ms, kern=kern)
+
+
+def cpu_baseline(min_seconds=10.0):
+    """The fp64 oracle on the host cores: whole 28-layer forwards of the 16 x 96-token
+    batch, repeated until at least `min_seconds` of CPU work has been timed."""
+    import numpy as np
+    from oracle import te_oracle as O
+    from synth import workloads as W
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    wl = W.workload("stack_b16")
+    dims = wl.dims
+    lens = W.seq_lens(wl.layouts)
+    emb = W.embeddings(dims, wl.layouts)
+    pos = O.positions(wl.layouts)
+    ws = [W.layer_weights(dims, l) for l in range(dims.n_layers)]
+    fin = W.final_norm_gain(dims)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        O.encode(emb, pos, lens, dims, lambda l: ws[l], fin)
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= min_seconds:
+            break
+    return {"value": round(sum(lens) * reps / dt, 2), "unit": "tokens/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": f"{reps} full 28-layer forward(s) of 16 frames x 96 tokens "
+                      f"({dt:.1f} s, fp64 numpy oracle)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="stack_b16")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-batch1", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); frames are independent, "
+              "so more GPUs would each run this same single-GPU path on a share of the batch.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    assert torch.cuda.is_available(), "no GPU"
+
+    main_run = run_workload(torch, args.workload, args.steps, args.warmup, timing_class=3)
+    dims, T = main_run["dims"], main_run["T"]
+    K = args.steps
+    ms_step = main_run["wall_s"] * 1e3 / K
+    tok_s = T * K / main_run["wall_s"]
+    frames_s = len(main_run["lens"]) * K / main_run["wall_s"]
+    n_launch, kern_ms = main_run["kern"]
+    gu_flops = gemm_flops(dims, T)["gate_up"]
+    avg_us = kern_ms * 1e3 / max(n_launch, 1)
+    achieved = gu_flops / (avg_us * 1e-6) / 1e12
+    total_tflops = step_flops(dims, main_run["lens"]) * K / main_run["wall_s"] / 1e12
+    res = {
+        "metric": "encoder prefill tokens/s (96 tok/frame, bs16; bs1 in batch1)",
+        "value": round(tok_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 (weights; activations as bf16 hi+lo pairs, fp32 accumulate)",
+        "data": "synthetic (seeded random-init weights and embeddings)",
+        "config": {"workload": f"{args.workload}: {len(main_run['lens'])} frames x "
+                               f"{max(main_run['lens'])} tokens, 28-layer Qwen3-VL-2B-class decoder "
+                               "(D 2048, 16q/8kv heads, d 128, FFN 6144), M-RoPE 24/20/20",
+                   "batch": len(main_run["lens"]), "tokens_per_step": T},
+        "frames_per_s": round(frames_s, 1),
+        "model_tflops": round(total_tflops, 1),
+        "roofline": {"kernel": "gate/up GEMM + SwiGLU", "bound": "mfma",
+                     "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "avg_launch_us": round(avg_us, 2), "launches": n_launch,
+                     "flops_per_launch": gu_flops},
+    }
+    if not args.no_batch1:
+        b1 = run_workload(torch, "stack_b1", K, args.warmup)
+        t1 = b1["wall_s"] / K
+        wbytes = dims.n_layers * dims.params_per_layer * 2 + 2 * b1["T"] * dims.hidden * 2
+        res["batch1"] = {"workload": "stack_b1: 1 frame x 96 tokens, 28 layers",
+                         "tokens_per_s": round(b1["T"] / t1, 1), "frames_per_s": round(1 / t1, 1),
+                         "ms_per_step": round(t1 * 1e3, 4),
+                         "hbm_roofline": {"bound": "hbm", "achieved": round(wbytes / t1 / 1e9, 1),
+                                          "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                                          "frac": round(wbytes / t1 / 1e9 / PEAK_HBM_GBS, 4),
+                                          "bytes_per_step": wbytes}}
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

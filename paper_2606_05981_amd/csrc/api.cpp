@@ -1,0 +1,426 @@
+// C ABI of the encoder: argument validation, the sequence plan, weight
+// repacking at creation and the per-call launch schedule. Nothing here reads
+// device memory back during mte_encode / mte_encode_layers /
+// mte_build_positions: the sequence plan is computed from the host lengths
+// and handed to the kernels by value.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "../../include/mte.h"
+#include "launch.h"
+
+using namespace mte;
+
+namespace {
+
+typedef uint16_t bf16_storage;
+constexpr int64_t kMaxTokens = (1 << 24) - 1;  // positions and offsets stay exact in fp32 / int32
+constexpr int kNumClasses = 5;
+
+struct LayerW {
+  void *w_qkv, *w_o, *w_gu, *w_d;              // storage type, repacked
+  float *attn_norm, *mlp_norm, *q_norm, *k_norm;
+};
+
+size_t esize(int dtype) { return dtype == MTE_BF16 ? 2 : 4; }
+int in_fmt(int dtype) { return dtype == MTE_BF16 ? FMT_BF16 : FMT_F32; }
+
+}  // namespace
+
+struct mte_encoder {
+  mte_config cfg;
+  int device = 0;
+  std::vector<LayerW> layers;
+  void *wbuf = nullptr;      // all GEMM weights
+  float *gbuf = nullptr;     // all norm gains (fp32)
+  float *final_norm = nullptr;
+  // Activations feeding the matrix cores are fp32 (MODE_F32) or bf16 hi/lo
+  // planes (MODE_BF16X2); both take 4 bytes per element.
+  int mode = MODE_F32;
+  int act_fmt = FMT_F32;
+  float *h = nullptr;        // [max_tokens, D] fp32 residual stream
+  void *xn = nullptr;        // [max_tokens, D] normalised GEMM input
+  float *qkv = nullptr;      // [max_tokens, (Hq + 2 Hkv) d] fp32
+  void *attn = nullptr;      // [max_tokens, Hq d] attention output
+  void *act = nullptr;       // [max_tokens, F] SwiGLU output
+  RopeParams rope;
+  // kernel timing
+  int timing_class = -1;
+  std::vector<hipEvent_t> ev;  // pairs: [2i] start, [2i+1] stop
+  int ev_used = 0;
+  int ev_cap = 0;
+};
+
+extern "C" {
+
+const char *mte_status_string(int status) {
+  switch (status) {
+    case MTE_OK: return "ok";
+    case MTE_E_INVALID: return "invalid argument";
+    case MTE_E_CAPACITY: return "beyond the encoder's capacity";
+    case MTE_E_HIP: return "HIP runtime error";
+    case MTE_E_OOM: return "device out of memory";
+    case MTE_E_UNSUPPORTED: return "unsupported configuration";
+    default: return "unknown status";
+  }
+}
+
+int mte_config_validate(const mte_config *c) {
+  if (!c) return MTE_E_INVALID;
+  if (c->n_layers < 0 || c->hidden <= 0 || c->n_q_heads <= 0 || c->n_kv_heads <= 0 ||
+      c->head_dim <= 0 || c->ffn <= 0)
+    return MTE_E_INVALID;
+  if (!(c->rms_eps > 0.f) || !(c->rope_theta > 0.f) || !std::isfinite(c->rms_eps) ||
+      !std::isfinite(c->rope_theta))
+    return MTE_E_INVALID;
+  if (c->n_q_heads % c->n_kv_heads != 0) return MTE_E_INVALID;
+  if (c->head_dim % 2 != 0) return MTE_E_INVALID;
+  for (int i = 0; i < 3; ++i)
+    if (c->mrope_section[i] < 0) return MTE_E_INVALID;
+  if (c->mrope_section[0] + c->mrope_section[1] + c->mrope_section[2] != c->head_dim / 2)
+    return MTE_E_INVALID;
+  if (c->mrope_layout != MTE_MROPE_SECTIONS && c->mrope_layout != MTE_MROPE_INTERLEAVED)
+    return MTE_E_INVALID;
+  if (c->qk_norm != 0 && c->qk_norm != 1) return MTE_E_INVALID;
+  if ((c->dtype != MTE_F32 && c->dtype != MTE_BF16) ||
+      (c->out_dtype != MTE_F32 && c->out_dtype != MTE_BF16))
+    return MTE_E_INVALID;
+  if (c->max_tokens <= 0 || c->max_batch <= 0 || c->max_seq <= 0) return MTE_E_INVALID;
+  // Shapes the kernels are built for.
+  if (c->head_dim != 64 && c->head_dim != 128) return MTE_E_UNSUPPORTED;
+  const int rep = c->n_q_heads / c->n_kv_heads;
+  if (!(rep == 1 || rep == 2 || rep % 4 == 0)) return MTE_E_UNSUPPORTED;
+  if (c->hidden % 256 || c->ffn % 256 || (c->n_q_heads * c->head_dim) % 256 ||
+      (c->n_kv_heads * c->head_dim) % 128)
+    return MTE_E_UNSUPPORTED;
+  if (c->max_tokens > kMaxTokens) return MTE_E_UNSUPPORTED;
+  return MTE_OK;
+}
+
+int mte_check_batch(const mte_config *c, const int32_t *seq_lens, int32_t batch,
+                    int32_t *total_tokens) {
+  if (!c || !seq_lens || batch <= 0) return MTE_E_INVALID;
+  int64_t tot = 0;
+  bool over = batch > c->max_batch;
+  for (int i = 0; i < batch; ++i) {
+    if (seq_lens[i] <= 0) return MTE_E_INVALID;
+    if (seq_lens[i] > c->max_seq) over = true;
+    tot += seq_lens[i];
+  }
+  if (over || tot > c->max_tokens) return MTE_E_CAPACITY;
+  if (total_tokens) *total_tokens = (int32_t)tot;
+  return MTE_OK;
+}
+
+int mte_build_positions(const mte_seq_layout *layouts, int32_t batch, int32_t *pos_thw,
+                        hipStream_t stream) {
+  if (!layouts || !pos_thw || batch <= 0) return MTE_E_INVALID;
+  int64_t T = 0;
+  std::vector<int32_t> l5((size_t)batch * 5);
+  for (int i = 0; i < batch; ++i) {
+    const mte_seq_layout &s = layouts[i];
+    if (s.n_text_before < 0 || s.n_text_after < 0 || s.grid_t < 0 || s.grid_h < 0 || s.grid_w < 0)
+      return MTE_E_INVALID;
+    const bool any = s.grid_t || s.grid_h || s.grid_w;
+    const bool all = s.grid_t && s.grid_h && s.grid_w;
+    if (any && !all) return MTE_E_INVALID;
+    const int64_t nimg = (int64_t)s.grid_t * s.grid_h * s.grid_w;
+    const int64_t len = (int64_t)s.n_text_before + nimg + s.n_text_after;
+    if (len <= 0) return MTE_E_INVALID;
+    T += len;
+    if (T > kMaxTokens) return MTE_E_INVALID;
+    int32_t *d = &l5[(size_t)i * 5];
+    d[0] = s.n_text_before; d[1] = s.grid_t; d[2] = s.grid_h; d[3] = s.grid_w; d[4] = s.n_text_after;
+  }
+  return launch_positions(l5.data(), batch, pos_thw, (int)T, stream) == hipSuccess ? MTE_OK : MTE_E_HIP;
+}
+
+void mte_encoder_destroy(mte_encoder *e) {
+  if (!e) return;
+  int cur = 0;
+  hipGetDevice(&cur);
+  hipSetDevice(e->device);
+  hipDeviceSynchronize();
+  for (hipEvent_t ev : e->ev) hipEventDestroy(ev);
+  hipFree(e->wbuf);
+  hipFree(e->gbuf);
+  hipFree(e->h);
+  hipFree(e->xn);
+  hipFree(e->qkv);
+  hipFree(e->attn);
+  hipFree(e->act);
+  hipSetDevice(cur);
+  delete e;
+}
+
+int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t stream,
+                       mte_encoder **out) {
+  int st = mte_config_validate(cfg);
+  if (st != MTE_OK) return st;
+  if (!w || !out || (cfg->n_layers > 0 && !w->layers) || !w->final_norm) return MTE_E_INVALID;
+  const mte_config &c = *cfg;
+  for (int l = 0; l < c.n_layers; ++l) {
+    const mte_layer_weights &L = w->layers[l];
+    if (!L.attn_norm || !L.w_q || !L.w_k || !L.w_v || !L.w_o || !L.mlp_norm || !L.w_gate ||
+        !L.w_up || !L.w_down)
+      return MTE_E_INVALID;
+    if (c.qk_norm && (!L.q_norm || !L.k_norm)) return MTE_E_INVALID;
+  }
+  mte_encoder *e = new (std::nothrow) mte_encoder();
+  if (!e) return MTE_E_OOM;
+  e->cfg = c;
+  if (hipGetDevice(&e->device) != hipSuccess) { delete e; return MTE_E_HIP; }
+
+  const size_t es = esize(c.dtype);
+  const size_t D = c.hidden, F = c.ffn, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads;
+  const size_t nqkv = (Hq + 2 * Hkv) * d;
+  const size_t b_qkv = nqkv * D * es, b_o = D * Hq * d * es, b_gu = 2 * F * D * es, b_d = D * F * es;
+  const size_t per_layer = b_qkv + b_o + b_gu + b_d;
+  const size_t g_per_layer = 2 * D + 2 * d;
+  const size_t MT = c.max_tokens;
+
+  auto fail = [&](int code) { mte_encoder_destroy(e); return code; };
+  if (c.n_layers > 0 && hipMalloc(&e->wbuf, per_layer * c.n_layers) != hipSuccess) return fail(MTE_E_OOM);
+  if (hipMalloc((void **)&e->gbuf, (g_per_layer * c.n_layers + D) * sizeof(float)) != hipSuccess)
+    return fail(MTE_E_OOM);
+  e->mode = c.dtype == MTE_BF16 ? MODE_BF16X2 : MODE_F32;
+  e->act_fmt = c.dtype == MTE_BF16 ? FMT_BF16X2 : FMT_F32;
+  if (hipMalloc((void **)&e->h, MT * D * sizeof(float)) != hipSuccess ||
+      hipMalloc(&e->xn, MT * D * 4) != hipSuccess ||
+      hipMalloc((void **)&e->qkv, MT * nqkv * sizeof(float)) != hipSuccess ||
+      hipMalloc(&e->attn, MT * Hq * d * 4) != hipSuccess ||
+      hipMalloc(&e->act, MT * F * 4) != hipSuccess)
+    return fail(MTE_E_OOM);
+
+  // Repack the weights: fused [Wq; Wk; Wv], gate/up interleaved in blocks
+  // of 32 rows, fp32 norm gains.
+  e->layers.resize(c.n_layers);
+  hipError_t he = hipSuccess;
+  for (int l = 0; l < c.n_layers && he == hipSuccess; ++l) {
+    const mte_layer_weights &L = w->layers[l];
+    char *base = (char *)e->wbuf + per_layer * l;
+    LayerW &o = e->layers[l];
+    o.w_qkv = base;
+    o.w_o = base + b_qkv;
+    o.w_gu = base + b_qkv + b_o;
+    o.w_d = base + b_qkv + b_o + b_gu;
+    float *gb = e->gbuf + g_per_layer * l;
+    o.attn_norm = gb;
+    o.mlp_norm = gb + D;
+    o.q_norm = gb + 2 * D;
+    o.k_norm = gb + 2 * D + d;
+    const size_t bq = Hq * d * D * es, bk = Hkv * d * D * es;
+    he = hipMemcpyAsync(o.w_qkv, L.w_q, bq, hipMemcpyDeviceToDevice, stream);
+    if (he == hipSuccess) he = hipMemcpyAsync((char *)o.w_qkv + bq, L.w_k, bk, hipMemcpyDeviceToDevice, stream);
+    if (he == hipSuccess) he = hipMemcpyAsync((char *)o.w_qkv + bq + bk, L.w_v, bk, hipMemcpyDeviceToDevice, stream);
+    if (he == hipSuccess) he = hipMemcpyAsync(o.w_o, L.w_o, b_o, hipMemcpyDeviceToDevice, stream);
+    if (he == hipSuccess) he = hipMemcpyAsync(o.w_d, L.w_down, b_d, hipMemcpyDeviceToDevice, stream);
+    if (he == hipSuccess) he = launch_interleave_gate_up((int)es, L.w_gate, L.w_up, o.w_gu, (int)F, (int)D, stream);
+    if (he == hipSuccess) he = launch_to_f32(in_fmt(c.dtype), L.attn_norm, o.attn_norm, (int)D, stream);
+    if (he == hipSuccess) he = launch_to_f32(in_fmt(c.dtype), L.mlp_norm, o.mlp_norm, (int)D, stream);
+    if (he == hipSuccess && c.qk_norm) he = launch_to_f32(in_fmt(c.dtype), L.q_norm, o.q_norm, (int)d, stream);
+    if (he == hipSuccess && c.qk_norm) he = launch_to_f32(in_fmt(c.dtype), L.k_norm, o.k_norm, (int)d, stream);
+  }
+  e->final_norm = e->gbuf + g_per_layer * c.n_layers;
+  if (he == hipSuccess) he = launch_to_f32(in_fmt(c.dtype), w->final_norm, e->final_norm, (int)D, stream);
+  if (he == hipSuccess) he = hipStreamSynchronize(stream);
+  if (he != hipSuccess) return fail(MTE_E_HIP);
+
+  // Rotary tables: inverse frequencies in float64, pair -> axis.
+  const int half = c.head_dim / 2;
+  for (int j = 0; j < 64; ++j) {
+    e->rope.inv_freq[j] = j < half ? std::pow((double)c.rope_theta, -2.0 * j / c.head_dim) : 0.0;
+    int ax = 0;
+    if (j < half) {
+      if (c.mrope_layout == MTE_MROPE_SECTIONS) {
+        ax = j < c.mrope_section[0] ? 0 : (j < c.mrope_section[0] + c.mrope_section[1] ? 1 : 2);
+      } else {
+        if (j % 3 == 1 && j < 3 * c.mrope_section[1]) ax = 1;
+        else if (j % 3 == 2 && j < 3 * c.mrope_section[2]) ax = 2;
+      }
+    }
+    e->rope.axis[j] = (uint8_t)ax;
+  }
+  *out = e;
+  return MTE_OK;
+}
+
+}  // extern "C"
+
+namespace {
+
+struct Timer {
+  mte_encoder *e;
+  hipStream_t s;
+  bool on;
+  Timer(mte_encoder *e_, int cls, hipStream_t s_) : e(e_), s(s_) {
+    on = e->timing_class == cls && e->ev_used < e->ev_cap;
+    if (on) hipEventRecord(e->ev[2 * e->ev_used], s);
+  }
+  ~Timer() {
+    if (on) {
+      hipEventRecord(e->ev[2 * e->ev_used + 1], s);
+      e->ev_used++;
+    }
+  }
+};
+
+// Second plane of a bf16x2 activation buffer with `cols` columns.
+void *lo_plane(const mte_encoder *e, void *buf, size_t cols) {
+  return e->mode == MODE_BF16X2 ? (void *)((bf16_storage *)buf + (size_t)e->cfg.max_tokens * cols) : nullptr;
+}
+
+// Runs layers [l0, l1) on the fp32 residual stream `h` (T rows).
+hipError_t run_layers(mte_encoder *e, float *h, const int32_t *pos, const std::vector<int32_t> &cu,
+                      int batch, int T, int l0, int l1, bool first_norm_done, hipStream_t s) {
+  const mte_config &c = e->cfg;
+  const int D = c.hidden, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
+  const int nqkv = (Hq + 2 * Hkv) * d;
+  const size_t MT = c.max_tokens;
+  const int mode = e->mode, af = e->act_fmt;
+  void *xn_lo = lo_plane(e, e->xn, D), *attn_lo = lo_plane(e, e->attn, (size_t)Hq * d),
+       *act_lo = lo_plane(e, e->act, F);
+  hipError_t err = hipSuccess;
+#define MTE_TRY(x) do { err = (x); if (err != hipSuccess) return err; } while (0)
+  for (int l = l0; l < l1; ++l) {
+    const LayerW &W = e->layers[l];
+    if (!(l == l0 && first_norm_done))
+      MTE_TRY(launch_rmsnorm(FMT_F32, af, h, nullptr, W.attn_norm, e->xn, MT * D, T, D, c.rms_eps, s));
+    {
+      Timer t(e, 0, s);
+      MTE_TRY(launch_gemm(mode, EPI_STORE, e->xn, xn_lo, W.w_qkv, e->qkv, 0, T, nqkv, D, nqkv, s));
+    }
+    MTE_TRY(launch_qk_rope(e->qkv, pos, c.qk_norm ? W.q_norm : nullptr, W.k_norm, T, Hq, Hkv, d,
+                           c.rms_eps, e->rope, s));
+    {
+      Timer t(e, 1, s);
+      MTE_TRY(launch_attention(mode, e->qkv, e->attn, MT * Hq * d, cu.data(), batch, Hq, Hkv, d, s));
+    }
+    {
+      Timer t(e, 2, s);
+      MTE_TRY(launch_gemm(mode, EPI_RESID, e->attn, attn_lo, W.w_o, h, 0, T, D, Hq * d, D, s));
+    }
+    MTE_TRY(launch_rmsnorm(FMT_F32, af, h, nullptr, W.mlp_norm, e->xn, MT * D, T, D, c.rms_eps, s));
+    {
+      Timer t(e, 3, s);
+      MTE_TRY(launch_gemm(mode, EPI_SWIGLU, e->xn, xn_lo, W.w_gu, e->act, MT * F, T, 2 * F, D, F, s));
+    }
+    {
+      Timer t(e, 4, s);
+      MTE_TRY(launch_gemm(mode, EPI_RESID, e->act, act_lo, W.w_d, h, 0, T, D, F, D, s));
+    }
+  }
+#undef MTE_TRY
+  return err;
+}
+
+struct DeviceGuard {
+  int prev = -1;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&prev) == hipSuccess && prev != dev) hipSetDevice(dev);
+    else prev = -1;
+  }
+  ~DeviceGuard() {
+    if (prev >= 0) hipSetDevice(prev);
+  }
+};
+
+}  // namespace
+
+extern "C" {
+
+int mte_encode(mte_encoder *e, const void *embeds, const int32_t *pos_thw, const int32_t *seq_lens,
+               int32_t batch, void *out_hidden, hipStream_t stream) {
+  if (!e || !embeds || !pos_thw || !out_hidden) return MTE_E_INVALID;
+  int32_t T = 0;
+  int st = mte_check_batch(&e->cfg, seq_lens, batch, &T);
+  if (st != MTE_OK) return st;
+  const mte_config &c = e->cfg;
+  const size_t in_bytes = (size_t)T * c.hidden * esize(c.dtype);
+  const size_t out_bytes = (size_t)T * c.hidden * esize(c.out_dtype);
+  const char *ib = (const char *)embeds, *ob = (const char *)out_hidden;
+  if (ib < ob + out_bytes && ob < ib + in_bytes) return MTE_E_INVALID;
+  std::vector<int32_t> cu(batch + 1, 0);
+  for (int i = 0; i < batch; ++i) cu[i + 1] = cu[i] + seq_lens[i];
+  DeviceGuard g(e->device);
+  hipError_t err;
+  const int out_fmt = in_fmt(c.out_dtype);
+  if (c.n_layers == 0) {
+    err = launch_rmsnorm(in_fmt(c.dtype), out_fmt, embeds, nullptr, e->final_norm, out_hidden, 0, T,
+                         c.hidden, c.rms_eps, stream);
+    return err == hipSuccess ? MTE_OK : MTE_E_HIP;
+  }
+  // Layer 0's attention norm also seeds the fp32 residual stream from the embeddings.
+  err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, embeds, e->h, e->layers[0].attn_norm, e->xn,
+                       (size_t)c.max_tokens * c.hidden, T, c.hidden, c.rms_eps, stream);
+  if (err == hipSuccess) err = run_layers(e, e->h, pos_thw, cu, batch, T, 0, c.n_layers, true, stream);
+  if (err == hipSuccess)
+    err = launch_rmsnorm(FMT_F32, out_fmt, e->h, nullptr, e->final_norm, out_hidden, 0, T, c.hidden,
+                         c.rms_eps, stream);
+  return err == hipSuccess ? MTE_OK : MTE_E_HIP;
+}
+
+int mte_encode_layers(mte_encoder *e, const float *h_in, const int32_t *pos_thw,
+                      const int32_t *seq_lens, int32_t batch, int32_t layer_begin, int32_t layer_end,
+                      float *h_out, hipStream_t stream) {
+  if (!e || !h_in || !pos_thw || !h_out) return MTE_E_INVALID;
+  int32_t T = 0;
+  int st = mte_check_batch(&e->cfg, seq_lens, batch, &T);
+  if (st != MTE_OK) return st;
+  if (layer_begin < 0 || layer_end < layer_begin || layer_end > e->cfg.n_layers) return MTE_E_INVALID;
+  const size_t bytes = (size_t)T * e->cfg.hidden * sizeof(float);
+  const char *ib = (const char *)h_in, *ob = (const char *)h_out;
+  if (ib != ob && ib < ob + bytes && ob < ib + bytes) return MTE_E_INVALID;
+  std::vector<int32_t> cu(batch + 1, 0);
+  for (int i = 0; i < batch; ++i) cu[i + 1] = cu[i] + seq_lens[i];
+  DeviceGuard g(e->device);
+  hipError_t err = hipSuccess;
+  if (h_out != h_in) err = hipMemcpyAsync(h_out, h_in, bytes, hipMemcpyDeviceToDevice, stream);
+  if (err == hipSuccess)
+    err = run_layers(e, h_out, pos_thw, cu, batch, T, layer_begin, layer_end, false, stream);
+  return err == hipSuccess ? MTE_OK : MTE_E_HIP;
+}
+
+int mte_timing_enable(mte_encoder *e, int32_t kernel_class, int32_t capacity) {
+  if (!e || kernel_class < 0 || kernel_class >= kNumClasses || capacity <= 0) return MTE_E_INVALID;
+  DeviceGuard g(e->device);
+  while ((int)e->ev.size() < 2 * capacity) {
+    hipEvent_t ev;
+    if (hipEventCreate(&ev) != hipSuccess) return MTE_E_HIP;
+    e->ev.push_back(ev);
+  }
+  e->ev_cap = capacity;
+  e->ev_used = 0;
+  e->timing_class = kernel_class;
+  return MTE_OK;
+}
+
+int mte_timing_read(mte_encoder *e, int32_t *launches, double *total_ms) {
+  if (!e || !launches || !total_ms) return MTE_E_INVALID;
+  DeviceGuard g(e->device);
+  double tot = 0.0;
+  for (int i = 0; i < e->ev_used; ++i) {
+    if (hipEventSynchronize(e->ev[2 * i + 1]) != hipSuccess) return MTE_E_HIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, e->ev[2 * i], e->ev[2 * i + 1]) != hipSuccess) return MTE_E_HIP;
+    tot += ms;
+  }
+  *launches = e->ev_used;
+  *total_ms = tot;
+  e->ev_used = 0;
+  return MTE_OK;
+}
+
+int mte_timing_disable(mte_encoder *e) {
+  if (!e) return MTE_E_INVALID;
+  e->timing_class = -1;
+  e->ev_used = 0;
+  return MTE_OK;
+}
+
+}  // extern "C"

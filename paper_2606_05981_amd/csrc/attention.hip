@@ -1,0 +1,313 @@
+// Causal grouped-query attention over packed, ragged sequences (prefill).
+//
+// For every sequence, query head h and token i:
+//   o[i, h] = sum_{j <= i} softmax_j(q_i . k_j / sqrt(d)) v_j,
+// with k, v taken from kv head h / (Hq / Hkv) and j ranging over the same
+// sequence only.
+//
+// One workgroup (4 waves) serves one kv head, one tile of query rows of one
+// sequence and the query heads of that kv head assigned to it; every wave
+// owns 32 query rows of one query head. Key/value tiles of 32 tokens are
+// staged in LDS once and shared by all four waves (K row-major, V
+// transposed). Per wave and kv tile:
+//   S^T = K Q^T   (32x32 MFMA; lane l ends up owning query l%32)
+//   online softmax in fp32 over the lane's 16 scores plus one cross-lane
+//   exchange (lane ^ 32)
+//   O^T += V^T P^T  (32x32 MFMA; again query l%32 per lane, so the
+//   rescaling of O by the running-max correction is a per-lane scalar).
+//
+// q, k, v arrive in fp32. MODE_F32 multiplies them on the fp32 matrix
+// cores. MODE_BF16X2 splits every operand x into bf16 hi + lo
+// (lo = bf16(x - hi)) and forms each product from three bf16 MFMAs,
+// hi*hi + lo*hi + hi*lo (the lo*lo term is below fp32 accumulation noise).
+// The sequence table (offsets, first tile of each sequence) is passed by
+// value in the kernel arguments, so nothing is read back to the host.
+#include <type_traits>
+
+#include "common.h"
+#include "launch.h"
+
+namespace mte {
+
+constexpr int kMaxSeqPerLaunch = 256;
+
+struct AttnArgs {
+  const float *qkv;
+  char *o;
+  size_t o_plane;  // elements between the hi and lo planes of o (MODE_BF16X2)
+  int ld_qkv;      // floats per token row of qkv
+  int Hq, Hkv, rep;
+  int wph;         // waves per query head (query rows per workgroup = 32 * wph)
+  int hpb;         // query heads per workgroup
+  int head_blocks;
+  int n_seq;
+  int cu[kMaxSeqPerLaunch + 1];     // absolute token offsets
+  int tile0[kMaxSeqPerLaunch + 1];  // first workgroup tile of each sequence
+};
+
+template <int NCH>
+__device__ __forceinline__ int kswz(int r, int c) {
+  if constexpr (NCH >= 16) return c ^ (r & 15);
+  else return c ^ ((r ^ (r >> 3)) & 7);
+}
+
+// Splits EC fp32 values into NP planes of element type T (NP = 1: plain).
+template <typename T, int NP, int EC>
+__device__ __forceinline__ void split_vals(const float *x, T (&out)[NP][EC]) {
+#pragma unroll
+  for (int e = 0; e < EC; ++e) {
+    T hi = from_f32<T>(x[e]);
+    out[0][e] = hi;
+    if constexpr (NP == 2) out[1][e] = from_f32<T>(x[e] - to_f32(hi));
+  }
+}
+
+template <int MODE, int HD>
+__global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
+  typedef typename std::conditional<MODE == MODE_F32, float, bf16>::type T;
+  constexpr int NP = (MODE == MODE_BF16X2) ? 2 : 1;   // planes per operand
+  constexpr int KV = 32;
+  constexpr int EC = 16 / (int)sizeof(T);        // elements per 16-byte chunk
+  constexpr int NCH = HD / EC;                   // chunks per head row
+  constexpr int EPF = Frag<T>::kElems;           // values per fragment (== EC)
+  constexpr int NFP = 16 / EPF;                  // P fragments per 32-kv tile
+  constexpr int VTP = KV + 4;                    // padded V^T row (elements)
+  constexpr int ND = HD / 32;                    // 32-wide d blocks
+  typedef typename Frag<T>::type frag_t;
+
+  __shared__ u32x4 sK[NP][KV * NCH];
+  __shared__ T sVt[NP][HD * VTP];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int lrow = lane & 31, lgrp = lane >> 5;
+
+  // Which sequence / query tile / heads this workgroup serves.
+  const int tile = blockIdx.x;
+  int lo = 0, hi = a.n_seq - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (a.tile0[mid] <= tile) lo = mid; else hi = mid - 1;
+  }
+  const int seq = lo;
+  const int s0 = a.cu[seq], L = a.cu[seq + 1] - s0;
+  const int QT = 32 * a.wph;
+  const int q0 = (tile - a.tile0[seq]) * QT;
+  const int g = blockIdx.y / a.head_blocks, hb = blockIdx.y % a.head_blocks;
+  const int head = g * a.rep + hb * a.hpb + wave / a.wph;
+  const int qw = q0 + (wave % a.wph) * 32;         // first query row of this wave
+  const int q_last = min(q0 + QT, L) - 1;          // last valid query row of the workgroup
+  const int wave_last = min(qw + 31, L - 1);       // last valid query row of this wave
+  const size_t ld = (size_t)a.ld_qkv;
+  const float *base = a.qkv + (size_t)s0 * ld;
+  const int k_off = (a.Hq + g) * HD;
+  const int v_off = (a.Hq + a.Hkv + g) * HD;
+
+  // Q fragments of this wave's 32 rows (B operand of S^T = K Q^T).
+  frag_t qf[NP][NCH / 2];
+  {
+    const int qi = qw + lrow;
+    const float *qp = base + (size_t)qi * ld + head * HD;
+#pragma unroll
+    for (int kk = 0; kk < NCH / 2; ++kk) {
+      float x[EC];
+#pragma unroll
+      for (int e = 0; e < EC; ++e) x[e] = 0.f;
+      if (qi < L) {
+#pragma unroll
+        for (int e = 0; e < EC; e += 4) {
+          f32x4 v = *(const f32x4 *)(qp + (kk * 2 + lgrp) * EC + e);
+          x[e] = v[0]; x[e + 1] = v[1]; x[e + 2] = v[2]; x[e + 3] = v[3];
+        }
+      }
+      T sp[NP][EC];
+      split_vals<T, NP, EC>(x, sp);
+#pragma unroll
+      for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int e = 0; e < EC; ++e) qf[p][kk][e] = sp[p][e];
+    }
+  }
+  // Scores are kept in log2 units: s * log2(e) / sqrt(d).
+  const float sc = 1.4426950408889634f * rsqrtf((float)HD);
+
+  f32x16 oacc[ND];
+#pragma unroll
+  for (int n = 0; n < ND; ++n)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[n][r] = 0.f;
+  float m_i = -INFINITY, l_i = 0.f;
+  const int my_q = qw + lrow;
+
+  const int n_blocks = (q_last >= 0) ? (q_last / KV + 1) : 0;
+  for (int kb = 0; kb < n_blocks; ++kb) {
+    const int kv0 = kb * KV;
+    // Stage K (row-major, swizzled) and V (transposed) of tokens kv0..kv0+31.
+    for (int idx = tid; idx < KV * NCH; idx += 256) {
+      const int r = idx / NCH, c = idx % NCH;
+      float kx[EC], vx[EC];
+#pragma unroll
+      for (int e = 0; e < EC; ++e) kx[e] = vx[e] = 0.f;
+      if (kv0 + r < L) {
+        const float *rp = base + (size_t)(kv0 + r) * ld;
+#pragma unroll
+        for (int e = 0; e < EC; e += 4) {
+          f32x4 kv = *(const f32x4 *)(rp + k_off + c * EC + e);
+          f32x4 vv = *(const f32x4 *)(rp + v_off + c * EC + e);
+          kx[e] = kv[0]; kx[e + 1] = kv[1]; kx[e + 2] = kv[2]; kx[e + 3] = kv[3];
+          vx[e] = vv[0]; vx[e + 1] = vv[1]; vx[e + 2] = vv[2]; vx[e + 3] = vv[3];
+        }
+      }
+      T ks[NP][EC], vs[NP][EC];
+      split_vals<T, NP, EC>(kx, ks);
+      split_vals<T, NP, EC>(vx, vs);
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+        u32x4 w;
+        __builtin_memcpy(&w, ks[p], 16);
+        sK[p][r * NCH + kswz<NCH>(r, c)] = w;
+#pragma unroll
+        for (int e = 0; e < EC; ++e) sVt[p][(c * EC + e) * VTP + r] = vs[p][e];
+      }
+    }
+    __syncthreads();
+
+    if (qw < L && kv0 <= wave_last) {
+      f32x16 s;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[r] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < NCH / 2; ++kk) {
+        const int slot = lrow * NCH + kswz<NCH>(lrow, kk * 2 + lgrp);
+        const frag_t k0 = __builtin_bit_cast(frag_t, sK[0][slot]);
+        mfma32(s, k0, qf[0][kk]);
+        if constexpr (NP == 2) {
+          const frag_t k1 = __builtin_bit_cast(frag_t, sK[1][slot]);
+          mfma32(s, k1, qf[0][kk]);
+          mfma32(s, k0, qf[1][kk]);
+        }
+      }
+      float mb = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int kv = kv0 + acc_row(r, lane);
+        s[r] = (kv <= my_q && kv < L) ? s[r] * sc : -INFINITY;
+        mb = fmaxf(mb, s[r]);
+      }
+      mb = warp_max_xor(mb, 32);
+      const float m_new = fmaxf(m_i, mb);
+      const float alpha = exp2f(m_i - m_new);
+      m_i = m_new;
+      float p[16];
+      float ps = 0.f;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        p[r] = exp2f(s[r] - m_new);
+        ps += p[r];
+      }
+      l_i = l_i * alpha + ps;
+#pragma unroll
+      for (int n = 0; n < ND; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[n][r] *= alpha;
+      // P fragments: element e of fragment f is P value i = EPF*f + e, which
+      // belongs to key row 8*(i/4) + 4*lgrp + i%4 of this tile.
+      frag_t pf[NP][NFP];
+#pragma unroll
+      for (int f = 0; f < NFP; ++f) {
+        T sp[NP][EPF];
+        split_vals<T, NP, EPF>(p + EPF * f, sp);
+#pragma unroll
+        for (int q = 0; q < NP; ++q)
+#pragma unroll
+          for (int e = 0; e < EPF; ++e) pf[q][f][e] = sp[q][e];
+      }
+#pragma unroll
+      for (int n = 0; n < ND; ++n) {
+#pragma unroll
+        for (int f = 0; f < NFP; ++f) {
+          frag_t vf[NP];
+#pragma unroll
+          for (int q = 0; q < NP; ++q) {
+            const T *vrow = sVt[q] + (n * 32 + lrow) * VTP + 4 * lgrp;
+#pragma unroll
+            for (int e = 0; e < EPF; ++e) {
+              const int i = EPF * f + e;
+              vf[q][e] = vrow[8 * (i >> 2) + (i & 3)];
+            }
+          }
+          mfma32(oacc[n], vf[0], pf[0][f]);
+          if constexpr (NP == 2) {
+            mfma32(oacc[n], vf[1], pf[0][f]);
+            mfma32(oacc[n], vf[0], pf[1][f]);
+          }
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  if (qw < L) {
+    const float lt = l_i + __shfl_xor(l_i, 32, kWave);
+    const float inv = 1.f / lt;
+    if (my_q < L) {
+      const size_t ob = ((size_t)(s0 + my_q) * a.Hq + head) * HD;
+#pragma unroll
+      for (int n = 0; n < ND; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float y = oacc[n][r] * inv;
+          const size_t o = ob + n * 32 + acc_row(r, lane);
+          if constexpr (MODE == MODE_F32) {
+            ((float *)a.o)[o] = y;
+          } else {
+            const bf16 h = (bf16)y;
+            ((bf16 *)a.o)[o] = h;
+            ((bf16 *)a.o)[o + a.o_plane] = (bf16)(y - (float)h);
+          }
+        }
+    }
+  }
+}
+
+hipError_t launch_attention(int mode, const float *qkv, void *o, size_t o_plane, const int32_t *cu,
+                            int batch, int Hq, int Hkv, int d, hipStream_t s) {
+  const int rep = Hq / Hkv;
+  AttnArgs a;
+  a.qkv = qkv;
+  a.o = (char *)o;
+  a.o_plane = o_plane;
+  a.ld_qkv = (Hq + 2 * Hkv) * d;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.rep = rep;
+  if (rep >= 4) { a.wph = 1; a.hpb = 4; a.head_blocks = rep / 4; }
+  else { a.wph = 4 / rep; a.hpb = rep; a.head_blocks = 1; }
+  const int QT = 32 * a.wph;
+  for (int first = 0; first < batch; first += kMaxSeqPerLaunch) {
+    const int n = batch - first < kMaxSeqPerLaunch ? batch - first : kMaxSeqPerLaunch;
+    a.n_seq = n;
+    int tiles = 0;
+    for (int i = 0; i < n; ++i) {
+      a.cu[i] = cu[first + i];
+      a.tile0[i] = tiles;
+      const int L = cu[first + i + 1] - cu[first + i];
+      tiles += (L + QT - 1) / QT;
+    }
+    a.cu[n] = cu[first + n];
+    a.tile0[n] = tiles;
+    if (tiles == 0) continue;
+    dim3 grid(tiles, Hkv * a.head_blocks);
+    if (mode == MODE_BF16X2) {
+      if (d == 128) hipLaunchKernelGGL((k_attn<MODE_BF16X2, 128>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_attn<MODE_BF16X2, 64>), grid, dim3(256), 0, s, a);
+    } else {
+      if (d == 128) hipLaunchKernelGGL((k_attn<MODE_F32, 128>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_attn<MODE_F32, 64>), grid, dim3(256), 0, s, a);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace mte

@@ -1,0 +1,74 @@
+// Host-side launchers of the encoder kernels (internal to libmte).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace mte {
+
+// Arithmetic of the matrix-core steps.
+enum Mode {
+  MODE_F32 = 0,     // fp32 weights and activations, fp32 MFMA
+  MODE_BF16X2 = 1,  // bf16 weights; activations as bf16 hi + lo planes, bf16 MFMA
+};
+
+// Storage formats of activation buffers.
+enum Fmt {
+  FMT_F32 = 0,
+  FMT_BF16 = 1,
+  FMT_BF16X2 = 2,   // two bf16 planes [rows, cols]: hi, and lo = bf16(x - hi) at +plane elements
+};
+
+enum Epilogue {
+  EPI_STORE = 0,   // C (float) [m, n] = acc
+  EPI_SWIGLU = 1,  // gate/up rows interleaved in blocks of 32: C[m, f] = silu(gate) * up,
+                   // written as float (MODE_F32) or bf16 hi/lo planes (MODE_BF16X2)
+  EPI_RESID = 2,   // C (float residual stream) [m, n] += acc
+};
+
+// C = A[M, K] * W[N, K]^T. MODE_F32: A, W float. MODE_BF16X2: A = A_hi + A_lo
+// (bf16 planes), W bf16. ldc: C's row pitch in elements; c_plane: distance
+// in elements between the hi and lo planes of a bf16x2 C.
+hipError_t launch_gemm(int mode, int epi, const void *A, const void *A_lo, const void *W, void *C,
+                       size_t c_plane, int M, int N, int K, int ldc, hipStream_t s);
+
+// Per-row RMSNorm: out[r, :] = in[r, :] / sqrt(mean(in[r,:]^2) + eps) * g.
+// in: `in_fmt` (FMT_F32 or FMT_BF16) [rows, D]; when copy_to != nullptr the
+// input row is also written to copy_to as float (seeds the fp32 residual
+// stream from the embeddings). g: float [D]. out: `out_fmt`, lo plane at
+// out + out_plane elements for FMT_BF16X2.
+hipError_t launch_rmsnorm(int in_fmt, int out_fmt, const void *in, float *copy_to, const float *g,
+                          void *out, size_t out_plane, int rows, int D, float eps, hipStream_t s);
+
+struct RopeParams {
+  double inv_freq[64];       // theta^(-2j/d) for pair j
+  uint8_t axis[64];          // position axis (0 t, 1 h, 2 w) of pair j
+};
+
+// In-place per-head RMSNorm (when q_norm != nullptr) and multimodal rotary
+// embedding of the q and k heads of a packed fp32 qkv buffer [T, (Hq+2Hkv)*d].
+hipError_t launch_qk_rope(float *qkv, const int32_t *pos_thw, const float *q_norm,
+                          const float *k_norm, int T, int Hq, int Hkv, int d, float eps,
+                          const RopeParams &rp, hipStream_t s);
+
+// Causal GQA attention over packed sequences. qkv: fp32 [T, (Hq+2Hkv)*d], q
+// heads first, then k, then v; o: [T, Hq*d] as float (MODE_F32) or bf16
+// hi/lo planes o_plane elements apart (MODE_BF16X2). cu: host
+// int32[batch+1] sequence offsets. Launches in chunks of <= 256 sequences.
+hipError_t launch_attention(int mode, const float *qkv, void *o, size_t o_plane, const int32_t *cu,
+                            int batch, int Hq, int Hkv, int d, hipStream_t s);
+
+// Positions of packed sequences (see mte_build_positions).
+hipError_t launch_positions(const int32_t *layouts5, int batch, int32_t *pos_thw, int T,
+                            hipStream_t s);
+
+// dst[i] = (float) src[i] for n elements of storage format src_fmt (FMT_F32 / FMT_BF16).
+hipError_t launch_to_f32(int src_fmt, const void *src, float *dst, int n, hipStream_t s);
+
+// Packs gate [F, D] and up [F, D] (element size esize bytes) into dst [2F, D]:
+// block b of 64 rows holds gate rows 32b..32b+31 then up rows 32b..32b+31.
+hipError_t launch_interleave_gate_up(int esize, const void *gate, const void *up, void *dst,
+                                     int F, int D, hipStream_t s);
+
+}  // namespace mte

@@ -1,0 +1,219 @@
+// Row-wise kernels of the encoder: RMSNorm, per-head QK-norm + multimodal
+// rotary embedding, on-device position ids, and the weight repacking used
+// at encoder creation.
+#include "common.h"
+#include "launch.h"
+
+namespace mte {
+
+// ------------------------------------------------------------- RMSNorm
+// out = x / sqrt(mean(x^2) + eps) * g, one 256-thread block per row.
+// OUT_FMT FMT_BF16X2 writes bf16 hi to out and bf16(y - hi) to out + plane.
+template <typename TI, int OUT_FMT>
+__global__ __launch_bounds__(256) void k_rmsnorm(const TI *__restrict__ in, float *__restrict__ copy_to,
+                                                 const float *__restrict__ gain, void *__restrict__ out,
+                                                 size_t plane, int D, float eps) {
+  __shared__ float red[4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const TI *x = in + (size_t)row * D;
+  float ss = 0.f;
+  for (int c = tid; c < D; c += 256) {
+    float v = to_f32(x[c]);
+    ss += v * v;
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) ss = warp_sum_xor(ss, m);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  const float rs = rsqrtf((red[0] + red[1] + red[2] + red[3]) / (float)D + eps);
+  for (int c = tid; c < D; c += 256) {
+    const float v = to_f32(x[c]);
+    const size_t o = (size_t)row * D + c;
+    if (copy_to) copy_to[o] = v;
+    const float y = v * rs * gain[c];
+    if constexpr (OUT_FMT == FMT_F32) {
+      ((float *)out)[o] = y;
+    } else if constexpr (OUT_FMT == FMT_BF16) {
+      ((bf16 *)out)[o] = (bf16)y;
+    } else {
+      const bf16 h = (bf16)y;
+      ((bf16 *)out)[o] = h;
+      ((bf16 *)out)[o + plane] = (bf16)(y - (float)h);
+    }
+  }
+}
+
+template <typename TI>
+static void rmsnorm_out(int out_fmt, dim3 grid, const TI *in, float *copy_to, const float *g, void *out,
+                        size_t plane, int D, float eps, hipStream_t s) {
+  if (out_fmt == FMT_F32)
+    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_F32>), grid, dim3(256), 0, s, in, copy_to, g, out, plane, D, eps);
+  else if (out_fmt == FMT_BF16)
+    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_BF16>), grid, dim3(256), 0, s, in, copy_to, g, out, plane, D, eps);
+  else
+    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_BF16X2>), grid, dim3(256), 0, s, in, copy_to, g, out, plane, D, eps);
+}
+
+hipError_t launch_rmsnorm(int in_fmt, int out_fmt, const void *in, float *copy_to, const float *g,
+                          void *out, size_t out_plane, int rows, int D, float eps, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  dim3 grid(rows);
+  if (in_fmt == FMT_BF16)
+    rmsnorm_out<bf16>(out_fmt, grid, (const bf16 *)in, copy_to, g, out, out_plane, D, eps, s);
+  else
+    rmsnorm_out<float>(out_fmt, grid, (const float *)in, copy_to, g, out, out_plane, D, eps, s);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------- QK-norm + M-RoPE
+// One block per token. The token's d/2 rotation angles are computed once
+// (float64 angle and sincos, rounded to fp32) and shared by its Hq + Hkv
+// query and key heads. Thread j of a head owns rotary pair (j, j + d/2);
+// a head's d/2 threads sit in one wave, so the per-head sum of squares of
+// the QK-norm is a butterfly over those lanes.
+__global__ __launch_bounds__(256) void k_qk_rope(float *__restrict__ qkv, const int32_t *__restrict__ pos,
+                                                 const float *__restrict__ qn, const float *__restrict__ kn,
+                                                 int T_tokens, int Hq, int Hkv, int d, float eps,
+                                                 RopeParams rp) {
+  __shared__ float cs[64], sn[64];
+  const int tok = blockIdx.x, tid = threadIdx.x;
+  const int half = d >> 1;
+  if (tid < half) {
+    const int ax = rp.axis[tid];
+    const double ang = (double)pos[(size_t)ax * T_tokens + tok] * rp.inv_freq[tid];
+    double sv, cv;
+    sincos(ang, &sv, &cv);
+    cs[tid] = (float)cv;
+    sn[tid] = (float)sv;
+  }
+  __syncthreads();
+  const int nh = Hq + Hkv;
+  float *row = qkv + (size_t)tok * (Hq + 2 * Hkv) * d;
+  for (int t = tid; t < nh * half; t += 256) {
+    const int h = t / half, j = t % half;
+    float *z = row + h * d;
+    float u = z[j], w = z[j + half];
+    if (qn) {
+      const float *gn = (h < Hq) ? qn : kn;
+      float ss = u * u + w * w;
+      for (int m = half >> 1; m >= 1; m >>= 1) ss = warp_sum_xor(ss, m);
+      const float rs = rsqrtf(ss / (float)d + eps);
+      u = u * rs * gn[j];
+      w = w * rs * gn[j + half];
+    }
+    const float c = cs[j], s = sn[j];
+    z[j] = u * c - w * s;
+    z[j + half] = w * c + u * s;
+  }
+}
+
+hipError_t launch_qk_rope(float *qkv, const int32_t *pos_thw, const float *q_norm,
+                          const float *k_norm, int T, int Hq, int Hkv, int d, float eps,
+                          const RopeParams &rp, hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_qk_rope, dim3(T), dim3(256), 0, s, qkv, pos_thw, q_norm, k_norm, T, Hq, Hkv,
+                     d, eps, rp);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------ positions
+constexpr int kPosSeqPerLaunch = 128;
+
+struct PosArgs {
+  int n_seq;
+  int start[kPosSeqPerLaunch + 1];   // absolute token offsets
+  int nb[kPosSeqPerLaunch];          // text tokens before the image
+  int gt[kPosSeqPerLaunch], gh[kPosSeqPerLaunch], gw[kPosSeqPerLaunch];
+};
+
+__global__ __launch_bounds__(256) void k_positions(int32_t *__restrict__ pos, int T_tokens, PosArgs a) {
+  const int tk = a.start[0] + blockIdx.x * 256 + threadIdx.x;
+  if (tk >= a.start[a.n_seq]) return;
+  int lo = 0, hi = a.n_seq - 1;
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (a.start[mid] <= tk) lo = mid; else hi = mid - 1;
+  }
+  const int i = tk - a.start[lo];
+  const int nb = a.nb[lo], gt = a.gt[lo], gh = a.gh[lo], gw = a.gw[lo];
+  const int plane = gh * gw, nimg = gt * plane;
+  int t, h, w;
+  if (i < nb) {
+    t = h = w = i;
+  } else if (i < nb + nimg) {
+    const int k = i - nb;
+    t = nb + k / plane;
+    h = nb + (k / gw) % gh;
+    w = nb + k % gw;
+  } else {
+    // one past the largest position used so far
+    int mx = nb - 1;
+    if (nimg > 0) mx = nb + max(gt - 1, max(gh - 1, gw - 1));
+    t = h = w = mx + 1 + (i - nb - nimg);
+  }
+  pos[tk] = t;
+  pos[(size_t)T_tokens + tk] = h;
+  pos[2 * (size_t)T_tokens + tk] = w;
+}
+
+hipError_t launch_positions(const int32_t *layouts5, int batch, int32_t *pos_thw, int T,
+                            hipStream_t s) {
+  int tok = 0;
+  for (int first = 0; first < batch; first += kPosSeqPerLaunch) {
+    const int n = batch - first < kPosSeqPerLaunch ? batch - first : kPosSeqPerLaunch;
+    PosArgs a;
+    a.n_seq = n;
+    a.start[0] = tok;
+    for (int i = 0; i < n; ++i) {
+      const int32_t *l = layouts5 + 5 * (first + i);
+      a.nb[i] = l[0];
+      a.gt[i] = l[1];
+      a.gh[i] = l[2];
+      a.gw[i] = l[3];
+      tok += l[0] + l[1] * l[2] * l[3] + l[4];
+      a.start[i + 1] = tok;
+    }
+    const int cnt = a.start[n] - a.start[0];
+    if (cnt > 0) {
+      hipLaunchKernelGGL(k_positions, dim3((cnt + 255) / 256), dim3(256), 0, s, pos_thw, T, a);
+      hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+  }
+  return hipSuccess;
+}
+
+// ------------------------------------------------------ weight repacking
+template <typename T>
+__global__ void k_to_f32(const T *__restrict__ src, float *__restrict__ dst, int n) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i < n) dst[i] = to_f32(src[i]);
+}
+
+hipError_t launch_to_f32(int src_fmt, const void *src, float *dst, int n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  dim3 grid((n + 255) / 256);
+  if (src_fmt == FMT_BF16) hipLaunchKernelGGL(k_to_f32<bf16>, grid, dim3(256), 0, s, (const bf16 *)src, dst, n);
+  else hipLaunchKernelGGL(k_to_f32<float>, grid, dim3(256), 0, s, (const float *)src, dst, n);
+  return hipGetLastError();
+}
+
+// dst row r (of 2F): block b = r / 64 holds gate rows 32b.. then up rows 32b..
+__global__ void k_interleave(const char *__restrict__ gate, const char *__restrict__ up,
+                             char *__restrict__ dst, int row_bytes) {
+  const int r = blockIdx.x, b = r >> 6, w = r & 63;
+  const char *src = (w < 32 ? gate : up) + (size_t)(32 * b + (w & 31)) * row_bytes;
+  char *d = dst + (size_t)r * row_bytes;
+  for (int c = threadIdx.x * 16; c < row_bytes; c += 256 * 16)
+    *(u32x4 *)(d + c) = *(const u32x4 *)(src + c);
+}
+
+hipError_t launch_interleave_gate_up(int esize, const void *gate, const void *up, void *dst,
+                                     int F, int D, hipStream_t s) {
+  const int row_bytes = D * esize;
+  hipLaunchKernelGGL(k_interleave, dim3(2 * F), dim3(256), 0, s, (const char *)gate,
+                     (const char *)up, (char *)dst, row_bytes);
+  return hipGetLastError();
+}
+
+}  // namespace mte

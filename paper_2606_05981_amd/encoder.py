@@ -1,0 +1,100 @@
+"""Torch-facing wrapper of the C ABI: tensors in, tensors out.
+
+PyTorch only provides device memory and streams here; every step of the
+encoder runs in libmte's HIP kernels. Nothing falls back to another
+implementation: a missing library raises at import, a failing call raises
+MteError.
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Optional, Sequence
+
+import torch
+
+from . import binding as B
+
+WEIGHT_KEYS = ("attn_norm", "w_q", "w_k", "w_v", "q_norm", "k_norm", "w_o", "mlp_norm",
+               "w_gate", "w_up", "w_down")
+TORCH_DTYPE = {B.MTE_F32: torch.float32, B.MTE_BF16: torch.bfloat16}
+
+
+def _stream(stream: Optional[torch.cuda.Stream]) -> int:
+    return (stream or torch.cuda.current_stream()).cuda_stream
+
+
+class TextEncoder:
+    """Owns one mte_encoder. Weights are copied into the library at creation."""
+
+    def __init__(self, cfg: B.mte_config, layers: Sequence[Dict[str, torch.Tensor]],
+                 final_norm: torch.Tensor, stream: Optional[torch.cuda.Stream] = None):
+        self.cfg = cfg
+        self.dtype = TORCH_DTYPE[cfg.dtype]
+        self.out_dtype = TORCH_DTYPE[cfg.out_dtype]
+        for L in layers:
+            for k, t in L.items():
+                if t is not None and (t.dtype != self.dtype or not t.is_cuda or not t.is_contiguous()):
+                    raise ValueError(f"weight {k}: expected contiguous {self.dtype} on the GPU")
+        ptrs = [{k: (L[k].data_ptr() if L.get(k) is not None else None) for k in WEIGHT_KEYS}
+                for L in layers]
+        self.handle = B.mte_encoder_create(cfg, ptrs, final_norm.data_ptr(), _stream(stream))
+
+    @classmethod
+    def from_host(cls, cfg: B.mte_config, layer_arrays, final_norm, device="cuda",
+                  stream: Optional[torch.cuda.Stream] = None) -> "TextEncoder":
+        """Creates the encoder from host arrays (numpy or CPU tensors), one layer at a time
+        on the device, so peak device memory is one layer beyond the library's copy."""
+        dt = TORCH_DTYPE[cfg.dtype]
+        layers: List[Dict[str, torch.Tensor]] = []
+        for arrs in layer_arrays:
+            layers.append({k: torch.as_tensor(arrs[k]).to(device=device, dtype=dt).contiguous()
+                           for k in WEIGHT_KEYS if k in arrs})
+        fn = torch.as_tensor(final_norm).to(device=device, dtype=dt).contiguous()
+        enc = cls(cfg, layers, fn, stream)
+        torch.cuda.synchronize()
+        return enc
+
+    def encode(self, embeds: torch.Tensor, pos_thw: torch.Tensor, seq_lens: Sequence[int],
+               out: Optional[torch.Tensor] = None,
+               stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+        T = int(sum(seq_lens))
+        if embeds.dtype != self.dtype or embeds.shape != (T, self.cfg.hidden) or not embeds.is_contiguous():
+            raise ValueError("embeds must be a contiguous [T, hidden] tensor of the encoder dtype")
+        if pos_thw.dtype != torch.int32 or pos_thw.shape != (3, T) or not pos_thw.is_contiguous():
+            raise ValueError("pos_thw must be a contiguous int32 [3, T] tensor")
+        if out is None:
+            out = torch.empty((T, self.cfg.hidden), dtype=self.out_dtype, device=embeds.device)
+        B.mte_encode(self.handle, embeds.data_ptr(), pos_thw.data_ptr(), list(seq_lens),
+                     len(seq_lens), out.data_ptr(), _stream(stream))
+        return out
+
+    def encode_layers(self, h_in: torch.Tensor, pos_thw: torch.Tensor, seq_lens: Sequence[int],
+                      layer_begin: int, layer_end: int, h_out: Optional[torch.Tensor] = None,
+                      stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+        T = int(sum(seq_lens))
+        if h_in.dtype != torch.float32 or h_in.shape != (T, self.cfg.hidden) or not h_in.is_contiguous():
+            raise ValueError("h_in must be a contiguous float32 [T, hidden] tensor")
+        if h_out is None:
+            h_out = torch.empty_like(h_in)
+        B.mte_encode_layers(self.handle, h_in.data_ptr(), pos_thw.data_ptr(), list(seq_lens),
+                            len(seq_lens), layer_begin, layer_end, h_out.data_ptr(), _stream(stream))
+        return h_out
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            B.mte_encoder_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def build_positions(layouts: Sequence[Sequence[int]], device="cuda",
+                    stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """(t, h, w) positions of packed sequences, built on the device -> int32 [3, T]."""
+    T = sum(int(l[0]) + int(l[1]) * int(l[2]) * int(l[3]) + int(l[4]) for l in layouts)
+    pos = torch.empty((3, T), dtype=torch.int32, device=device)
+    B.mte_build_positions(layouts, pos.data_ptr(), _stream(stream))
+    return pos

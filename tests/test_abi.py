@@ -1,0 +1,129 @@
+"""Host-side checks of the C ABI: the library loads, exports every declared
+symbol, and rejects bad arguments before any HIP call (runs without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def B():
+    from paper_2606_05981_amd import binding
+    return binding
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "mte.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\**\s*(mte_[a-z_]+)\s*\(", src, flags=re.M)
+    return sorted(set(names))
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for n in ("mte_encoder_create", "mte_encode", "mte_build_positions", "mte_encoder_destroy",
+              "mte_status_string", "mte_config_validate", "mte_check_batch", "mte_encode_layers"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(B):
+    lib = ctypes.CDLL(B.LIB_PATH)
+    missing = [n for n in _declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def _full(B, **kw):
+    args = dict(n_layers=28, hidden=2048, n_q_heads=16, n_kv_heads=8, head_dim=128, ffn=6144)
+    args.update(kw)
+    return B.make_config(**args)
+
+
+def test_valid_configs(B):
+    assert B.mte_config_validate(_full(B)) == 0
+    assert B.mte_config_validate(_full(B, n_layers=0)) == 0
+    tiny = B.make_config(2, 256, 4, 2, 64, 768, mrope_section=(12, 10, 10), dtype=B.MTE_F32)
+    assert B.mte_config_validate(tiny) == 0
+    assert B.mte_config_validate(_full(B, mrope_layout=1, qk_norm=0)) == 0
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_q_heads=16, n_kv_heads=5), -1),          # Hq % Hkv != 0
+    (dict(mrope_section=(24, 20, 19)), -1),          # sections do not sum to d/2
+    (dict(mrope_section=(-1, 45, 20)), -1),
+    (dict(hidden=0), -1), (dict(n_layers=-1), -1), (dict(ffn=-256), -1),
+    (dict(max_tokens=0), -1), (dict(max_batch=0), -1), (dict(max_seq=-3), -1),
+    (dict(rms_eps=0.0), -1), (dict(rope_theta=-1.0), -1), (dict(rms_eps=float("nan")), -1),
+    (dict(dtype=7), -1), (dict(out_dtype=2), -1), (dict(mrope_layout=3), -1), (dict(qk_norm=2), -1),
+    (dict(head_dim=96, mrope_section=(16, 16, 16)), -5),   # head_dim not built
+    (dict(hidden=2000), -5), (dict(ffn=6000), -5),
+    (dict(n_q_heads=12, n_kv_heads=4), -5),          # group of 3 query heads
+    (dict(max_tokens=1 << 24), -5),
+])
+def test_invalid_configs(B, kw, status):
+    assert B.mte_config_validate(_full(B, **kw)) == status
+
+
+def test_null_config(B):
+    assert B.lib.mte_config_validate(None) == -1
+
+
+def test_check_batch(B):
+    cfg = _full(B, max_tokens=1000, max_batch=4, max_seq=320)
+    assert B.mte_check_batch(cfg, [96, 320, 1]) == (0, 417)
+    assert B.mte_check_batch(cfg, [96, 0])[0] == -1           # empty sequence
+    assert B.mte_check_batch(cfg, [96, -4])[0] == -1
+    assert B.mte_check_batch(cfg, [321])[0] == -2             # longer than max_seq
+    assert B.mte_check_batch(cfg, [1] * 5)[0] == -2           # more than max_batch
+    assert B.mte_check_batch(cfg, [320, 320, 320, 100])[0] == -2  # more than max_tokens
+    assert B.mte_check_batch(cfg, [96], batch=0)[0] == -1
+    assert B.mte_check_batch(None, [96])[0] == -1
+    assert B.mte_check_batch(cfg, None, batch=1)[0] == -1
+
+
+def test_encode_rejects_null_encoder(B):
+    assert B.lib.mte_encode(None, 1, 1, B._i32([4]), 1, 1, None) == -1
+    assert B.lib.mte_encode_layers(None, 1, 1, B._i32([4]), 1, 0, 1, 1, None) == -1
+    assert B.lib.mte_timing_enable(None, 0, 4) == -1
+    B.lib.mte_encoder_destroy(None)  # no-op
+
+
+def test_create_rejects_bad_arguments_before_hip(B):
+    bad = _full(B, n_q_heads=16, n_kv_heads=5)
+    h = ctypes.c_void_p()
+    w = B.mte_weights(None, None)
+    assert B.lib.mte_encoder_create(ctypes.byref(bad), ctypes.byref(w), None, ctypes.byref(h)) == -1
+    good = _full(B)
+    # null weights / null layer array / null final norm
+    assert B.lib.mte_encoder_create(ctypes.byref(good), None, None, ctypes.byref(h)) == -1
+    assert B.lib.mte_encoder_create(ctypes.byref(good), ctypes.byref(w), None, ctypes.byref(h)) == -1
+    layers = (B.mte_layer_weights * 28)()
+    w2 = B.mte_weights(layers, 1234)
+    assert B.lib.mte_encoder_create(ctypes.byref(good), ctypes.byref(w2), None, ctypes.byref(h)) == -1
+    assert h.value is None
+
+
+@pytest.mark.parametrize("layouts", [
+    [(0, 1, 8, 8, -1)],           # negative count
+    [(0, 1, 0, 8, 32)],           # partially empty grid
+    [(0, 0, 0, 0, 0)],            # empty sequence
+    [(0, 1, 8, 8, 32), (-2, 0, 0, 0, 5)],
+    [(0, 1, 4096, 4096, 0)],      # 2^24 tokens
+])
+def test_build_positions_rejects_bad_layouts(B, layouts):
+    arr = (B.mte_seq_layout * len(layouts))(*[B.mte_seq_layout(*l) for l in layouts])
+    assert B.lib.mte_build_positions(arr, len(layouts), 4096, None) == -1
+
+
+def test_build_positions_rejects_null(B):
+    arr = (B.mte_seq_layout * 1)(B.mte_seq_layout(0, 1, 2, 2, 1))
+    assert B.lib.mte_build_positions(None, 1, 4096, None) == -1
+    assert B.lib.mte_build_positions(arr, 1, None, None) == -1
+    assert B.lib.mte_build_positions(arr, 0, 4096, None) == -1
+
+
+def test_status_strings(B):
+    for s in (0, -1, -2, -3, -4, -5, 17):
+        assert isinstance(B.mte_status_string(s), str) and B.mte_status_string(s)

@@ -1,0 +1,259 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 CPU oracle.
+
+Tolerances (error = max|gpu - oracle| / rms(oracle) over all tokens and
+channels): fp32 storage <= 1e-4; bf16 storage with fp32 accumulation
+<= 1e-2 for one layer (residual stream after the layer, from the oracle's
+exact layer input) and <= 3e-2 for the 28-layer stack output.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import te_oracle as O
+from synth import workloads as W
+from tests.gpu_common import (final_g, layer_w, layout_tuples, make_encoder, oracle_encode,
+                              rel_err, seq_slices)
+
+pytestmark = pytest.mark.gpu
+
+TOL_F32 = 1e-4
+TOL_LAYER = 1e-2
+TOL_STACK = 3e-2
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available(), "no GPU"
+    return t
+
+
+def _gpu_encode(torch, enc, dims, emb, layouts, raw=False):
+    from paper_2606_05981_amd.encoder import build_positions
+    dt = torch.bfloat16 if dims.dtype == "bf16" else torch.float32
+    x = torch.from_numpy(emb).to("cuda", dt)
+    pos = build_positions(layout_tuples(layouts))
+    out = enc.encode(x, pos, W.seq_lens(layouts))
+    torch.cuda.synchronize()
+    return out.cpu() if raw else out.float().cpu().numpy()
+
+
+# ------------------------------------------------------------ positions
+@pytest.mark.parametrize("case", ["tiny", "frames96", "mixed32", "text_before", "temporal", "many"])
+def test_positions_bit_exact(torch, case):
+    from paper_2606_05981_amd.encoder import build_positions
+    layouts = {
+        "tiny": W.workload("tiny_fp32").layouts,
+        "frames96": W.workload("stack_b16").layouts,
+        "mixed32": W.workload("stack_mixed32").layouts,
+        "text_before": (W.SeqLayout(3, 1, 2, 2, 2), W.SeqLayout(5, 0, 0, 0, 0), W.SeqLayout(0, 1, 3, 5, 0)),
+        "temporal": (W.SeqLayout(2, 3, 4, 2, 7), W.SeqLayout(0, 2, 2, 2, 1)),
+        "many": tuple(W.SeqLayout(i % 3, 1, 1 + i % 4, 2, i % 5) for i in range(300)),
+    }[case]
+    _say("positions", case)
+    got = build_positions(layout_tuples(layouts)).cpu().numpy()
+    np.testing.assert_array_equal(got, O.positions(layouts))
+
+
+# ------------------------------------------------------- tiny fp32 stack
+@pytest.mark.parametrize("mrope_layout,qk_norm", [(0, 1), (1, 1), (0, 0)])
+def test_tiny_fp32_stack(torch, mrope_layout, qk_norm):
+    wl = W.workload("tiny_fp32")
+    dims = wl.dims.with_(mrope_layout=mrope_layout, qk_norm=qk_norm)
+    _say("tiny fp32", mrope_layout, qk_norm)
+    emb = W.embeddings(dims, wl.layouts)
+    enc = make_encoder(dims)
+    got = _gpu_encode(torch, enc, dims, emb, wl.layouts)
+    enc.close()
+    err = rel_err(got, oracle_encode(dims, emb, wl.layouts))
+    _say("  err", err)
+    assert err <= TOL_F32
+
+
+def test_tiny_fp32_ragged_edges(torch):
+    """Lengths 1, 2, tile edges +-1 and text-only sequences in one packed batch."""
+    dims = W.DIMS_TINY
+    layouts = (W.SeqLayout(1, 0, 0, 0, 0), W.SeqLayout(0, 1, 1, 1, 1), W.SeqLayout(0, 1, 4, 4, 15),
+               W.SeqLayout(0, 1, 4, 4, 16), W.SeqLayout(0, 1, 4, 4, 17), W.SeqLayout(3, 1, 6, 5, 30),
+               W.SeqLayout(64, 0, 0, 0, 1), W.SeqLayout(0, 1, 8, 8, 33), W.SeqLayout(2, 2, 4, 4, 100))
+    emb = W.embeddings(dims, layouts)
+    _say("tiny ragged", W.seq_lens(layouts))
+    enc = make_encoder(dims)
+    got = _gpu_encode(torch, enc, dims, emb, layouts)
+    enc.close()
+    ref = oracle_encode(dims, emb, layouts)
+    for sl in seq_slices(layouts):
+        assert rel_err(got[sl], ref[sl]) <= TOL_F32, sl
+    assert rel_err(got, ref) <= TOL_F32
+
+
+def test_tiny_zero_layers_is_final_norm(torch):
+    dims = W.DIMS_TINY.with_(n_layers=0)
+    wl = W.workload("tiny_fp32")
+    emb = W.embeddings(dims, wl.layouts)
+    enc = make_encoder(dims)
+    got = _gpu_encode(torch, enc, dims, emb, wl.layouts)
+    enc.close()
+    assert rel_err(got, O.rmsnorm(emb, final_g(dims), dims.rms_eps)) <= TOL_F32
+
+
+# ----------------------------------------------------- one bf16 layer
+def test_layer1_bf16_residual_after_layer(torch):
+    wl = W.workload("layer1_b1")
+    dims = wl.dims
+    emb = W.embeddings(dims, wl.layouts)
+    pos = O.positions(wl.layouts)
+    _say("layer1 bf16 per-layer")
+    enc = make_encoder(dims)
+    from paper_2606_05981_amd.encoder import build_positions
+    h_in = torch.from_numpy(emb.astype(np.float32)).cuda()
+    h = enc.encode_layers(h_in, build_positions(layout_tuples(wl.layouts)), W.seq_lens(wl.layouts), 0, 1)
+    torch.cuda.synchronize()
+    ref = O.layer_forward(emb, pos, W.seq_lens(wl.layouts), layer_w(dims, 0), dims)
+    err = rel_err(h.cpu().numpy(), ref)
+    _say("  err", err)
+    assert err <= TOL_LAYER
+    got = _gpu_encode(torch, enc, dims, emb, wl.layouts)
+    enc.close()
+    err2 = rel_err(got, O.rmsnorm(ref, final_g(dims), dims.rms_eps))
+    _say("  err(final norm)", err2)
+    assert err2 <= TOL_LAYER
+
+
+def test_bf16_output_is_rounded_fp32_result(torch):
+    """With a bf16 output, each value is the fp32 result rounded to nearest bf16."""
+    from paper_2606_05981_amd import binding as B
+    wl = W.workload("layer1_b1")
+    dims = wl.dims
+    emb = W.embeddings(dims, wl.layouts, std=37.0, outliers=6)
+    e32 = make_encoder(dims)
+    e16 = make_encoder(dims, out_dtype=B.MTE_BF16)
+    y32 = _gpu_encode(torch, e32, dims, emb, wl.layouts, raw=True)
+    y16 = _gpu_encode(torch, e16, dims, emb, wl.layouts, raw=True)
+    e32.close(); e16.close()
+    assert y16.dtype == torch.bfloat16
+    assert torch.equal(y16, y32.to(torch.bfloat16))
+
+
+# --------------------------------------------------- 28-layer stacks
+@pytest.fixture(scope="module")
+def full_enc(torch):
+    _say("building the 28-layer encoder")
+    enc = make_encoder(W.DIMS_FULL, max_tokens=32 * 320, max_batch=64, max_seq=4096)
+    yield enc
+    enc.close()
+
+
+def test_stack_b1_and_per_layer(torch, full_enc):
+    wl = W.workload("stack_b1")
+    dims = wl.dims
+    emb = W.embeddings(dims, wl.layouts)
+    _say("stack b1")
+    got = _gpu_encode(torch, full_enc, dims, emb, wl.layouts)
+    keep = (0, 13, 27)
+    ref = oracle_encode(dims, emb, wl.layouts, keep=keep)
+    kept = dict(O.encode.kept)
+    err = rel_err(got, ref)
+    _say("  err 28 layers", err)
+    assert err <= TOL_STACK
+    from paper_2606_05981_amd.encoder import build_positions
+    pos_g = build_positions(layout_tuples(wl.layouts))
+    pos = O.positions(wl.layouts)
+    for l in keep:
+        x = kept[l].astype(np.float32)
+        h = full_enc.encode_layers(torch.from_numpy(x).cuda(), pos_g, W.seq_lens(wl.layouts), l, l + 1)
+        torch.cuda.synchronize()
+        r = O.layer_forward(x, pos, W.seq_lens(wl.layouts), layer_w(dims, l), dims)
+        e = rel_err(h.cpu().numpy(), r)
+        _say(f"  err layer {l}", e)
+        assert e <= TOL_LAYER
+
+
+@pytest.mark.parametrize("name,sample", [
+    ("stack_b16", (0, 7, 15)),
+    ("stack_b8", (3,)),
+    ("stack_mixed32", "minmax"),
+    ("stack_b32_l320", (31,)),
+])
+def test_stack_batched_sampled_sequences(torch, full_enc, name, sample):
+    """The whole batch runs on the GPU; sampled sequences are re-run alone in the oracle
+    (sequences are independent: the oracle pins packed == alone)."""
+    wl = W.workload(name)
+    dims = wl.dims
+    emb = W.embeddings(dims, wl.layouts)
+    _say(name, "T =", wl.tokens)
+    got = _gpu_encode(torch, full_enc, dims, emb, wl.layouts)
+    lens = W.seq_lens(wl.layouts)
+    if sample == "minmax":
+        sample = (int(np.argmin(lens)), int(np.argmax(lens)))
+    sl = seq_slices(wl.layouts)
+    for i in sample:
+        ref = oracle_encode(dims, emb[sl[i]], [wl.layouts[i]])
+        e = rel_err(got[sl[i]], ref)
+        _say(f"  seq {i} (L={lens[i]}) err", e)
+        assert e <= TOL_STACK
+
+
+def test_stack_wide_range_inputs(torch, full_enc):
+    """Embeddings with std 37 and +-1160 outliers (the trained encoder's activation range)."""
+    wl = W.workload("stack_b1")
+    dims = wl.dims
+    emb = W.embeddings(dims, wl.layouts, std=37.0, outliers=6)
+    got = _gpu_encode(torch, full_enc, dims, emb, wl.layouts)
+    assert np.isfinite(got).all()
+    err = rel_err(got, oracle_encode(dims, emb, wl.layouts))
+    _say("wide range err", err)
+    assert err <= TOL_STACK
+
+
+# ------------------------------------------------- GPU-side invariants
+def test_packed_equals_alone_and_permutation(torch):
+    """Each row's result is independent of its neighbours in the packed batch."""
+    dims = W.DIMS_FULL.with_(n_layers=2)
+    layouts = (W.FRAME_96, W.SeqLayout(0, 1, 10, 9, 41), W.SeqLayout(0, 1, 8, 8, 1))
+    emb = W.embeddings(dims, layouts)
+    enc = make_encoder(dims)
+    full = _gpu_encode(torch, enc, dims, emb, layouts)
+    sl = seq_slices(layouts)
+    for i, s in enumerate(layouts):
+        alone = _gpu_encode(torch, enc, dims, np.ascontiguousarray(emb[sl[i]]), [s])
+        np.testing.assert_array_equal(alone, full[sl[i]])
+    perm = [2, 0, 1]
+    idx = np.concatenate([np.arange(sl[i].start, sl[i].stop) for i in perm])
+    out = _gpu_encode(torch, enc, dims, np.ascontiguousarray(emb[idx]), [layouts[i] for i in perm])
+    enc.close()
+    np.testing.assert_array_equal(out, full[idx])
+
+
+def test_graph_capture_replays_match_eager(torch):
+    """mte_encode performs no host sync or allocation: it captures into a graph."""
+    from paper_2606_05981_amd.encoder import build_positions
+    dims = W.DIMS_FULL.with_(n_layers=2)
+    layouts = (W.FRAME_96,) * 3
+    emb = W.embeddings(dims, layouts)
+    enc = make_encoder(dims)
+    x = torch.from_numpy(emb).to("cuda", torch.bfloat16)
+    pos = build_positions(layout_tuples(layouts))
+    lens = W.seq_lens(layouts)
+    eager = enc.encode(x, pos, lens).clone()
+    out = torch.empty_like(eager)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            enc.encode(x, pos, lens, out=out)
+    torch.cuda.current_stream().wait_stream(s)
+    for r in range(3):
+        out.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager), r
+        enc.encode(x, pos, lens)   # eager work between replays
+        torch.cuda.synchronize()
+    enc.close()
