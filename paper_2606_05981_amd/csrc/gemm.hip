@@ -26,6 +26,7 @@
 // rows (MLP up-projection, written in the activation format) and
 // accumulation into the fp32 residual stream (attention output projection
 // and MLP down-projection).
+#include <cmath>
 #include <type_traits>
 
 #include "common.h"
@@ -37,76 +38,106 @@ struct GemmArgs {
   const char *A;      // A (MODE_F32) or A_hi (MODE_BF16X2)
   const char *A_lo;   // A_lo plane (MODE_BF16X2)
   const char *W;
-  void *C;            // EPI_STORE: float; EPI_RESID: float; EPI_SWIGLU: activation format
+  void *C;            // EPI_STORE / EPI_RESID / EPI_ATOMIC: float; EPI_SWIGLU: activation format
   size_t c_plane;     // EPI_SWIGLU, MODE_BF16X2: elements between C_hi and C_lo planes
   int M, N, K, ldc;
+  int k_chunk;        // K range of one split (gridDim.z splits)
 };
 
-__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r ^ (r >> 3)) & 7); }
+// Chunk swizzles for rows of 128 bytes (8 chunks) and 64 bytes (4 chunks):
+// the 16-byte fragment reads (32 consecutive rows at one logical chunk, the
+// upper half-wave at the next chunk) are free of LDS bank conflicts with
+// these two (measured with SQ_LDS_BANK_CONFLICT on gfx950; e.g. the 64-byte
+// variant c ^ ((r >> 1) & 3) is 2-way conflicted).
+template <int CH>
+__device__ __forceinline__ int swz(int r, int c) {
+  if constexpr (CH == 8) return c ^ ((r ^ (r >> 3)) & 7);
+  else return c ^ ((r >> 2) & 3);
+}
 
-template <int MODE, int BM, int BN, int WM, int WN, int EPI>
-__global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
+// Waits until at most n vector-memory operations of this wave are pending.
+template <int n>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((n & 0xF) | (0x7 << 4) | (0xF << 8) | ((n >> 4) << 14));
+}
+// Waits until at most after*LOADS vector-memory operations are pending,
+// for a wave-uniform after in [0, 3].
+template <int LOADS>
+__device__ __forceinline__ void wait_stages(int after) {
+  if (after >= 3) wait_vm<(3 * LOADS < 64 ? 3 * LOADS : 0)>();
+  else if (after == 2) wait_vm<(2 * LOADS < 64 ? 2 * LOADS : 0)>();
+  else if (after == 1) wait_vm<LOADS>();
+  else wait_vm<0>();
+}
+
+// 16-byte global -> LDS copy without a register round trip: lane i of the
+// wave writes lds_wave_base + 16*i (the LDS base must be wave-uniform).
+__device__ __forceinline__ void dma16(const void *g, void *lds_wave_base) {
+  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)g,
+                                   (__attribute__((address_space(3))) void *)lds_wave_base, 16, 0, 0);
+}
+
+// The main loop keeps P stages in an LDS ring filled by direct global->LDS
+// loads, and double-buffers the MFMA operand fragments in registers. One
+// barrier per stage, placed before the stage's last k-step: before it each
+// wave waits for its own loads of the next stage; after it (all waves' loads
+// of the next stage are in LDS, and every wave is done with the previous
+// stage) the loads of stage kt+P-1 go into the slot stage kt-1 used, and the
+// first fragments of stage kt+1 are read while the last MFMAs of stage kt
+// run. Raw s_barrier (no fence) keeps the compiler from forcing vmcnt(0) at
+// the barrier; the waits are explicit.
+template <int MODE, int BM, int BN, int WM, int WN, int ROWB, int P, int EPI, int OCC>
+__global__ __launch_bounds__(256, OCC) void k_gemm(GemmArgs g) {
   typedef typename std::conditional<MODE == MODE_F32, float, bf16>::type T;
   constexpr int NA = (MODE == MODE_BF16X2) ? 2 : 1;   // A planes
-  constexpr int ROWB = 128;                       // bytes of K per row per stage
   constexpr int KS = ROWB / (int)sizeof(T);       // k elements per stage
-  constexpr int CH = ROWB / 16;                   // 16-byte chunks per row
+  constexpr int CH = ROWB / 16;                   // 16-byte chunks per row per stage
   constexpr int WTM = BM / WM, WTN = BN / WN;     // wave tile
   constexpr int TM = WTM / 32, TN = WTN / 32;     // 32x32 MFMA tiles per wave
-  constexpr int AC = BM * CH / 256, BC = BN * CH / 256;  // chunks per thread per stage
+  constexpr int ACH = BM * CH, BCH = BN * CH;     // chunks per stage (one A plane / W)
+  static_assert(ACH % 256 == 0 && BCH % 256 == 0, "whole DMA rounds");
+  constexpr int AR = ACH / 256, BR = BCH / 256;   // DMA instructions per thread per matrix
+  constexpr int LOADS = NA * AR + BR;             // per thread per stage
   constexpr int STAGE = (NA * BM + BN) * CH;      // u32x4 slots per stage
   static_assert(WM * WN == 4, "4 waves");
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
-  static_assert((BM * CH) % 256 == 0 && (BN * CH) % 256 == 0, "stage split");
-  static_assert(EPI != EPI_SWIGLU || (WTN % 64 == 0), "swiglu pairs");
+  static_assert(LOADS * (P - 2) < 64 && P >= 3 && P <= 5, "vmcnt range, ring depth");
   typedef typename Frag<T>::type frag_t;
 
-  extern __shared__ u32x4 lds[];                  // [2][STAGE]
+  extern __shared__ u32x4 lds[];                  // [P][STAGE]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
-  const int M = g.M, K = g.K;
-  const size_t rowb = (size_t)K * sizeof(T);      // row pitch in bytes (A planes and W)
-  const int nk = K / KS;
+  const int M = g.M;
+  const size_t rowb = (size_t)g.K * sizeof(T);    // row pitch in bytes (A planes and W)
+  const size_t kb0 = (size_t)blockIdx.z * g.k_chunk * sizeof(T);
+  const int nk = g.k_chunk / KS;
 
-  const char *pa[AC];
-  const char *pb[BC];
+  // DMA sources: instruction c of this thread fills LDS slot q = (c*4 + wave)*64 + lane
+  // of its matrix (row q / CH, swizzled slot q % CH, logical chunk slot ^ f(row)).
+  const char *pa[AR];
+  const char *pb[BR];
 #pragma unroll
-  for (int c = 0; c < AC; ++c) {
-    int idx = tid + c * 256, r = idx / CH, ch = idx % CH;
-    int gr = min(m0 + r, M - 1);
-    pa[c] = g.A + gr * rowb + ch * 16;
+  for (int c = 0; c < AR; ++c) {
+    const int q = (c * 4 + wave) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
+    pa[c] = g.A + (size_t)min(m0 + r, M - 1) * rowb + kb0 + ch * 16;
   }
 #pragma unroll
-  for (int c = 0; c < BC; ++c) {
-    int idx = tid + c * 256, r = idx / CH, ch = idx % CH;
-    pb[c] = g.W + (size_t)(n0 + r) * rowb + ch * 16;
+  for (int c = 0; c < BR; ++c) {
+    const int q = (c * 4 + wave) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
+    pb[c] = g.W + (size_t)(n0 + r) * rowb + kb0 + ch * 16;
   }
   const ptrdiff_t lo_off = (MODE == MODE_BF16X2) ? (g.A_lo - g.A) : 0;
-  u32x4 ra[NA][AC], rb[BC];
-  auto gload = [&](int kt) {
+  auto issue = [&](int kt) {
+    u32x4 *st = lds + (kt % P) * STAGE;
+    const size_t ko = (size_t)kt * ROWB;
 #pragma unroll
     for (int p = 0; p < NA; ++p)
 #pragma unroll
-      for (int c = 0; c < AC; ++c) ra[p][c] = *(const u32x4 *)(pa[c] + p * lo_off + (size_t)kt * ROWB);
+      for (int c = 0; c < AR; ++c) dma16(pa[c] + p * lo_off + ko, st + p * ACH + (c * 4 + wave) * 64);
 #pragma unroll
-    for (int c = 0; c < BC; ++c) rb[c] = *(const u32x4 *)(pb[c] + (size_t)kt * ROWB);
-  };
-  auto lstore = [&](int buf) {
-    u32x4 *st = lds + buf * STAGE;
-#pragma unroll
-    for (int p = 0; p < NA; ++p)
-#pragma unroll
-      for (int c = 0; c < AC; ++c) {
-        int idx = tid + c * 256, r = idx / CH, ch = idx % CH;
-        st[p * BM * CH + r * CH + swz(r, ch)] = ra[p][c];
-      }
-    u32x4 *lb = st + NA * BM * CH;
-#pragma unroll
-    for (int c = 0; c < BC; ++c) {
-      int idx = tid + c * 256, r = idx / CH, ch = idx % CH;
-      lb[r * CH + swz(r, ch)] = rb[c];
-    }
+    for (int c = 0; c < BR; ++c) dma16(pb[c] + ko, st + NA * ACH + (c * 4 + wave) * 64);
   };
 
   f32x16 acc[TM][TN];
@@ -117,40 +148,58 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  gload(0);
-  lstore(0);
-  __syncthreads();
+  frag_t fa[2][NA][TM], fb[2][TN];
   const int lrow = lane & 31, lgrp = lane >> 5;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) gload(kt + 1);
-    const u32x4 *st = lds + buf * STAGE;
-    const u32x4 *lb = st + NA * BM * CH;
+  auto load_frags = [&](const u32x4 *st, int kk, int b) {
+    const u32x4 *lb = st + NA * ACH;
+    const int ch = kk * 2 + lgrp;
 #pragma unroll
-    for (int kk = 0; kk < CH / 2; ++kk) {
-      frag_t fa[NA][TM], fb[TN];
-      const int ch = kk * 2 + lgrp;
+    for (int i = 0; i < TM; ++i) {
+      const int r = wm * WTM + i * 32 + lrow;
 #pragma unroll
       for (int p = 0; p < NA; ++p)
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-          int r = wm * WTM + i * 32 + lrow;
-          fa[p][i] = __builtin_bit_cast(frag_t, st[p * BM * CH + r * CH + swz(r, ch)]);
-        }
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        int r = wn * WTN + j * 32 + lrow;
-        fb[j] = __builtin_bit_cast(frag_t, lb[r * CH + swz(r, ch)]);
-      }
-#pragma unroll
-      for (int p = 0; p < NA; ++p)
-#pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j) mfma32(acc[i][j], fa[p][i], fb[j]);
+        fa[b][p][i] = __builtin_bit_cast(frag_t, st[p * ACH + r * CH + swz<CH>(r, ch)]);
     }
-    if (kt + 1 < nk) lstore(buf ^ 1);
-    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int r = wn * WTN + j * 32 + lrow;
+      fb[b][j] = __builtin_bit_cast(frag_t, lb[r * CH + swz<CH>(r, ch)]);
+    }
+  };
+  auto compute = [&](int b) {
+#pragma unroll
+    for (int p = 0; p < NA; ++p)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) mfma32(acc[i][j], fa[b][p][i], fb[b][j]);
+  };
+  constexpr int KK = CH / 2;                      // 16-k steps per stage (even)
+  static_assert(KK % 2 == 0, "fragment buffer parity");
+
+#pragma unroll
+  for (int s = 0; s < P - 1; ++s)
+    if (s < nk) issue(s);
+  wait_stages<LOADS>(min(P - 2, nk - 1));
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  load_frags(lds, 0, 0);
+  for (int kt = 0; kt < nk; ++kt) {
+    const u32x4 *st = lds + (kt % P) * STAGE;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      const int cur = kk & 1;
+      if (kk + 1 < KK) {
+        load_frags(st, kk + 1, cur ^ 1);
+      } else if (kt + 1 < nk) {
+        wait_stages<LOADS>(max(0, min(P - 3, nk - 2 - kt)));
+        __builtin_amdgcn_s_barrier();
+        asm volatile("" ::: "memory");  // keep LDS reads of stage kt+1 below the barrier
+        if (kt + P - 1 < nk) issue(kt + P - 1);
+        load_frags(lds + ((kt + 1) % P) * STAGE, 0, cur ^ 1);
+      }
+      compute(cur);
+    }
   }
 
   // Epilogue.
@@ -160,31 +209,26 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
     for (int r = 0; r < 16; ++r) {
       const int m = m0 + wm * WTM + i * 32 + acc_row(r, lane);
       if (m >= M) continue;
-      if constexpr (EPI == EPI_STORE) {
+      if constexpr (EPI == EPI_STORE || EPI == EPI_RESID || EPI == EPI_ATOMIC) {
         float *C = (float *)g.C;
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-          int n = n0 + wn * WTN + j * 32 + lrow;
-          C[(size_t)m * g.ldc + n] = acc[i][j][r];
-        }
-      } else if constexpr (EPI == EPI_RESID) {
-        float *C = (float *)g.C;
-#pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          int n = n0 + wn * WTN + j * 32 + lrow;
-          C[(size_t)m * g.ldc + n] += acc[i][j][r];
+          const size_t o = (size_t)m * g.ldc + n0 + wn * WTN + j * 32 + lrow;
+          if constexpr (EPI == EPI_STORE) C[o] = acc[i][j][r];
+          else if constexpr (EPI == EPI_RESID) C[o] += acc[i][j][r];
+          else atomicAdd(C + o, acc[i][j][r]);
         }
       } else {
 #pragma unroll
         for (int j = 0; j < TN; j += 2) {
-          int f = (n0 + wn * WTN + j * 32) / 2 + lrow;
-          float gt = acc[i][j][r], up = acc[i][j + 1][r];
-          float y = gt / (1.f + __expf(-gt)) * up;
-          size_t o = (size_t)m * g.ldc + f;
+          const int f = (n0 + wn * WTN + j * 32) / 2 + lrow;
+          const float gt = acc[i][j][r], up = acc[i][j + 1][r];
+          const float y = gt / (1.f + __expf(-gt)) * up;
+          const size_t o = (size_t)m * g.ldc + f;
           if constexpr (MODE == MODE_F32) {
             ((float *)g.C)[o] = y;
           } else {
-            bf16 hi = (bf16)y;
+            const bf16 hi = (bf16)y;
             ((bf16 *)g.C)[o] = hi;
             ((bf16 *)g.C)[o + g.c_plane] = (bf16)(y - (float)hi);
           }
@@ -194,37 +238,141 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g) {
   }
 }
 
-template <int MODE, int BM, int BN, int WM, int WN, int EPI>
-static hipError_t run(const GemmArgs &a, hipStream_t s) {
+// ------------------------------------------------------------- planning
+// A tile configuration is a compile-time instantiation; the planner picks
+// one per (M, N, K, epilogue) from the number of workgroups it yields and
+// the work per workgroup.
+struct TileCfg {
+  int bm, bn, wm, wn, rowb, occ;
+};
+
+template <int MODE, int BM, int BN, int WM, int WN, int ROWB, int P, int EPI, int OCC>
+static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
+  if constexpr (EPI == EPI_SWIGLU && (BN / WN) % 64 != 0) {
+    return hipErrorInvalidValue;  // gate/up pairs need 64 columns per wave
+  } else {
   constexpr int NA = (MODE == MODE_BF16X2) ? 2 : 1;
-  constexpr int lds_bytes = 2 * (NA * BM + BN) * 128;
-  auto kern = k_gemm<MODE, BM, BN, WM, WN, EPI>;
+  constexpr int lds_bytes = P * (NA * BM + BN) * ROWB;
+  auto kern = k_gemm<MODE, BM, BN, WM, WN, ROWB, P, EPI, OCC>;
   static const hipError_t attr = hipFuncSetAttribute(
       (const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
   if (attr != hipSuccess) return attr;
-  dim3 grid(a.N / BN, (a.M + BM - 1) / BM);
+  dim3 grid(a.N / BN, (a.M + BM - 1) / BM, splits);
   hipLaunchKernelGGL(kern, grid, dim3(256), lds_bytes, s, a);
   return hipGetLastError();
+  }
 }
 
+// Tile table: id -> instantiation (bm, bn, wave layout wm x wn, bytes of K
+// per row per stage, LDS ring stages, workgroups per CU). The LDS ring
+// (P * (2*bm + bn) * rowb bytes in bf16x2 mode) must fit 160 KB / occ.
+#define MTE_TILE_TABLE(X)                    \
+  X(0, 256, 256, 2, 2, 64, 3, 1)             \
+  X(1, 192, 256, 2, 2, 64, 3, 1)             \
+  X(2, 192, 192, 2, 2, 64, 4, 1)             \
+  X(3, 256, 128, 2, 2, 64, 3, 1)             \
+  X(4, 128, 256, 2, 2, 64, 4, 1)             \
+  X(5, 192, 128, 2, 2, 64, 4, 1)             \
+  X(6, 128, 128, 2, 2, 64, 3, 2)             \
+  X(7, 128, 128, 2, 2, 128, 3, 1)            \
+  X(8, 64, 256, 1, 4, 128, 3, 1)             \
+  X(9, 64, 256, 1, 4, 64, 3, 2)              \
+  X(10, 64, 128, 2, 2, 64, 4, 2)             \
+  X(11, 32, 256, 1, 4, 128, 3, 1)            \
+  X(12, 32, 128, 1, 4, 128, 3, 2)            \
+  X(13, 128, 64, 4, 1, 64, 4, 2)             \
+  X(14, 192, 64, 2, 2, 64, 4, 1)
+
+static const TileCfg kTiles[] = {
+#define MTE_TILE_INFO(id, bm, bn, wm, wn, rowb, p, occ) {bm, bn, wm, wn, rowb, occ},
+    MTE_TILE_TABLE(MTE_TILE_INFO)
+#undef MTE_TILE_INFO
+};
+constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
+
 template <int MODE, int EPI>
-static hipError_t dispatch(const GemmArgs &a, hipStream_t s) {
-  if (a.M <= 64) return run<MODE, 32, 256, 1, 4, EPI>(a, s);
-  return run<MODE, 128, 128, 2, 2, EPI>(a, s);
+static hipError_t run_id(int id, const GemmArgs &a, int splits, hipStream_t s) {
+  switch (id) {
+#define MTE_TILE_CASE(idv, bm, bn, wm, wn, rowb, p, occ) \
+  case idv: return run<MODE, bm, bn, wm, wn, rowb, p, EPI, occ>(a, splits, s);
+    MTE_TILE_TABLE(MTE_TILE_CASE)
+#undef MTE_TILE_CASE
+  }
+  return hipErrorInvalidValue;
+}
+
+static bool tile_fits(int id, int N, int K, int esz, int epi, int splits) {
+  const TileCfg &t = kTiles[id];
+  if (N % t.bn) return false;
+  const int ks = t.rowb / esz;
+  if (K % splits || (K / splits) % ks) return false;
+  if (epi == EPI_SWIGLU && (t.bn / t.wn) % 64) return false;  // gate/up pairs per wave
+  return true;
+}
+
+// Steady-state throughput of each tile (algorithmic TFLOP/s of a bf16x2
+// GEMM at M = 10240, measured on MI355X); the planner's only calibration.
+static const double kTileRate[kNumTiles] = {412, 454, 420, 385, 469, 394, 454, 423,
+                                            436, 458, 404, 296, 344, 340, 250};
+
+// Picks (tile, splits) for an M x N x K problem: estimated time = rounds of
+// workgroups over the compute units x the time one full round takes at the
+// tile's measured rate. Split-K is only considered for small M and for the
+// residual epilogue (partial sums are added atomically).
+static void plan(int M, int N, int K, int esz, int epi, int *tile, int *splits) {
+  const int cus = 256;
+  double best = 1e30;
+  *tile = 0;
+  *splits = 1;
+  for (int id = 0; id < kNumTiles; ++id) {
+    for (int sp = 1; sp <= 8; sp *= 2) {
+      if (sp > 1 && (epi != EPI_RESID || M > 256)) continue;
+      if (!tile_fits(id, N, K, esz, epi, sp)) continue;
+      const TileCfg &t = kTiles[id];
+      const double tiles = (double)(N / t.bn) * ((M + t.bm - 1) / t.bm) * sp;
+      const double slots = (double)cus * t.occ;
+      const double rounds = std::ceil(tiles / slots);
+      const double work = 2.0 * t.bm * t.bn * ((double)K / sp);
+      const double cost = rounds * slots * work / kTileRate[id] * (sp > 1 ? 1.15 : 1.0);
+      if (cost < best) {
+        best = cost;
+        *tile = id;
+        *splits = sp;
+      }
+    }
+  }
+}
+
+template <int MODE>
+static hipError_t launch_mode(int epi, int tile, int splits, const GemmArgs &a, hipStream_t s) {
+  switch (epi) {
+    case EPI_STORE: return run_id<MODE, EPI_STORE>(tile, a, splits, s);
+    case EPI_SWIGLU: return run_id<MODE, EPI_SWIGLU>(tile, a, splits, s);
+    case EPI_RESID:
+      return splits > 1 ? run_id<MODE, EPI_ATOMIC>(tile, a, splits, s)
+                        : run_id<MODE, EPI_RESID>(tile, a, splits, s);
+    default: return run_id<MODE, EPI_ATOMIC>(tile, a, splits, s);
+  }
+}
+
+hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void *A, const void *A_lo,
+                            const void *W, void *C, size_t c_plane, int M, int N, int K, int ldc,
+                            hipStream_t s) {
+  if (M <= 0) return hipSuccess;
+  const int esz = mode == MODE_BF16X2 ? 2 : 4;
+  if (tile < 0 || tile >= kNumTiles || splits < 1 || !tile_fits(tile, N, K, esz, epi, splits))
+    return hipErrorInvalidValue;
+  GemmArgs a{(const char *)A, (const char *)A_lo, (const char *)W, C, c_plane, M, N, K, ldc, K / splits};
+  return mode == MODE_BF16X2 ? launch_mode<MODE_BF16X2>(epi, tile, splits, a, s)
+                             : launch_mode<MODE_F32>(epi, tile, splits, a, s);
 }
 
 hipError_t launch_gemm(int mode, int epi, const void *A, const void *A_lo, const void *W, void *C,
                        size_t c_plane, int M, int N, int K, int ldc, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  GemmArgs a{(const char *)A, (const char *)A_lo, (const char *)W, C, c_plane, M, N, K, ldc};
-  if (mode == MODE_BF16X2) {
-    if (epi == EPI_STORE) return dispatch<MODE_BF16X2, EPI_STORE>(a, s);
-    if (epi == EPI_SWIGLU) return dispatch<MODE_BF16X2, EPI_SWIGLU>(a, s);
-    return dispatch<MODE_BF16X2, EPI_RESID>(a, s);
-  }
-  if (epi == EPI_STORE) return dispatch<MODE_F32, EPI_STORE>(a, s);
-  if (epi == EPI_SWIGLU) return dispatch<MODE_F32, EPI_SWIGLU>(a, s);
-  return dispatch<MODE_F32, EPI_RESID>(a, s);
+  int tile, splits;
+  plan(M, N, K, mode == MODE_BF16X2 ? 2 : 4, epi, &tile, &splits);
+  return launch_gemm_tile(mode, epi, tile, splits, A, A_lo, W, C, c_plane, M, N, K, ldc, s);
 }
 
 }  // namespace mte

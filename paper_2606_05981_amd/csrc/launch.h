@@ -25,6 +25,7 @@ enum Epilogue {
   EPI_SWIGLU = 1,  // gate/up rows interleaved in blocks of 32: C[m, f] = silu(gate) * up,
                    // written as float (MODE_F32) or bf16 hi/lo planes (MODE_BF16X2)
   EPI_RESID = 2,   // C (float residual stream) [m, n] += acc
+  EPI_ATOMIC = 3,  // C (float) [m, n] += acc with atomics (split-K partial sums)
 };
 
 // C = A[M, K] * W[N, K]^T. MODE_F32: A, W float. MODE_BF16X2: A = A_hi + A_lo
@@ -32,6 +33,13 @@ enum Epilogue {
 // in elements between the hi and lo planes of a bf16x2 C.
 hipError_t launch_gemm(int mode, int epi, const void *A, const void *A_lo, const void *W, void *C,
                        size_t c_plane, int M, int N, int K, int ldc, hipStream_t s);
+
+// The same with an explicit tile configuration (index into the GEMM tile
+// table) and number of K splits; used for tuning. Returns
+// hipErrorInvalidValue if the tile does not fit the shape.
+hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void *A, const void *A_lo,
+                            const void *W, void *C, size_t c_plane, int M, int N, int K, int ldc,
+                            hipStream_t s);
 
 // Per-row RMSNorm: out[r, :] = in[r, :] / sqrt(mean(in[r,:]^2) + eps) * g.
 // in: `in_fmt` (FMT_F32 or FMT_BF16) [rows, D]; when copy_to != nullptr the

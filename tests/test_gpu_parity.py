@@ -126,7 +126,9 @@ def test_layer1_bf16_residual_after_layer(torch):
 
 
 def test_bf16_output_is_rounded_fp32_result(torch):
-    """With a bf16 output, each value is the fp32 result rounded to nearest bf16."""
+    """With a bf16 output, each value is the fp32 result rounded to nearest bf16 (two runs
+    may differ in the last fp32 bits where split-K partial sums are added atomically, so
+    a value next to a rounding boundary may round either way)."""
     from paper_2606_05981_amd import binding as B
     wl = W.workload("layer1_b1")
     dims = wl.dims
@@ -137,7 +139,15 @@ def test_bf16_output_is_rounded_fp32_result(torch):
     y16 = _gpu_encode(torch, e16, dims, emb, wl.layouts, raw=True)
     e32.close(); e16.close()
     assert y16.dtype == torch.bfloat16
-    assert torch.equal(y16, y32.to(torch.bfloat16))
+    a, b = y16.float(), y32
+    half_ulp = torch.ldexp(torch.ones_like(b), torch.frexp(b)[1] - 9)
+    excess = (a - b).abs() - (half_ulp + 1e-5 * b.pow(2).mean().sqrt())
+    i = int(excess.argmax())
+    _say("  worst", a.reshape(-1)[i].item(), b.reshape(-1)[i].item(), half_ulp.reshape(-1)[i].item())
+    assert excess.max().item() <= 0
+    frac_equal = (y16 == y32.to(torch.bfloat16)).float().mean().item()
+    _say("  equal fraction", frac_equal)
+    assert frac_equal > 0.999
 
 
 # --------------------------------------------------- 28-layer stacks
@@ -213,7 +223,8 @@ def test_stack_wide_range_inputs(torch, full_enc):
 
 # ------------------------------------------------- GPU-side invariants
 def test_packed_equals_alone_and_permutation(torch):
-    """Each row's result is independent of its neighbours in the packed batch."""
+    """Each row's result is independent of its neighbours in the packed batch (up to the
+    order in which split-K partial sums are added)."""
     dims = W.DIMS_FULL.with_(n_layers=2)
     layouts = (W.FRAME_96, W.SeqLayout(0, 1, 10, 9, 41), W.SeqLayout(0, 1, 8, 8, 1))
     emb = W.embeddings(dims, layouts)
@@ -222,12 +233,12 @@ def test_packed_equals_alone_and_permutation(torch):
     sl = seq_slices(layouts)
     for i, s in enumerate(layouts):
         alone = _gpu_encode(torch, enc, dims, np.ascontiguousarray(emb[sl[i]]), [s])
-        np.testing.assert_array_equal(alone, full[sl[i]])
+        assert rel_err(alone, full[sl[i]]) <= 1e-4
     perm = [2, 0, 1]
     idx = np.concatenate([np.arange(sl[i].start, sl[i].stop) for i in perm])
     out = _gpu_encode(torch, enc, dims, np.ascontiguousarray(emb[idx]), [layouts[i] for i in perm])
     enc.close()
-    np.testing.assert_array_equal(out, full[idx])
+    assert rel_err(out, full[idx]) <= 1e-4
 
 
 def test_graph_capture_replays_match_eager(torch):
@@ -253,7 +264,9 @@ def test_graph_capture_replays_match_eager(torch):
         out.fill_(float("nan"))
         g.replay()
         torch.cuda.synchronize()
-        assert torch.equal(out, eager), r
+        assert bool(torch.isfinite(out).all()), r
+        d = (out.float() - eager.float()).abs().max() / eager.float().pow(2).mean().sqrt()
+        assert d.item() <= 1e-5, (r, d.item())
         enc.encode(x, pos, lens)   # eager work between replays
         torch.cuda.synchronize()
     enc.close()
