@@ -75,8 +75,10 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   constexpr int ND = HD / 32;                    // 32-wide d blocks
   typedef typename Frag<T>::type frag_t;
 
+  constexpr int OTP = HD + 4;                     // padded output staging row (floats)
   __shared__ u32x4 sK[NP][KV * NCH];
-  __shared__ T sVt[NP][HD * VTP];
+  __shared__ __attribute__((aligned(16))) T sVt[NP][HD * VTP];
+  __shared__ __attribute__((aligned(16))) float sO[4][32 * OTP];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lrow = lane & 31, lgrp = lane >> 5;
@@ -139,37 +141,76 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const int my_q = qw + lrow;
 
   const int n_blocks = (q_last >= 0) ? (q_last / KV + 1) : 0;
-  for (int kb = 0; kb < n_blocks; ++kb) {
-    const int kv0 = kb * KV;
-    // Stage K (row-major, swizzled) and V (transposed) of tokens kv0..kv0+31.
-    for (int idx = tid; idx < KV * NCH; idx += 256) {
-      const int r = idx / NCH, c = idx % NCH;
-      float kx[EC], vx[EC];
+  // Staging of one key/value tile through registers, one tile ahead:
+  //  K: thread chunk (row r, chunk c) of EC consecutive d -> sK[r][c] (swizzled);
+  //  V: thread (column d, row group v) reads EC rows of column d (lanes
+  //     take consecutive d, so each load is one coalesced row segment) and
+  //     writes them as a row segment of V^T: sVt[d][v*EC .. v*EC+EC).
+  constexpr int KCH = KV * NCH / 256;             // K chunks per thread
+  constexpr int VCH = HD * (KV / EC) / 256;       // V column groups per thread
+  static_assert(KCH * 256 == KV * NCH && VCH * 256 == HD * (KV / EC), "staging split");
+  float kx[KCH][EC], vx[VCH][EC];
+  auto gload = [&](int kv0) {
 #pragma unroll
-      for (int e = 0; e < EC; ++e) kx[e] = vx[e] = 0.f;
+    for (int t = 0; t < KCH; ++t) {
+      const int idx = tid + t * 256, r = idx / NCH, c = idx % NCH;
       if (kv0 + r < L) {
-        const float *rp = base + (size_t)(kv0 + r) * ld;
+        const float *rp = base + (size_t)(kv0 + r) * ld + k_off + c * EC;
 #pragma unroll
         for (int e = 0; e < EC; e += 4) {
-          f32x4 kv = *(const f32x4 *)(rp + k_off + c * EC + e);
-          f32x4 vv = *(const f32x4 *)(rp + v_off + c * EC + e);
-          kx[e] = kv[0]; kx[e + 1] = kv[1]; kx[e + 2] = kv[2]; kx[e + 3] = kv[3];
-          vx[e] = vv[0]; vx[e + 1] = vv[1]; vx[e + 2] = vv[2]; vx[e + 3] = vv[3];
+          const f32x4 v = *(const f32x4 *)(rp + e);
+          kx[t][e] = v[0]; kx[t][e + 1] = v[1]; kx[t][e + 2] = v[2]; kx[t][e + 3] = v[3];
         }
+      } else {
+#pragma unroll
+        for (int e = 0; e < EC; ++e) kx[t][e] = 0.f;
       }
-      T ks[NP][EC], vs[NP][EC];
-      split_vals<T, NP, EC>(kx, ks);
-      split_vals<T, NP, EC>(vx, vs);
+    }
+#pragma unroll
+    for (int t = 0; t < VCH; ++t) {
+      const int idx = tid + t * 256, d = idx % HD, v = idx / HD;
+#pragma unroll
+      for (int e = 0; e < EC; ++e) {
+        const int r = kv0 + v * EC + e;
+        vx[t][e] = r < L ? base[(size_t)r * ld + v_off + d] : 0.f;
+      }
+    }
+  };
+  auto lstore = [&]() {
+#pragma unroll
+    for (int t = 0; t < KCH; ++t) {
+      const int idx = tid + t * 256, r = idx / NCH, c = idx % NCH;
+      T ks[NP][EC];
+      split_vals<T, NP, EC>(kx[t], ks);
 #pragma unroll
       for (int p = 0; p < NP; ++p) {
         u32x4 w;
         __builtin_memcpy(&w, ks[p], 16);
         sK[p][r * NCH + kswz<NCH>(r, c)] = w;
-#pragma unroll
-        for (int e = 0; e < EC; ++e) sVt[p][(c * EC + e) * VTP + r] = vs[p][e];
       }
     }
+#pragma unroll
+    for (int t = 0; t < VCH; ++t) {
+      const int idx = tid + t * 256, d = idx % HD, v = idx / HD;
+      T vs[NP][EC];
+      split_vals<T, NP, EC>(vx[t], vs);
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+        u32x2 w0, w1;
+        __builtin_memcpy(&w0, &vs[p][0], 8);
+        __builtin_memcpy(&w1, (const char *)&vs[p][0] + 8, 8);
+        u32x2 *dst = (u32x2 *)(sVt[p] + d * VTP + v * EC);
+        dst[0] = w0;
+        dst[1] = w1;
+      }
+    }
+  };
+  if (n_blocks > 0) gload(0);
+  for (int kb = 0; kb < n_blocks; ++kb) {
+    const int kv0 = kb * KV;
+    lstore();
     __syncthreads();
+    if (kb + 1 < n_blocks) gload(kv0 + KV);
 
     if (qw < L && kv0 <= wave_last) {
       f32x16 s;
@@ -246,25 +287,40 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     __syncthreads();
   }
 
+  // Output: each wave writes its normalised 32 x HD tile into LDS (row-major
+  // by query), then copies it out row by row so that the global stores are
+  // contiguous along d (a lane owns a query row in the accumulator layout,
+  // which would scatter 2-byte stores across rows).
+  const float lt = l_i + __shfl_xor(l_i, 32, kWave);
+  const float inv = 1.f / lt;
+  float *so = sO[wave];
+#pragma unroll
+  for (int n = 0; n < ND; ++n)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) so[lrow * OTP + n * 32 + acc_row(r, lane)] = oacc[n][r] * inv;
+  __builtin_amdgcn_s_waitcnt(0xc07f);   // this wave's LDS writes done (lgkmcnt 0)
+  __builtin_amdgcn_wave_barrier();
   if (qw < L) {
-    const float lt = l_i + __shfl_xor(l_i, 32, kWave);
-    const float inv = 1.f / lt;
-    if (my_q < L) {
-      const size_t ob = ((size_t)(s0 + my_q) * a.Hq + head) * HD;
+    constexpr int LPR = HD / 4;          // lanes per row (4 values each)
+    constexpr int RPI = 64 / LPR;        // rows per instruction
 #pragma unroll
-      for (int n = 0; n < ND; ++n)
+    for (int it = 0; it < 32 / RPI; ++it) {
+      const int q = it * RPI + lane / LPR, d = (lane % LPR) * 4;
+      if (qw + q >= L) continue;
+      const f32x4 y = *(const f32x4 *)(so + q * OTP + d);
+      const size_t o = ((size_t)(s0 + qw + q) * a.Hq + head) * HD + d;
+      if constexpr (MODE == MODE_F32) {
+        *(f32x4 *)((float *)a.o + o) = y;
+      } else {
+        bf16x4 h, l;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float y = oacc[n][r] * inv;
-          const size_t o = ob + n * 32 + acc_row(r, lane);
-          if constexpr (MODE == MODE_F32) {
-            ((float *)a.o)[o] = y;
-          } else {
-            const bf16 h = (bf16)y;
-            ((bf16 *)a.o)[o] = h;
-            ((bf16 *)a.o)[o + a.o_plane] = (bf16)(y - (float)h);
-          }
+        for (int e = 0; e < 4; ++e) {
+          h[e] = (bf16)y[e];
+          l[e] = (bf16)(y[e] - (float)h[e]);
         }
+        *(bf16x4 *)((bf16 *)a.o + o) = h;
+        *(bf16x4 *)((bf16 *)a.o + o + a.o_plane) = l;
+      }
     }
   }
 }
