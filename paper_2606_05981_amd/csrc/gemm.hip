@@ -72,10 +72,25 @@ __device__ __forceinline__ void wait_stages(int after) {
 }
 
 // 16-byte global -> LDS copy without a register round trip: lane i of the
-// wave writes lds_wave_base + 16*i (the LDS base must be wave-uniform).
-__device__ __forceinline__ void dma16(const void *g, void *lds_wave_base) {
-  __builtin_amdgcn_global_load_lds((const __attribute__((address_space(1))) void *)g,
-                                   (__attribute__((address_space(3))) void *)lds_wave_base, 16, 0, 0);
+// wave writes lds_base + 16*i, lds_base wave-uniform. Written as inline asm
+// on purpose: the compiler's waitcnt pass treats the builtin form as LDS
+// traffic and then drains every outstanding LDS read (lgkmcnt(0)) before
+// the MFMAs that follow a stage's loads. The asm form is invisible to that
+// pass; the kernel orders these loads itself with explicit vmcnt waits and
+// barriers, and waits for all of them before it ends.
+// M0 is saved and restored around the load (the compiler reserves it), and
+// one wait state separates the M0 write from the load that reads it.
+__device__ __forceinline__ void dma16(const void *g, uint32_t lds_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(g), "s"(lds_base)
+      : "memory");
 }
 
 // The main loop keeps P stages in an LDS ring filled by direct global->LDS
@@ -88,7 +103,7 @@ __device__ __forceinline__ void dma16(const void *g, void *lds_wave_base) {
 // run. Raw s_barrier (no fence) keeps the compiler from forcing vmcnt(0) at
 // the barrier; the waits are explicit.
 template <int MODE, int BM, int BN, int WM, int WN, int ROWB, int P, int EPI, int OCC>
-__global__ __launch_bounds__(256, OCC) void k_gemm(GemmArgs g) {
+__global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void k_gemm(GemmArgs g) {
   typedef typename std::conditional<MODE == MODE_F32, float, bf16>::type T;
   constexpr int NA = (MODE == MODE_BF16X2) ? 2 : 1;   // A planes
   constexpr int KS = ROWB / (int)sizeof(T);       // k elements per stage
@@ -129,15 +144,20 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(GemmArgs g) {
     pb[c] = g.W + (size_t)(n0 + r) * rowb + kb0 + ch * 16;
   }
   const ptrdiff_t lo_off = (MODE == MODE_BF16X2) ? (g.A_lo - g.A) : 0;
-  auto issue = [&](int kt) {
-    u32x4 *st = lds + (kt % P) * STAGE;
-    const size_t ko = (size_t)kt * ROWB;
+  // Loads K-stage `ks` into ring slot `slot`.
+  const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
+  const int uwave = __builtin_amdgcn_readfirstlane(wave);   // wave-uniform in an SGPR
+  auto issue = [&](int ks, int slot) {
+    const uint32_t st = lds0 + (uint32_t)(slot * STAGE) * 16u;
+    const size_t ko = (size_t)ks * ROWB;
 #pragma unroll
     for (int p = 0; p < NA; ++p)
 #pragma unroll
-      for (int c = 0; c < AR; ++c) dma16(pa[c] + p * lo_off + ko, st + p * ACH + (c * 4 + wave) * 64);
+      for (int c = 0; c < AR; ++c)
+        dma16(pa[c] + p * lo_off + ko, st + (uint32_t)(p * ACH + (c * 4 + uwave) * 64) * 16u);
 #pragma unroll
-    for (int c = 0; c < BR; ++c) dma16(pb[c] + ko, st + NA * ACH + (c * 4 + wave) * 64);
+    for (int c = 0; c < BR; ++c)
+      dma16(pb[c] + ko, st + (uint32_t)(NA * ACH + (c * 4 + uwave) * 64) * 16u);
   };
 
   f32x16 acc[TM][TN];
@@ -177,10 +197,13 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(GemmArgs g) {
   constexpr int KK = CH / 2;                      // 16-k steps per stage (even)
   static_assert(KK % 2 == 0, "fragment buffer parity");
 
+  // The loop body is branch-free (a branch between LDS reads and their
+  // use makes the waitcnt pass drain all outstanding reads): every iteration
+  // issues a stage -- past the end, a repeat of the last one into the slot
+  // just freed, which is never read -- so every wait is a fixed vmcnt.
 #pragma unroll
-  for (int s = 0; s < P - 1; ++s)
-    if (s < nk) issue(s);
-  wait_stages<LOADS>(min(P - 2, nk - 1));
+  for (int s = 0; s < P - 1; ++s) issue(min(s, nk - 1), s);
+  wait_vm<(P - 2) * LOADS>();
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
   load_frags(lds, 0, 0);
@@ -191,16 +214,20 @@ __global__ __launch_bounds__(256, OCC) void k_gemm(GemmArgs g) {
       const int cur = kk & 1;
       if (kk + 1 < KK) {
         load_frags(st, kk + 1, cur ^ 1);
-      } else if (kt + 1 < nk) {
-        wait_stages<LOADS>(max(0, min(P - 3, nk - 2 - kt)));
-        __builtin_amdgcn_s_barrier();
-        asm volatile("" ::: "memory");  // keep LDS reads of stage kt+1 below the barrier
-        if (kt + P - 1 < nk) issue(kt + P - 1);
+      } else {
+        wait_vm<(P - 3) * LOADS>();      // this wave's loads of stage kt+1 landed
+        __builtin_amdgcn_s_barrier();    // ... everyone's, and stage kt-1 is free
+        asm volatile("" ::: "memory");   // keep LDS reads of stage kt+1 below the barrier
+        issue(min(kt + P - 1, nk - 1), (kt + P - 1) % P);
         load_frags(lds + ((kt + 1) % P) * STAGE, 0, cur ^ 1);
       }
+      // Keep the prefetch above the MFMAs that hide its latency (the
+      // scheduler would otherwise sink the reads to shorten live ranges).
+      __builtin_amdgcn_sched_barrier(0);
       compute(cur);
     }
   }
+  wait_vm<0>();                          // no load may land after the workgroup ends
 
   // Epilogue.
 #pragma unroll
