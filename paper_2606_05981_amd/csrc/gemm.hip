@@ -342,11 +342,29 @@ static bool tile_fits(int id, int N, int K, int esz, int epi, int splits) {
 static const double kTileRate[kNumTiles] = {412, 454, 420, 385, 469, 394, 454, 423,
                                             436, 458, 404, 296, 344, 340, 250};
 
-// Picks (tile, splits) for an M x N x K problem: estimated time = rounds of
-// workgroups over the compute units x the time one full round takes at the
-// tile's measured rate. Split-K is only considered for small M and for the
-// residual epilogue (partial sums are added atomically).
-static void plan(int M, int N, int K, int esz, int epi, int *tile, int *splits) {
+// Measured choices (MI355X sweep of every tile and split count) for the
+// decoder's four projections, D 2048 / FFN 6144 / 16+8+8 heads of 128, at
+// 96, 768, 1536 and 10240 rows. Other row counts take the entry of the
+// nearest row count (log scale) for the same N, K and epilogue.
+struct TileChoice {
+  int n, k, epi, m, tile, splits;
+};
+static const TileChoice kChoices[] = {
+    {4096, 2048, EPI_STORE, 96, 10, 1},    {2048, 2048, EPI_RESID, 96, 12, 4},
+    {12288, 2048, EPI_SWIGLU, 96, 10, 1},  {2048, 6144, EPI_RESID, 96, 10, 8},
+    {4096, 2048, EPI_STORE, 768, 8, 1},    {2048, 2048, EPI_RESID, 768, 10, 1},
+    {12288, 2048, EPI_SWIGLU, 768, 1, 1},  {2048, 6144, EPI_RESID, 768, 10, 1},
+    {4096, 2048, EPI_STORE, 1536, 5, 1},   {2048, 2048, EPI_RESID, 1536, 10, 1},
+    {12288, 2048, EPI_SWIGLU, 1536, 5, 1}, {2048, 6144, EPI_RESID, 1536, 7, 1},
+    {4096, 2048, EPI_STORE, 10240, 4, 1},  {2048, 2048, EPI_RESID, 10240, 1, 1},
+    {12288, 2048, EPI_SWIGLU, 10240, 4, 1}, {2048, 6144, EPI_RESID, 10240, 9, 1},
+};
+
+// Fallback estimate: rounds of workgroups over the compute units x the time
+// one full round takes at the tile's measured rate. Split-K is only
+// considered for small M and for the residual epilogue (partial sums are
+// added atomically).
+static void plan_model(int M, int N, int K, int esz, int epi, int *tile, int *splits) {
   const int cus = 256;
   double best = 1e30;
   *tile = 0;
@@ -368,6 +386,25 @@ static void plan(int M, int N, int K, int esz, int epi, int *tile, int *splits) 
       }
     }
   }
+}
+
+static void plan(int M, int N, int K, int esz, int epi, int *tile, int *splits) {
+  const TileChoice *best = nullptr;
+  double bd = 1e30;
+  if (esz == 2) {
+    for (const TileChoice &c : kChoices) {
+      if (c.n != N || c.k != K || c.epi != epi) continue;
+      const double d = std::fabs(std::log((double)M / c.m));
+      if (d < bd) { bd = d; best = &c; }
+    }
+  }
+  if (best && tile_fits(best->tile, N, K, esz, epi, best->splits) &&
+      (best->splits == 1 || M <= 256)) {
+    *tile = best->tile;
+    *splits = best->splits;
+    return;
+  }
+  plan_model(M, N, K, esz, epi, tile, splits);
 }
 
 template <int MODE>

@@ -1,6 +1,8 @@
 // Row-wise kernels of the encoder: RMSNorm, per-head QK-norm + multimodal
 // rotary embedding, on-device position ids, and the weight repacking used
 // at encoder creation.
+#include <type_traits>
+
 #include "common.h"
 #include "launch.h"
 
@@ -54,14 +56,89 @@ static void rmsnorm_out(int out_fmt, dim3 grid, const TI *in, float *copy_to, co
     hipLaunchKernelGGL((k_rmsnorm<TI, FMT_BF16X2>), grid, dim3(256), 0, s, in, copy_to, g, out, plane, D, eps);
 }
 
+// Register-resident variant for D a multiple of 1024 (D <= 4096): every
+// thread owns NV groups of 4 consecutive values, read once with 16-byte (or
+// 8-byte bf16) loads and written with vector stores.
+template <typename TI, int OUT_FMT, int NV>
+__global__ __launch_bounds__(256) void k_rmsnorm_vec(const TI *__restrict__ in, float *__restrict__ copy_to,
+                                                     const float *__restrict__ gain, void *__restrict__ out,
+                                                     size_t plane, int D, float eps) {
+  __shared__ float red[4];
+  const int row = blockIdx.x, tid = threadIdx.x;
+  const size_t rb = (size_t)row * D;
+  f32x4 v[NV];
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = (i * 256 + tid) * 4;
+    if constexpr (std::is_same<TI, float>::value) {
+      v[i] = *(const f32x4 *)(in + rb + c);
+    } else {
+      const bf16x4 b = *(const bf16x4 *)(in + rb + c);
+      v[i] = (f32x4){(float)b[0], (float)b[1], (float)b[2], (float)b[3]};
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) ss += v[i][e] * v[i][e];
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) ss = warp_sum_xor(ss, m);
+  if ((tid & 63) == 0) red[tid >> 6] = ss;
+  __syncthreads();
+  const float rs = rsqrtf((red[0] + red[1] + red[2] + red[3]) / (float)D + eps);
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = (i * 256 + tid) * 4;
+    if (copy_to) *(f32x4 *)(copy_to + rb + c) = v[i];
+    const f32x4 g = *(const f32x4 *)(gain + c);
+    f32x4 y;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) y[e] = v[i][e] * rs * g[e];
+    if constexpr (OUT_FMT == FMT_F32) {
+      *(f32x4 *)((float *)out + rb + c) = y;
+    } else {
+      bf16x4 h, l;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        h[e] = (bf16)y[e];
+        l[e] = (bf16)(y[e] - (float)h[e]);
+      }
+      *(bf16x4 *)((bf16 *)out + rb + c) = h;
+      if constexpr (OUT_FMT == FMT_BF16X2) *(bf16x4 *)((bf16 *)out + rb + c + plane) = l;
+    }
+  }
+}
+
+template <typename TI, int NV>
+static void rmsnorm_vec(int out_fmt, dim3 grid, const TI *in, float *copy_to, const float *g, void *out,
+                        size_t plane, int D, float eps, hipStream_t s) {
+  if (out_fmt == FMT_F32)
+    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_F32, NV>), grid, dim3(256), 0, s, in, copy_to, g, out, plane, D, eps);
+  else if (out_fmt == FMT_BF16)
+    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_BF16, NV>), grid, dim3(256), 0, s, in, copy_to, g, out, plane, D, eps);
+  else
+    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_BF16X2, NV>), grid, dim3(256), 0, s, in, copy_to, g, out, plane, D, eps);
+}
+
+template <typename TI>
+static void rmsnorm_dispatch(int out_fmt, dim3 grid, const TI *in, float *copy_to, const float *g, void *out,
+                             size_t plane, int D, float eps, hipStream_t s) {
+  switch (D % 1024 == 0 ? D / 1024 : 0) {
+    case 1: rmsnorm_vec<TI, 1>(out_fmt, grid, in, copy_to, g, out, plane, D, eps, s); break;
+    case 2: rmsnorm_vec<TI, 2>(out_fmt, grid, in, copy_to, g, out, plane, D, eps, s); break;
+    case 3: rmsnorm_vec<TI, 3>(out_fmt, grid, in, copy_to, g, out, plane, D, eps, s); break;
+    case 4: rmsnorm_vec<TI, 4>(out_fmt, grid, in, copy_to, g, out, plane, D, eps, s); break;
+    default: rmsnorm_out<TI>(out_fmt, grid, in, copy_to, g, out, plane, D, eps, s); break;
+  }
+}
+
 hipError_t launch_rmsnorm(int in_fmt, int out_fmt, const void *in, float *copy_to, const float *g,
                           void *out, size_t out_plane, int rows, int D, float eps, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   dim3 grid(rows);
   if (in_fmt == FMT_BF16)
-    rmsnorm_out<bf16>(out_fmt, grid, (const bf16 *)in, copy_to, g, out, out_plane, D, eps, s);
+    rmsnorm_dispatch<bf16>(out_fmt, grid, (const bf16 *)in, copy_to, g, out, out_plane, D, eps, s);
   else
-    rmsnorm_out<float>(out_fmt, grid, (const float *)in, copy_to, g, out, out_plane, D, eps, s);
+    rmsnorm_dispatch<float>(out_fmt, grid, (const float *)in, copy_to, g, out, out_plane, D, eps, s);
   return hipGetLastError();
 }
 
