@@ -22,6 +22,33 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_gemm_b16_traffic.json")
+KERNEL_SOURCES = ["paper_2606_05981_amd/csrc/gemm.hip", "paper_2606_05981_amd/csrc/common.h",
+                  "paper_2606_05981_amd/csrc/launch.h"]
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM-side bytes per gate/up GEMM launch from the committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE, each divided by its copy-kernel calibration
+    factor); None when the summary is missing or the kernel sources changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    return (t["fetch_kib_per_launch"] / t["fetch_factor"] +
+            t["write_kib_per_launch"] / t["write_factor"]) * 1024.0
 
 
 def gemm_flops(dims, T):
@@ -167,6 +194,8 @@ def main():
     frames_s = len(main_run["lens"]) * K / main_run["wall_s"]
     n_launch, kern_ms = main_run["kern"]
     gu_flops = gemm_flops(dims, T)["gate_up"]
+    # weights (bf16) + normalised input (bf16 hi/lo) + SwiGLU output (bf16 hi/lo)
+    gu_bytes = 2 * dims.ffn * dims.hidden * 2 + T * dims.hidden * 4 + T * dims.ffn * 4
     avg_us = kern_ms * 1e3 / max(n_launch, 1)
     achieved = gu_flops / (avg_us * 1e-6) / 1e12
     total_tflops = step_flops(dims, main_run["lens"]) * K / main_run["wall_s"] / 1e12
@@ -193,7 +222,8 @@ def main():
         "model_tflops": round(total_tflops, 1),
         "roofline": {"kernel": "gate/up GEMM + SwiGLU", "bound": "mfma",
                      "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic(),
+                     "algorithmic_bytes_per_launch": gu_bytes,
                      "avg_launch_us": round(avg_us, 2), "launches": n_launch,
                      "flops_per_launch": gu_flops},
     }

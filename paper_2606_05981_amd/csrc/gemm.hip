@@ -117,7 +117,7 @@ __global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, O
   constexpr int STAGE = (NA * BM + BN) * CH;      // u32x4 slots per stage
   static_assert(WM * WN == 4, "4 waves");
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
-  static_assert(LOADS * (P - 2) < 64 && P >= 3 && P <= 5, "vmcnt range, ring depth");
+  static_assert(LOADS * (P - 2) < 64 && P >= 3 && P <= 6, "vmcnt range, ring depth");
   typedef typename Frag<T>::type frag_t;
 
   extern __shared__ u32x4 lds[];                  // [P][STAGE]
@@ -147,17 +147,17 @@ __global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, O
   // Loads K-stage `ks` into ring slot `slot`.
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
   const int uwave = __builtin_amdgcn_readfirstlane(wave);   // wave-uniform in an SGPR
-  auto issue = [&](int ks, int slot) {
+  // DMA load x (0 <= x < LOADS) of K-stage `ks` into ring slot `slot`.
+  auto dma_one = [&](int ks, int slot, int x) {
     const uint32_t st = lds0 + (uint32_t)(slot * STAGE) * 16u;
     const size_t ko = (size_t)ks * ROWB;
-#pragma unroll
-    for (int p = 0; p < NA; ++p)
-#pragma unroll
-      for (int c = 0; c < AR; ++c)
-        dma16(pa[c] + p * lo_off + ko, st + (uint32_t)(p * ACH + (c * 4 + uwave) * 64) * 16u);
-#pragma unroll
-    for (int c = 0; c < BR; ++c)
+    if (x < NA * AR) {
+      const int p = x / AR, c = x % AR;
+      dma16(pa[c] + p * lo_off + ko, st + (uint32_t)(p * ACH + (c * 4 + uwave) * 64) * 16u);
+    } else {
+      const int c = x - NA * AR;
       dma16(pb[c] + ko, st + (uint32_t)(NA * ACH + (c * 4 + uwave) * 64) * 16u);
+    }
   };
 
   f32x16 acc[TM][TN];
@@ -170,61 +170,100 @@ __global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, O
 
   frag_t fa[2][NA][TM], fb[2][TN];
   const int lrow = lane & 31, lgrp = lane >> 5;
-  auto load_frags = [&](const u32x4 *st, int kk, int b) {
-    const u32x4 *lb = st + NA * ACH;
+  // Fragment read x (0 <= x < NR) of k-step kk of the stage at `st` into
+  // buffer b, in the order the MFMAs consume them: the W fragments, then the
+  // A fragments of each plane.
+  auto read_one = [&](const u32x4 *st, int kk, int b, int x) {
     const int ch = kk * 2 + lgrp;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
+    if (x < TN) {
+      const int r = wn * WTN + x * 32 + lrow;
+      fb[b][x] = __builtin_bit_cast(frag_t, st[NA * ACH + r * CH + swz<CH>(r, ch)]);
+    } else {
+      const int p = (x - TN) / TM, i = (x - TN) % TM;
       const int r = wm * WTM + i * 32 + lrow;
-#pragma unroll
-      for (int p = 0; p < NA; ++p)
-        fa[b][p][i] = __builtin_bit_cast(frag_t, st[p * ACH + r * CH + swz<CH>(r, ch)]);
-    }
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int r = wn * WTN + j * 32 + lrow;
-      fb[b][j] = __builtin_bit_cast(frag_t, lb[r * CH + swz<CH>(r, ch)]);
+      fa[b][p][i] = __builtin_bit_cast(frag_t, st[p * ACH + r * CH + swz<CH>(r, ch)]);
     }
   };
-  auto compute = [&](int b) {
-#pragma unroll
-    for (int p = 0; p < NA; ++p)
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) mfma32(acc[i][j], fa[b][p][i], fb[b][j]);
+  auto mfma_one = [&](int b, int x) {
+    const int j = x % TN, i = (x / TN) % TM, p = x / (TN * TM);
+    mfma32(acc[i][j], fa[b][p][i], fb[b][j]);
   };
   constexpr int KK = CH / 2;                      // 16-k steps per stage (even)
   static_assert(KK % 2 == 0, "fragment buffer parity");
+  constexpr int NM = NA * TM * TN;                // MFMAs per k-step
+  constexpr int NR = NA * TM + TN;                // fragment reads per k-step
+  // The loads of one stage are issued in NPART parts: part 0 right after the
+  // barrier of stage kt-P+1, parts 1.. in the k-steps before the barrier of
+  // stage kt-P+2. With P >= 4 every stage still has P-3 whole stages of loads
+  // in flight behind it at the barrier that waits for it; P = 3 issues each
+  // stage whole, after the barrier.
+  constexpr int NPART = (P >= 4) ? KK : 1;
+  constexpr int PART = (LOADS + NPART - 1) / NPART;
+
+  // One k-step: the NM MFMAs on fragment buffer `cur`, with the side work
+  // spread between them in issue order -- the NR fragment reads of the next
+  // k-step (k-step rkk of the stage at rst, into buffer cur^1), then DMA
+  // loads [d0, d1) of stage ks into slot `slot`. With `bar`, the barrier of
+  // the stage (after this wave's loads of the next stage have landed) goes
+  // after the first MFMA, ahead of all side work.
+  // Each unit of side work is pinned behind its MFMA by a scheduling
+  // barrier, so the matrix core keeps busy while it issues.
+  auto kstep = [&](int cur, const u32x4 *rst, int rkk, int ks, int slot, int d0, int d1, bool bar) {
+    const int nside = NR + (d1 - d0);
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      mfma_one(cur, m);
+      if (bar && m == 0) {
+        wait_vm<(P - 3) * LOADS>();        // this wave's loads of the next stage landed
+        __builtin_amdgcn_s_barrier();      // ... everyone's, and the previous stage is free
+        asm volatile("" ::: "memory");     // keep LDS reads of the next stage below it
+      }
+      const int s0 = (m * nside + NM - 1) / NM, s1 = ((m + 1) * nside + NM - 1) / NM;
+#pragma unroll
+      for (int x = s0; x < s1; ++x) {
+        if (x < NR) read_one(rst, rkk, cur ^ 1, x);
+        else dma_one(ks, slot, d0 + x - NR);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
 
   // The loop body is branch-free (a branch between LDS reads and their
   // use makes the waitcnt pass drain all outstanding reads): every iteration
-  // issues a stage -- past the end, a repeat of the last one into the slot
-  // just freed, which is never read -- so every wait is a fixed vmcnt.
+  // issues its loads -- past the end, repeats of the last stage into slots
+  // that are never read again -- so every wait is a fixed vmcnt.
+  // Prologue: stages 0..P-3 whole and part 0 of stage P-2 (P = 3: stages
+  // 0..P-2 whole), then stage 0 must have landed.
+  constexpr int PRE_FULL = (NPART > 1) ? P - 2 : P - 1;
+  constexpr int PRE_PART = (NPART > 1) ? (PART < LOADS ? PART : LOADS) : 0;
 #pragma unroll
-  for (int s = 0; s < P - 1; ++s) issue(min(s, nk - 1), s);
-  wait_vm<(P - 2) * LOADS>();
+  for (int s = 0; s < PRE_FULL; ++s)
+#pragma unroll
+    for (int x = 0; x < LOADS; ++x) dma_one(min(s, nk - 1), s, x);
+#pragma unroll
+  for (int x = 0; x < PRE_PART; ++x) dma_one(min(P - 2, nk - 1), P - 2, x);
+  wait_vm<(PRE_FULL - 1) * LOADS + PRE_PART>();
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
-  load_frags(lds, 0, 0);
+#pragma unroll
+  for (int x = 0; x < NR; ++x) read_one(lds, 0, 0, x);
   for (int kt = 0; kt < nk; ++kt) {
     const u32x4 *st = lds + (kt % P) * STAGE;
+    const u32x4 *nx = lds + ((kt + 1) % P) * STAGE;
+    const int ksa = min(kt + P - 2, nk - 1), sla = (kt + P - 2) % P;   // parts 1.. issued here
+    const int ksb = min(kt + P - 1, nk - 1), slb = (kt + P - 1) % P;   // part 0 issued here
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const int cur = kk & 1;
       if (kk + 1 < KK) {
-        load_frags(st, kk + 1, cur ^ 1);
+        const int q = kk + 1;                       // DMA part of this k-step
+        const int d0 = (NPART > 1) ? min(q * PART, LOADS) : 0;
+        const int d1 = (NPART > 1) ? min((q + 1) * PART, LOADS) : 0;
+        kstep(cur, st, kk + 1, ksa, sla, d0, d1, false);
       } else {
-        wait_vm<(P - 3) * LOADS>();      // this wave's loads of stage kt+1 landed
-        __builtin_amdgcn_s_barrier();    // ... everyone's, and stage kt-1 is free
-        asm volatile("" ::: "memory");   // keep LDS reads of stage kt+1 below the barrier
-        issue(min(kt + P - 1, nk - 1), (kt + P - 1) % P);
-        load_frags(lds + ((kt + 1) % P) * STAGE, 0, cur ^ 1);
+        const int d1 = (NPART > 1) ? min(PART, LOADS) : LOADS;
+        kstep(cur, nx, 0, ksb, slb, 0, d1, true);
       }
-      // Keep the prefetch above the MFMAs that hide its latency (the
-      // scheduler would otherwise sink the reads to shorten live ranges).
-      __builtin_amdgcn_sched_barrier(0);
-      compute(cur);
     }
   }
   wait_vm<0>();                          // no load may land after the workgroup ends
@@ -308,7 +347,10 @@ static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
   X(11, 32, 256, 1, 4, 128, 3, 1)            \
   X(12, 32, 128, 1, 4, 128, 3, 2)            \
   X(13, 128, 64, 4, 1, 64, 4, 2)             \
-  X(14, 192, 64, 2, 2, 64, 4, 1)
+  X(14, 192, 64, 2, 2, 64, 4, 1)             \
+  X(15, 192, 128, 2, 2, 64, 5, 1)            \
+  X(16, 128, 256, 2, 2, 64, 5, 1)            \
+  X(17, 128, 128, 2, 2, 64, 6, 1)
 
 static const TileCfg kTiles[] = {
 #define MTE_TILE_INFO(id, bm, bn, wm, wn, rowb, p, occ) {bm, bn, wm, wn, rowb, occ},
@@ -340,7 +382,7 @@ static bool tile_fits(int id, int N, int K, int esz, int epi, int splits) {
 // Steady-state throughput of each tile (algorithmic TFLOP/s of a bf16x2
 // GEMM at M = 10240, measured on MI355X); the planner's only calibration.
 static const double kTileRate[kNumTiles] = {412, 454, 420, 385, 469, 394, 454, 423,
-                                            436, 458, 404, 296, 344, 340, 250};
+                                            436, 458, 404, 296, 344, 340, 250, 394, 469, 454};
 
 // Measured choices (MI355X sweep of every tile and split count) for the
 // decoder's four projections, D 2048 / FFN 6144 / 16+8+8 heads of 128, at
@@ -354,8 +396,8 @@ static const TileChoice kChoices[] = {
     {12288, 2048, EPI_SWIGLU, 96, 10, 1},  {2048, 6144, EPI_RESID, 96, 10, 8},
     {4096, 2048, EPI_STORE, 768, 8, 1},    {2048, 2048, EPI_RESID, 768, 10, 1},
     {12288, 2048, EPI_SWIGLU, 768, 1, 1},  {2048, 6144, EPI_RESID, 768, 10, 1},
-    {4096, 2048, EPI_STORE, 1536, 5, 1},   {2048, 2048, EPI_RESID, 1536, 10, 1},
-    {12288, 2048, EPI_SWIGLU, 1536, 5, 1}, {2048, 6144, EPI_RESID, 1536, 7, 1},
+    {4096, 2048, EPI_STORE, 1536, 4, 1},   {2048, 2048, EPI_RESID, 1536, 17, 1},
+    {12288, 2048, EPI_SWIGLU, 1536, 15, 1}, {2048, 6144, EPI_RESID, 1536, 17, 1},
     {4096, 2048, EPI_STORE, 10240, 4, 1},  {2048, 2048, EPI_RESID, 10240, 1, 1},
     {12288, 2048, EPI_SWIGLU, 10240, 4, 1}, {2048, 6144, EPI_RESID, 10240, 9, 1},
 };
