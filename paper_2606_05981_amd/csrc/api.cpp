@@ -5,6 +5,7 @@
 // and handed to the kernels by value.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -48,6 +49,10 @@ struct mte_encoder {
   float *qkv = nullptr;      // [max_tokens, (Hq + 2 Hkv) d] fp32
   void *attn = nullptr;      // [max_tokens, Hq d] attention output
   void *act = nullptr;       // [max_tokens, F] SwiGLU output
+  // Partial sums of K-split projections (small batches): written by one
+  // GEMM, added up by the kernel that consumes its product.
+  float *ws = nullptr;
+  size_t ws_elems = 0;
   RopeParams rope;
   // kernel timing
   int timing_class = -1;
@@ -154,6 +159,7 @@ void mte_encoder_destroy(mte_encoder *e) {
   hipFree(e->qkv);
   hipFree(e->attn);
   hipFree(e->act);
+  hipFree(e->ws);
   hipSetDevice(cur);
   delete e;
 }
@@ -196,6 +202,9 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
       hipMalloc(&e->attn, MT * Hq * d * 4) != hipSuccess ||
       hipMalloc(&e->act, MT * F * 4) != hipSuccess)
     return fail(MTE_E_OOM);
+  // K splits are planned for at most 256 rows and 8 splits.
+  e->ws_elems = 8 * std::min<size_t>(MT, 256) * std::max(std::max(nqkv, 2 * F), D);
+  if (hipMalloc((void **)&e->ws, e->ws_elems * sizeof(float)) != hipSuccess) return fail(MTE_E_OOM);
 
   // Repack the weights: fused [Wq; Wk; Wv], gate/up interleaved in blocks
   // of 32 rows, fp32 norm gains.
@@ -277,7 +286,8 @@ void *lo_plane(const mte_encoder *e, void *buf, size_t cols) {
 
 // Runs layers [l0, l1) on the fp32 residual stream `h` (T rows).
 hipError_t run_layers(mte_encoder *e, float *h, const int32_t *pos, const std::vector<int32_t> &cu,
-                      int batch, int T, int l0, int l1, bool first_norm_done, hipStream_t s) {
+                      int batch, int T, int l0, int l1, bool first_norm_done, int *pending,
+                      hipStream_t s) {
   const mte_config &c = e->cfg;
   const int D = c.hidden, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
   const int nqkv = (Hq + 2 * Hkv) * d;
@@ -285,37 +295,50 @@ hipError_t run_layers(mte_encoder *e, float *h, const int32_t *pos, const std::v
   const int mode = e->mode, af = e->act_fmt;
   void *xn_lo = lo_plane(e, e->xn, D), *attn_lo = lo_plane(e, e->attn, (size_t)Hq * d),
        *act_lo = lo_plane(e, e->act, F);
+  float *ws = e->ws;
+  const size_t wn = e->ws_elems;
+  // `*pending` counts the partial sums of a K-split residual projection
+  // still in ws, to be added into h by the next RMSNorm.
+  int np = *pending;
   hipError_t err = hipSuccess;
 #define MTE_TRY(x) do { err = (x); if (err != hipSuccess) return err; } while (0)
   for (int l = l0; l < l1; ++l) {
     const LayerW &W = e->layers[l];
     if (!(l == l0 && first_norm_done))
-      MTE_TRY(launch_rmsnorm(FMT_F32, af, h, nullptr, W.attn_norm, e->xn, MT * D, T, D, c.rms_eps, s));
+      MTE_TRY(launch_rmsnorm(FMT_F32, af, h, np ? h : nullptr, np ? ws : nullptr, np, W.attn_norm, e->xn, MT * D, T,
+                             D, c.rms_eps, s));
+    int sp = 0;
     {
       Timer t(e, 0, s);
-      MTE_TRY(launch_gemm(mode, EPI_STORE, e->xn, xn_lo, W.w_qkv, e->qkv, 0, T, nqkv, D, nqkv, s));
+      MTE_TRY(launch_gemm(mode, EPI_STORE, e->xn, xn_lo, W.w_qkv, e->qkv, 0, T, nqkv, D, nqkv, ws, wn,
+                          &sp, s));
     }
-    MTE_TRY(launch_qk_rope(e->qkv, pos, c.qk_norm ? W.q_norm : nullptr, W.k_norm, T, Hq, Hkv, d,
-                           c.rms_eps, e->rope, s));
+    MTE_TRY(launch_qk_rope(e->qkv, sp ? ws : nullptr, sp, pos, c.qk_norm ? W.q_norm : nullptr,
+                           W.k_norm, T, Hq, Hkv, d, c.rms_eps, e->rope, s));
     {
       Timer t(e, 1, s);
       MTE_TRY(launch_attention(mode, e->qkv, e->attn, MT * Hq * d, cu.data(), batch, Hq, Hkv, d, s));
     }
     {
       Timer t(e, 2, s);
-      MTE_TRY(launch_gemm(mode, EPI_RESID, e->attn, attn_lo, W.w_o, h, 0, T, D, Hq * d, D, s));
+      MTE_TRY(launch_gemm(mode, EPI_RESID, e->attn, attn_lo, W.w_o, h, 0, T, D, Hq * d, D, ws, wn, &np,
+                          s));
     }
-    MTE_TRY(launch_rmsnorm(FMT_F32, af, h, nullptr, W.mlp_norm, e->xn, MT * D, T, D, c.rms_eps, s));
+    MTE_TRY(launch_rmsnorm(FMT_F32, af, h, np ? h : nullptr, np ? ws : nullptr, np, W.mlp_norm, e->xn, MT * D, T, D,
+                           c.rms_eps, s));
     {
       Timer t(e, 3, s);
-      MTE_TRY(launch_gemm(mode, EPI_SWIGLU, e->xn, xn_lo, W.w_gu, e->act, MT * F, T, 2 * F, D, F, s));
+      MTE_TRY(launch_gemm(mode, EPI_SWIGLU, e->xn, xn_lo, W.w_gu, e->act, MT * F, T, 2 * F, D, F, ws,
+                          wn, &sp, s));
     }
+    if (sp) MTE_TRY(launch_swiglu_parts(af, ws, sp, T, F, e->act, MT * F, s));
     {
       Timer t(e, 4, s);
-      MTE_TRY(launch_gemm(mode, EPI_RESID, e->act, act_lo, W.w_d, h, 0, T, D, F, D, s));
+      MTE_TRY(launch_gemm(mode, EPI_RESID, e->act, act_lo, W.w_d, h, 0, T, D, F, D, ws, wn, &np, s));
     }
   }
 #undef MTE_TRY
+  *pending = np;
   return err;
 }
 
@@ -351,17 +374,19 @@ int mte_encode(mte_encoder *e, const void *embeds, const int32_t *pos_thw, const
   hipError_t err;
   const int out_fmt = in_fmt(c.out_dtype);
   if (c.n_layers == 0) {
-    err = launch_rmsnorm(in_fmt(c.dtype), out_fmt, embeds, nullptr, e->final_norm, out_hidden, 0, T,
-                         c.hidden, c.rms_eps, stream);
+    err = launch_rmsnorm(in_fmt(c.dtype), out_fmt, embeds, nullptr, nullptr, 0, e->final_norm,
+                         out_hidden, 0, T, c.hidden, c.rms_eps, stream);
     return err == hipSuccess ? MTE_OK : MTE_E_HIP;
   }
   // Layer 0's attention norm also seeds the fp32 residual stream from the embeddings.
-  err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, embeds, e->h, e->layers[0].attn_norm, e->xn,
-                       (size_t)c.max_tokens * c.hidden, T, c.hidden, c.rms_eps, stream);
-  if (err == hipSuccess) err = run_layers(e, e->h, pos_thw, cu, batch, T, 0, c.n_layers, true, stream);
+  err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, embeds, e->h, nullptr, 0, e->layers[0].attn_norm,
+                       e->xn, (size_t)c.max_tokens * c.hidden, T, c.hidden, c.rms_eps, stream);
+  int np = 0;
   if (err == hipSuccess)
-    err = launch_rmsnorm(FMT_F32, out_fmt, e->h, nullptr, e->final_norm, out_hidden, 0, T, c.hidden,
-                         c.rms_eps, stream);
+    err = run_layers(e, e->h, pos_thw, cu, batch, T, 0, c.n_layers, true, &np, stream);
+  if (err == hipSuccess)
+    err = launch_rmsnorm(FMT_F32, out_fmt, e->h, nullptr, np ? e->ws : nullptr, np, e->final_norm,
+                         out_hidden, 0, T, c.hidden, c.rms_eps, stream);
   return err == hipSuccess ? MTE_OK : MTE_E_HIP;
 }
 
@@ -381,8 +406,10 @@ int mte_encode_layers(mte_encoder *e, const float *h_in, const int32_t *pos_thw,
   DeviceGuard g(e->device);
   hipError_t err = hipSuccess;
   if (h_out != h_in) err = hipMemcpyAsync(h_out, h_in, bytes, hipMemcpyDeviceToDevice, stream);
+  int np = 0;
   if (err == hipSuccess)
-    err = run_layers(e, h_out, pos_thw, cu, batch, T, layer_begin, layer_end, false, stream);
+    err = run_layers(e, h_out, pos_thw, cu, batch, T, layer_begin, layer_end, false, &np, stream);
+  if (err == hipSuccess && np) err = launch_resid_add(h_out, e->ws, np, T, e->cfg.hidden, stream);
   return err == hipSuccess ? MTE_OK : MTE_E_HIP;
 }
 

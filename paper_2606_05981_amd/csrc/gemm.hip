@@ -25,7 +25,10 @@
 // Epilogues are fused: fp32 store (QKV), SwiGLU over interleaved gate/up
 // rows (MLP up-projection, written in the activation format) and
 // accumulation into the fp32 residual stream (attention output projection
-// and MLP down-projection).
+// and MLP down-projection). With K split over workgroups (small M), each
+// split stores its partial sum instead, and the kernel that consumes the
+// product adds the partials up in split order, so results do not depend on
+// the order in which workgroups finish.
 #include <cmath>
 #include <type_traits>
 
@@ -38,8 +41,9 @@ struct GemmArgs {
   const char *A;      // A (MODE_F32) or A_hi (MODE_BF16X2)
   const char *A_lo;   // A_lo plane (MODE_BF16X2)
   const char *W;
-  void *C;            // EPI_STORE / EPI_RESID / EPI_ATOMIC: float; EPI_SWIGLU: activation format
-  size_t c_plane;     // EPI_SWIGLU, MODE_BF16X2: elements between C_hi and C_lo planes
+  void *C;            // EPI_STORE / EPI_RESID / EPI_PARTIAL: float; EPI_SWIGLU: activation format
+  size_t c_plane;     // EPI_SWIGLU, MODE_BF16X2: elements between C_hi and C_lo planes;
+                      // EPI_PARTIAL: elements between the partial sums of two K splits
   int M, N, K, ldc;
   int k_chunk;        // K range of one split (gridDim.z splits)
 };
@@ -275,14 +279,13 @@ __global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, O
     for (int r = 0; r < 16; ++r) {
       const int m = m0 + wm * WTM + i * 32 + acc_row(r, lane);
       if (m >= M) continue;
-      if constexpr (EPI == EPI_STORE || EPI == EPI_RESID || EPI == EPI_ATOMIC) {
-        float *C = (float *)g.C;
+      if constexpr (EPI == EPI_STORE || EPI == EPI_RESID || EPI == EPI_PARTIAL) {
+        float *C = (float *)g.C + (EPI == EPI_PARTIAL ? (size_t)blockIdx.z * g.c_plane : 0);
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
           const size_t o = (size_t)m * g.ldc + n0 + wn * WTN + j * 32 + lrow;
-          if constexpr (EPI == EPI_STORE) C[o] = acc[i][j][r];
-          else if constexpr (EPI == EPI_RESID) C[o] += acc[i][j][r];
-          else atomicAdd(C + o, acc[i][j][r]);
+          if constexpr (EPI == EPI_RESID) C[o] += acc[i][j][r];
+          else C[o] = acc[i][j][r];
         }
       } else {
 #pragma unroll
@@ -350,7 +353,9 @@ static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
   X(14, 192, 64, 2, 2, 64, 4, 1)             \
   X(15, 192, 128, 2, 2, 64, 5, 1)            \
   X(16, 128, 256, 2, 2, 64, 5, 1)            \
-  X(17, 128, 128, 2, 2, 64, 6, 1)
+  X(17, 128, 128, 2, 2, 64, 6, 1)            \
+  X(18, 96, 128, 1, 4, 128, 4, 1)            \
+  X(19, 96, 128, 1, 4, 128, 3, 1)
 
 static const TileCfg kTiles[] = {
 #define MTE_TILE_INFO(id, bm, bn, wm, wn, rowb, p, occ) {bm, bn, wm, wn, rowb, occ},
@@ -382,18 +387,23 @@ static bool tile_fits(int id, int N, int K, int esz, int epi, int splits) {
 // Steady-state throughput of each tile (algorithmic TFLOP/s of a bf16x2
 // GEMM at M = 10240, measured on MI355X); the planner's only calibration.
 static const double kTileRate[kNumTiles] = {412, 454, 420, 385, 469, 394, 454, 423,
-                                            436, 458, 404, 296, 344, 340, 250, 394, 469, 454};
+                                            436, 458, 404, 296, 344, 340, 250, 394, 469, 454,
+                                            300, 300};
 
 // Measured choices (MI355X sweep of every tile and split count) for the
 // decoder's four projections, D 2048 / FFN 6144 / 16+8+8 heads of 128, at
-// 96, 768, 1536 and 10240 rows. Other row counts take the entry of the
-// nearest row count (log scale) for the same N, K and epilogue.
+// 96, 192, 768, 1536 and 10240 rows. Other row counts take the entry of the
+// nearest row count (log scale) for the same N, K and epilogue. `epi` is
+// the epilogue of the finished product; splits > 1 means the K splits
+// write partial sums that the consuming kernel adds up.
 struct TileChoice {
   int n, k, epi, m, tile, splits;
 };
 static const TileChoice kChoices[] = {
-    {4096, 2048, EPI_STORE, 96, 10, 1},    {2048, 2048, EPI_RESID, 96, 12, 4},
-    {12288, 2048, EPI_SWIGLU, 96, 10, 1},  {2048, 6144, EPI_RESID, 96, 10, 8},
+    {4096, 2048, EPI_STORE, 96, 13, 4},    {2048, 2048, EPI_RESID, 96, 13, 8},
+    {12288, 2048, EPI_SWIGLU, 96, 18, 2},  {2048, 6144, EPI_RESID, 96, 18, 8},
+    {4096, 2048, EPI_STORE, 192, 18, 4},   {2048, 2048, EPI_RESID, 192, 10, 4},
+    {12288, 2048, EPI_SWIGLU, 192, 5, 2},  {2048, 6144, EPI_RESID, 192, 18, 8},
     {4096, 2048, EPI_STORE, 768, 8, 1},    {2048, 2048, EPI_RESID, 768, 10, 1},
     {12288, 2048, EPI_SWIGLU, 768, 1, 1},  {2048, 6144, EPI_RESID, 768, 10, 1},
     {4096, 2048, EPI_STORE, 1536, 4, 1},   {2048, 2048, EPI_RESID, 1536, 17, 1},
@@ -404,17 +414,17 @@ static const TileChoice kChoices[] = {
 
 // Fallback estimate: rounds of workgroups over the compute units x the time
 // one full round takes at the tile's measured rate. Split-K is only
-// considered for small M and for the residual epilogue (partial sums are
-// added atomically).
-static void plan_model(int M, int N, int K, int esz, int epi, int *tile, int *splits) {
+// considered for small M, and only where the partial sums fit `ws_elems`.
+static void plan_model(int M, int N, int K, int esz, int epi, size_t ws_elems, int *tile,
+                       int *splits) {
   const int cus = 256;
   double best = 1e30;
-  *tile = 0;
+  *tile = -1;
   *splits = 1;
   for (int id = 0; id < kNumTiles; ++id) {
     for (int sp = 1; sp <= 8; sp *= 2) {
-      if (sp > 1 && (epi != EPI_RESID || M > 256)) continue;
-      if (!tile_fits(id, N, K, esz, epi, sp)) continue;
+      if (sp > 1 && (M > 256 || (size_t)sp * M * N > ws_elems)) continue;
+      if (!tile_fits(id, N, K, esz, sp > 1 ? EPI_PARTIAL : epi, sp)) continue;
       const TileCfg &t = kTiles[id];
       const double tiles = (double)(N / t.bn) * ((M + t.bm - 1) / t.bm) * sp;
       const double slots = (double)cus * t.occ;
@@ -430,7 +440,7 @@ static void plan_model(int M, int N, int K, int esz, int epi, int *tile, int *sp
   }
 }
 
-static void plan(int M, int N, int K, int esz, int epi, int *tile, int *splits) {
+static void plan(int M, int N, int K, int esz, int epi, size_t ws_elems, int *tile, int *splits) {
   const TileChoice *best = nullptr;
   double bd = 1e30;
   if (esz == 2) {
@@ -440,13 +450,13 @@ static void plan(int M, int N, int K, int esz, int epi, int *tile, int *splits) 
       if (d < bd) { bd = d; best = &c; }
     }
   }
-  if (best && tile_fits(best->tile, N, K, esz, epi, best->splits) &&
-      (best->splits == 1 || M <= 256)) {
+  if (best && tile_fits(best->tile, N, K, esz, best->splits > 1 ? EPI_PARTIAL : epi, best->splits) &&
+      (best->splits == 1 || (M <= 256 && (size_t)best->splits * M * N <= ws_elems))) {
     *tile = best->tile;
     *splits = best->splits;
     return;
   }
-  plan_model(M, N, K, esz, epi, tile, splits);
+  plan_model(M, N, K, esz, epi, ws_elems, tile, splits);
 }
 
 template <int MODE>
@@ -454,10 +464,8 @@ static hipError_t launch_mode(int epi, int tile, int splits, const GemmArgs &a, 
   switch (epi) {
     case EPI_STORE: return run_id<MODE, EPI_STORE>(tile, a, splits, s);
     case EPI_SWIGLU: return run_id<MODE, EPI_SWIGLU>(tile, a, splits, s);
-    case EPI_RESID:
-      return splits > 1 ? run_id<MODE, EPI_ATOMIC>(tile, a, splits, s)
-                        : run_id<MODE, EPI_RESID>(tile, a, splits, s);
-    default: return run_id<MODE, EPI_ATOMIC>(tile, a, splits, s);
+    case EPI_RESID: return run_id<MODE, EPI_RESID>(tile, a, splits, s);
+    default: return run_id<MODE, EPI_PARTIAL>(tile, a, splits, s);
   }
 }
 
@@ -466,7 +474,8 @@ hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void 
                             hipStream_t s) {
   if (M <= 0) return hipSuccess;
   const int esz = mode == MODE_BF16X2 ? 2 : 4;
-  if (tile < 0 || tile >= kNumTiles || splits < 1 || !tile_fits(tile, N, K, esz, epi, splits))
+  if (tile < 0 || tile >= kNumTiles || splits < 1 || !tile_fits(tile, N, K, esz, epi, splits) ||
+      (splits > 1 && epi != EPI_PARTIAL))
     return hipErrorInvalidValue;
   GemmArgs a{(const char *)A, (const char *)A_lo, (const char *)W, C, c_plane, M, N, K, ldc, K / splits};
   return mode == MODE_BF16X2 ? launch_mode<MODE_BF16X2>(epi, tile, splits, a, s)
@@ -474,11 +483,19 @@ hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void 
 }
 
 hipError_t launch_gemm(int mode, int epi, const void *A, const void *A_lo, const void *W, void *C,
-                       size_t c_plane, int M, int N, int K, int ldc, hipStream_t s) {
+                       size_t c_plane, int M, int N, int K, int ldc, float *ws, size_t ws_elems,
+                       int *splits_out, hipStream_t s) {
+  *splits_out = 0;
   if (M <= 0) return hipSuccess;
   int tile, splits;
-  plan(M, N, K, mode == MODE_BF16X2 ? 2 : 4, epi, &tile, &splits);
-  return launch_gemm_tile(mode, epi, tile, splits, A, A_lo, W, C, c_plane, M, N, K, ldc, s);
+  plan(M, N, K, mode == MODE_BF16X2 ? 2 : 4, epi, ws ? ws_elems : 0, &tile, &splits);
+  if (tile < 0) return hipErrorInvalidValue;
+  if (splits > 1) {
+    *splits_out = splits;
+    return launch_gemm_tile(mode, EPI_PARTIAL, tile, splits, A, A_lo, W, ws, (size_t)M * N, M, N, K,
+                            N, s);
+  }
+  return launch_gemm_tile(mode, epi, tile, 1, A, A_lo, W, C, c_plane, M, N, K, ldc, s);
 }
 
 }  // namespace mte

@@ -25,40 +25,63 @@ enum Epilogue {
   EPI_SWIGLU = 1,  // gate/up rows interleaved in blocks of 32: C[m, f] = silu(gate) * up,
                    // written as float (MODE_F32) or bf16 hi/lo planes (MODE_BF16X2)
   EPI_RESID = 2,   // C (float residual stream) [m, n] += acc
-  EPI_ATOMIC = 3,  // C (float) [m, n] += acc with atomics (split-K partial sums)
+  EPI_PARTIAL = 3, // C (float) + split * c_plane [m, n] = acc: the partial sum of one K split
 };
 
 // C = A[M, K] * W[N, K]^T. MODE_F32: A, W float. MODE_BF16X2: A = A_hi + A_lo
 // (bf16 planes), W bf16. ldc: C's row pitch in elements; c_plane: distance
 // in elements between the hi and lo planes of a bf16x2 C.
+// The planner may split K (small M only) when the partial sums fit the
+// workspace ws (ws_elems floats; ws may be null): the product is then NOT
+// finished -- *splits_out (> 1) partial sums [M, N] (row pitch N, M*N
+// elements apart) are left in ws, in split order, for the consumer to add
+// up and apply `epi` to (for EPI_SWIGLU: the raw interleaved gate/up
+// columns). Otherwise *splits_out = 0 and C holds the result.
 hipError_t launch_gemm(int mode, int epi, const void *A, const void *A_lo, const void *W, void *C,
-                       size_t c_plane, int M, int N, int K, int ldc, hipStream_t s);
+                       size_t c_plane, int M, int N, int K, int ldc, float *ws, size_t ws_elems,
+                       int *splits_out, hipStream_t s);
 
 // The same with an explicit tile configuration (index into the GEMM tile
-// table) and number of K splits; used for tuning. Returns
-// hipErrorInvalidValue if the tile does not fit the shape.
+// table) and number of K splits (> 1 only with EPI_PARTIAL); used for
+// tuning. Returns hipErrorInvalidValue if the tile does not fit the shape.
 hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void *A, const void *A_lo,
                             const void *W, void *C, size_t c_plane, int M, int N, int K, int ldc,
                             hipStream_t s);
 
-// Per-row RMSNorm: out[r, :] = in[r, :] / sqrt(mean(in[r,:]^2) + eps) * g.
-// in: `in_fmt` (FMT_F32 or FMT_BF16) [rows, D]; when copy_to != nullptr the
-// input row is also written to copy_to as float (seeds the fp32 residual
-// stream from the embeddings). g: float [D]. out: `out_fmt`, lo plane at
-// out + out_plane elements for FMT_BF16X2.
-hipError_t launch_rmsnorm(int in_fmt, int out_fmt, const void *in, float *copy_to, const float *g,
-                          void *out, size_t out_plane, int rows, int D, float eps, hipStream_t s);
+// Per-row RMSNorm: out[r, :] = x[r, :] / sqrt(mean(x[r,:]^2) + eps) * g with
+// x = in + parts[0] + ... + parts[nparts-1] (float [rows, D] partial sums,
+// rows*D elements apart, added in that order; parts may be null).
+// in: `in_fmt` (FMT_F32 or FMT_BF16) [rows, D]; when copy_to != nullptr x is
+// also written to copy_to as float (copy_to may be in: the residual stream
+// takes the partial sums this way). g: float [D]. out: `out_fmt`, lo plane
+// at out + out_plane elements for FMT_BF16X2.
+hipError_t launch_rmsnorm(int in_fmt, int out_fmt, const void *in, float *copy_to, const float *parts,
+                          int nparts, const float *g, void *out, size_t out_plane, int rows, int D,
+                          float eps, hipStream_t s);
+
+// h[rows, D] += parts[0] + ... + parts[nparts-1] (float partial sums, rows*D
+// elements apart, in that order). D a multiple of 4.
+hipError_t launch_resid_add(float *h, const float *parts, int nparts, int rows, int D, hipStream_t s);
+
+// out[r, f] = silu(gate) * up with gate and up summed from nparts partial
+// sums [rows, 2F] of the interleaved gate/up projection (block b of 64
+// columns: gate 32b..32b+31, then up 32b..32b+31). out: FMT_F32 float
+// [rows, F], or FMT_BF16X2 bf16 hi / lo planes out_plane elements apart.
+hipError_t launch_swiglu_parts(int out_fmt, const float *parts, int nparts, int rows, int F, void *out,
+                               size_t out_plane, hipStream_t s);
 
 struct RopeParams {
   double inv_freq[64];       // theta^(-2j/d) for pair j
   uint8_t axis[64];          // position axis (0 t, 1 h, 2 w) of pair j
 };
 
-// In-place per-head RMSNorm (when q_norm != nullptr) and multimodal rotary
-// embedding of the q and k heads of a packed fp32 qkv buffer [T, (Hq+2Hkv)*d].
-hipError_t launch_qk_rope(float *qkv, const int32_t *pos_thw, const float *q_norm,
-                          const float *k_norm, int T, int Hq, int Hkv, int d, float eps,
-                          const RopeParams &rp, hipStream_t s);
+// Per-head RMSNorm (when q_norm != nullptr) and multimodal rotary embedding
+// of the q and k heads of a packed fp32 qkv buffer [T, (Hq+2Hkv)*d]: in
+// place, or, with nparts partial sums of the projection in `parts` (T*nqkv
+// elements apart), summed from them into qkv (v heads copied).
+hipError_t launch_qk_rope(float *qkv, const float *parts, int nparts, const int32_t *pos_thw,
+                          const float *q_norm, const float *k_norm, int T, int Hq, int Hkv, int d,
+                          float eps, const RopeParams &rp, hipStream_t s);
 
 // Causal GQA attention over packed sequences. qkv: fp32 [T, (Hq+2Hkv)*d], q
 // heads first, then k, then v; o: [T, Hq*d] as float (MODE_F32) or bf16

@@ -9,18 +9,34 @@
 namespace mte {
 
 // ------------------------------------------------------------- RMSNorm
-// out = x / sqrt(mean(x^2) + eps) * g, one 256-thread block per row.
+// out = x / sqrt(mean(x^2) + eps) * g, one 256-thread block per row, where
+// x = in + the np partial sums parts[0..np) (pitch pstride elements), added
+// in that order. copy_to (may alias in) receives x as float.
 // OUT_FMT FMT_BF16X2 writes bf16 hi to out and bf16(y - hi) to out + plane.
+struct Parts {
+  const float *p;   // partial sums [np][rows, D]
+  int np;           // 0 .. kMaxParts
+  size_t stride;    // elements between two partial sums
+};
+constexpr int kMaxParts = 8;
+
+template <typename TI>
+__device__ __forceinline__ float row_in(const TI *x, const Parts &pt, size_t o) {
+  float v = to_f32(x[o]);
+  for (int k = 0; k < pt.np; ++k) v += pt.p[(size_t)k * pt.stride + o];
+  return v;
+}
+
 template <typename TI, int OUT_FMT>
-__global__ __launch_bounds__(256) void k_rmsnorm(const TI *__restrict__ in, float *__restrict__ copy_to,
+__global__ __launch_bounds__(256) void k_rmsnorm(const TI *in, float *copy_to, Parts pt,
                                                  const float *__restrict__ gain, void *__restrict__ out,
                                                  size_t plane, int D, float eps) {
   __shared__ float red[4];
   const int row = blockIdx.x, tid = threadIdx.x;
-  const TI *x = in + (size_t)row * D;
+  const size_t rb = (size_t)row * D;
   float ss = 0.f;
   for (int c = tid; c < D; c += 256) {
-    float v = to_f32(x[c]);
+    const float v = row_in(in, pt, rb + c);
     ss += v * v;
   }
 #pragma unroll
@@ -29,8 +45,8 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const TI *__restrict__ in, floa
   __syncthreads();
   const float rs = rsqrtf((red[0] + red[1] + red[2] + red[3]) / (float)D + eps);
   for (int c = tid; c < D; c += 256) {
-    const float v = to_f32(x[c]);
-    const size_t o = (size_t)row * D + c;
+    const size_t o = rb + c;
+    const float v = row_in(in, pt, o);   // same thread, same element: copy_to may alias in
     if (copy_to) copy_to[o] = v;
     const float y = v * rs * gain[c];
     if constexpr (OUT_FMT == FMT_F32) {
@@ -46,21 +62,21 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const TI *__restrict__ in, floa
 }
 
 template <typename TI>
-static void rmsnorm_out(int out_fmt, dim3 grid, const TI *in, float *copy_to, const float *g, void *out,
-                        size_t plane, int D, float eps, hipStream_t s) {
+static void rmsnorm_out(int out_fmt, dim3 grid, const TI *in, float *copy_to, const Parts &pt,
+                        const float *g, void *out, size_t plane, int D, float eps, hipStream_t s) {
   if (out_fmt == FMT_F32)
-    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_F32>), grid, dim3(256), 0, s, in, copy_to, g, out, plane, D, eps);
+    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_F32>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, plane, D, eps);
   else if (out_fmt == FMT_BF16)
-    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_BF16>), grid, dim3(256), 0, s, in, copy_to, g, out, plane, D, eps);
+    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_BF16>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, plane, D, eps);
   else
-    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_BF16X2>), grid, dim3(256), 0, s, in, copy_to, g, out, plane, D, eps);
+    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_BF16X2>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, plane, D, eps);
 }
 
 // Register-resident variant for D a multiple of 1024 (D <= 4096): every
 // thread owns NV groups of 4 consecutive values, read once with 16-byte (or
 // 8-byte bf16) loads and written with vector stores.
 template <typename TI, int OUT_FMT, int NV>
-__global__ __launch_bounds__(256) void k_rmsnorm_vec(const TI *__restrict__ in, float *__restrict__ copy_to,
+__global__ __launch_bounds__(256) void k_rmsnorm_vec(const TI *in, float *copy_to, Parts pt,
                                                      const float *__restrict__ gain, void *__restrict__ out,
                                                      size_t plane, int D, float eps) {
   __shared__ float red[4];
@@ -77,6 +93,15 @@ __global__ __launch_bounds__(256) void k_rmsnorm_vec(const TI *__restrict__ in, 
       const bf16x4 b = *(const bf16x4 *)(in + rb + c);
       v[i] = (f32x4){(float)b[0], (float)b[1], (float)b[2], (float)b[3]};
     }
+    f32x4 q[kMaxParts];
+#pragma unroll
+    for (int k = 0; k < kMaxParts; ++k)     // all loads first, then the adds in split order
+      if (k < pt.np) q[k] = *(const f32x4 *)(pt.p + (size_t)k * pt.stride + rb + c);
+#pragma unroll
+    for (int k = 0; k < kMaxParts; ++k)
+      if (k < pt.np)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[i][e] += q[k][e];
 #pragma unroll
     for (int e = 0; e < 4; ++e) ss += v[i][e] * v[i][e];
   }
@@ -109,46 +134,128 @@ __global__ __launch_bounds__(256) void k_rmsnorm_vec(const TI *__restrict__ in, 
 }
 
 template <typename TI, int NV>
-static void rmsnorm_vec(int out_fmt, dim3 grid, const TI *in, float *copy_to, const float *g, void *out,
-                        size_t plane, int D, float eps, hipStream_t s) {
+static void rmsnorm_vec(int out_fmt, dim3 grid, const TI *in, float *copy_to, const Parts &pt,
+                        const float *g, void *out, size_t plane, int D, float eps, hipStream_t s) {
   if (out_fmt == FMT_F32)
-    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_F32, NV>), grid, dim3(256), 0, s, in, copy_to, g, out, plane, D, eps);
+    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_F32, NV>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, plane, D, eps);
   else if (out_fmt == FMT_BF16)
-    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_BF16, NV>), grid, dim3(256), 0, s, in, copy_to, g, out, plane, D, eps);
+    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_BF16, NV>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, plane, D, eps);
   else
-    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_BF16X2, NV>), grid, dim3(256), 0, s, in, copy_to, g, out, plane, D, eps);
+    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_BF16X2, NV>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, plane, D, eps);
 }
 
 template <typename TI>
-static void rmsnorm_dispatch(int out_fmt, dim3 grid, const TI *in, float *copy_to, const float *g, void *out,
-                             size_t plane, int D, float eps, hipStream_t s) {
+static void rmsnorm_dispatch(int out_fmt, dim3 grid, const TI *in, float *copy_to, const Parts &pt,
+                             const float *g, void *out, size_t plane, int D, float eps, hipStream_t s) {
   switch (D % 1024 == 0 ? D / 1024 : 0) {
-    case 1: rmsnorm_vec<TI, 1>(out_fmt, grid, in, copy_to, g, out, plane, D, eps, s); break;
-    case 2: rmsnorm_vec<TI, 2>(out_fmt, grid, in, copy_to, g, out, plane, D, eps, s); break;
-    case 3: rmsnorm_vec<TI, 3>(out_fmt, grid, in, copy_to, g, out, plane, D, eps, s); break;
-    case 4: rmsnorm_vec<TI, 4>(out_fmt, grid, in, copy_to, g, out, plane, D, eps, s); break;
-    default: rmsnorm_out<TI>(out_fmt, grid, in, copy_to, g, out, plane, D, eps, s); break;
+    case 1: rmsnorm_vec<TI, 1>(out_fmt, grid, in, copy_to, pt, g, out, plane, D, eps, s); break;
+    case 2: rmsnorm_vec<TI, 2>(out_fmt, grid, in, copy_to, pt, g, out, plane, D, eps, s); break;
+    case 3: rmsnorm_vec<TI, 3>(out_fmt, grid, in, copy_to, pt, g, out, plane, D, eps, s); break;
+    case 4: rmsnorm_vec<TI, 4>(out_fmt, grid, in, copy_to, pt, g, out, plane, D, eps, s); break;
+    default: rmsnorm_out<TI>(out_fmt, grid, in, copy_to, pt, g, out, plane, D, eps, s); break;
   }
 }
 
-hipError_t launch_rmsnorm(int in_fmt, int out_fmt, const void *in, float *copy_to, const float *g,
-                          void *out, size_t out_plane, int rows, int D, float eps, hipStream_t s) {
+hipError_t launch_rmsnorm(int in_fmt, int out_fmt, const void *in, float *copy_to, const float *parts,
+                          int nparts, const float *g, void *out, size_t out_plane, int rows, int D,
+                          float eps, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
+  if (parts && nparts > kMaxParts) return hipErrorInvalidValue;
   dim3 grid(rows);
+  const Parts pt{parts, parts ? nparts : 0, (size_t)rows * D};
   if (in_fmt == FMT_BF16)
-    rmsnorm_dispatch<bf16>(out_fmt, grid, (const bf16 *)in, copy_to, g, out, out_plane, D, eps, s);
+    rmsnorm_dispatch<bf16>(out_fmt, grid, (const bf16 *)in, copy_to, pt, g, out, out_plane, D, eps, s);
   else
-    rmsnorm_dispatch<float>(out_fmt, grid, (const float *)in, copy_to, g, out, out_plane, D, eps, s);
+    rmsnorm_dispatch<float>(out_fmt, grid, (const float *)in, copy_to, pt, g, out, out_plane, D, eps, s);
+  return hipGetLastError();
+}
+
+// h[r, c] += parts[0][r, c] + ... + parts[np-1][r, c], in that order.
+__global__ __launch_bounds__(256) void k_resid_add(float *__restrict__ h, Parts pt, size_t n4) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n4) return;
+  f32x4 v = ((const f32x4 *)h)[i];
+  f32x4 q[kMaxParts];
+#pragma unroll
+  for (int k = 0; k < kMaxParts; ++k)
+    if (k < pt.np) q[k] = ((const f32x4 *)(pt.p + (size_t)k * pt.stride))[i];
+#pragma unroll
+  for (int k = 0; k < kMaxParts; ++k)
+    if (k < pt.np)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] += q[k][e];
+  ((f32x4 *)h)[i] = v;
+}
+
+hipError_t launch_resid_add(float *h, const float *parts, int nparts, int rows, int D, hipStream_t s) {
+  const size_t n = (size_t)rows * D;
+  if (n == 0 || nparts <= 0) return hipSuccess;
+  if (nparts > kMaxParts || D % 4) return hipErrorInvalidValue;
+  const Parts pt{parts, nparts, n};
+  hipLaunchKernelGGL(k_resid_add, dim3((unsigned)((n / 4 + 255) / 256)), dim3(256), 0, s, h, pt, n / 4);
+  return hipGetLastError();
+}
+
+// SwiGLU of summed gate/up partial sums. parts: np x [rows, 2F], gate and up
+// columns interleaved in blocks of 32 (block b: gate 32b.., then up 32b..).
+// out [rows, F]: float (OUT_FMT FMT_F32) or bf16 hi / lo planes `plane` apart.
+template <int OUT_FMT>
+__global__ __launch_bounds__(256) void k_swiglu_parts(Parts pt, int F, void *__restrict__ out,
+                                                      size_t plane, size_t n) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;   // output element (r, f)
+  if (i >= n) return;
+  const size_t r = i / F;
+  const int f = (int)(i % F);
+  const size_t gc = r * 2 * F + 64 * (f >> 5) + (f & 31);
+  float qg[kMaxParts], qu[kMaxParts];
+#pragma unroll
+  for (int k = 0; k < kMaxParts; ++k)
+    if (k < pt.np) {
+      qg[k] = pt.p[(size_t)k * pt.stride + gc];
+      qu[k] = pt.p[(size_t)k * pt.stride + gc + 32];
+    }
+  float gt = qg[0], up = qu[0];
+#pragma unroll
+  for (int k = 1; k < kMaxParts; ++k)
+    if (k < pt.np) {
+      gt += qg[k];
+      up += qu[k];
+    }
+  const float y = gt / (1.f + __expf(-gt)) * up;
+  if constexpr (OUT_FMT == FMT_F32) {
+    ((float *)out)[i] = y;
+  } else {
+    const bf16 hi = (bf16)y;
+    ((bf16 *)out)[i] = hi;
+    ((bf16 *)out)[i + plane] = (bf16)(y - (float)hi);
+  }
+}
+
+hipError_t launch_swiglu_parts(int out_fmt, const float *parts, int nparts, int rows, int F, void *out,
+                               size_t out_plane, hipStream_t s) {
+  const size_t n = (size_t)rows * F;
+  if (n == 0) return hipSuccess;
+  if (nparts < 1 || nparts > kMaxParts || F % 32) return hipErrorInvalidValue;
+  const Parts pt{parts, nparts, (size_t)rows * 2 * F};
+  dim3 grid((unsigned)((n + 255) / 256));
+  if (out_fmt == FMT_F32)
+    hipLaunchKernelGGL(k_swiglu_parts<FMT_F32>, grid, dim3(256), 0, s, pt, F, out, out_plane, n);
+  else
+    hipLaunchKernelGGL(k_swiglu_parts<FMT_BF16X2>, grid, dim3(256), 0, s, pt, F, out, out_plane, n);
   return hipGetLastError();
 }
 
 // ------------------------------------------------- QK-norm + M-RoPE
-// One block per token. The token's d/2 rotation angles are computed once
-// (float64 angle and sincos, rounded to fp32) and shared by its Hq + Hkv
-// query and key heads. Thread j of a head owns rotary pair (j, j + d/2);
-// a head's d/2 threads sit in one wave, so the per-head sum of squares of
-// the QK-norm is a butterfly over those lanes.
-__global__ __launch_bounds__(256) void k_qk_rope(float *__restrict__ qkv, const int32_t *__restrict__ pos,
+// Grid (token, item block). Items are the token's rotary pairs, head-major
+// (pair j of q/k head h is item h*d/2 + j; a head's d/2 items sit in one
+// wave, so the per-head sum of squares of the QK-norm is a butterfly over
+// those lanes), followed, when the projection arrives as partial sums
+// (split-K), by its v elements, which are summed (in split order) and
+// copied; without partial sums qkv is updated in place. Each block computes
+// the token's d/2 rotation angles (float64 angle and sincos, rounded to
+// fp32).
+__global__ __launch_bounds__(256) void k_qk_rope(float *__restrict__ qkv, Parts pt,
+                                                 const int32_t *__restrict__ pos,
                                                  const float *__restrict__ qn, const float *__restrict__ kn,
                                                  int T_tokens, int Hq, int Hkv, int d, float eps,
                                                  RopeParams rp) {
@@ -164,12 +271,26 @@ __global__ __launch_bounds__(256) void k_qk_rope(float *__restrict__ qkv, const 
     sn[tid] = (float)sv;
   }
   __syncthreads();
-  const int nh = Hq + Hkv;
-  float *row = qkv + (size_t)tok * (Hq + 2 * Hkv) * d;
-  for (int t = tid; t < nh * half; t += 256) {
-    const int h = t / half, j = t % half;
-    float *z = row + h * d;
-    float u = z[j], w = z[j + half];
+  const int nh = Hq + Hkv, nqkv = (Hq + 2 * Hkv) * d;
+  float *row = qkv + (size_t)tok * nqkv;
+  const float *prow = pt.p + (size_t)tok * nqkv;
+  auto ld = [&](int c) -> float {
+    if (pt.np == 0) return row[c];
+    float q[kMaxParts];
+#pragma unroll
+    for (int k = 0; k < kMaxParts; ++k)
+      if (k < pt.np) q[k] = prow[(size_t)k * pt.stride + c];
+    float v = q[0];
+#pragma unroll
+    for (int k = 1; k < kMaxParts; ++k)
+      if (k < pt.np) v += q[k];
+    return v;
+  };
+  const int it = blockIdx.y * 256 + tid;
+  if (it < nh * half) {
+    const int h = it / half, j = it % half;
+    const int c0 = h * d + j;
+    float u = ld(c0), w = ld(c0 + half);
     if (qn) {
       const float *gn = (h < Hq) ? qn : kn;
       float ss = u * u + w * w;
@@ -179,17 +300,23 @@ __global__ __launch_bounds__(256) void k_qk_rope(float *__restrict__ qkv, const 
       w = w * rs * gn[j + half];
     }
     const float c = cs[j], s = sn[j];
-    z[j] = u * c - w * s;
-    z[j + half] = w * c + u * s;
+    row[c0] = u * c - w * s;
+    row[c0 + half] = w * c + u * s;
+  } else if (pt.np > 0 && it < nh * half + Hkv * d) {
+    const int c = nh * d + (it - nh * half);
+    row[c] = ld(c);
   }
 }
 
-hipError_t launch_qk_rope(float *qkv, const int32_t *pos_thw, const float *q_norm,
-                          const float *k_norm, int T, int Hq, int Hkv, int d, float eps,
-                          const RopeParams &rp, hipStream_t s) {
+hipError_t launch_qk_rope(float *qkv, const float *parts, int nparts, const int32_t *pos_thw,
+                          const float *q_norm, const float *k_norm, int T, int Hq, int Hkv, int d,
+                          float eps, const RopeParams &rp, hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  hipLaunchKernelGGL(k_qk_rope, dim3(T), dim3(256), 0, s, qkv, pos_thw, q_norm, k_norm, T, Hq, Hkv,
-                     d, eps, rp);
+  if (nparts > kMaxParts) return hipErrorInvalidValue;
+  const Parts pt{parts ? parts : qkv, parts ? nparts : 0, (size_t)T * (Hq + 2 * Hkv) * d};
+  const int items = (Hq + Hkv) * (d / 2) + (pt.np ? Hkv * d : 0);
+  hipLaunchKernelGGL(k_qk_rope, dim3(T, (items + 255) / 256), dim3(256), 0, s, qkv, pt, pos_thw,
+                     q_norm, k_norm, T, Hq, Hkv, d, eps, rp);
   return hipGetLastError();
 }
 
