@@ -53,6 +53,7 @@ struct mte_encoder {
   // GEMM, added up by the kernel that consumes its product.
   float *ws = nullptr;
   size_t ws_elems = 0;
+  float *rcos = nullptr, *rsin = nullptr;   // [max_tokens, d/2] rotary table of the current batch
   RopeParams rope;
   // kernel timing
   int timing_class = -1;
@@ -160,6 +161,8 @@ void mte_encoder_destroy(mte_encoder *e) {
   hipFree(e->attn);
   hipFree(e->act);
   hipFree(e->ws);
+  hipFree(e->rcos);
+  hipFree(e->rsin);
   hipSetDevice(cur);
   delete e;
 }
@@ -204,7 +207,10 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
     return fail(MTE_E_OOM);
   // K splits are planned for at most 256 rows and 8 splits.
   e->ws_elems = 8 * std::min<size_t>(MT, 256) * std::max(std::max(nqkv, 2 * F), D);
-  if (hipMalloc((void **)&e->ws, e->ws_elems * sizeof(float)) != hipSuccess) return fail(MTE_E_OOM);
+  if (hipMalloc((void **)&e->ws, e->ws_elems * sizeof(float)) != hipSuccess ||
+      hipMalloc((void **)&e->rcos, MT * (d / 2) * sizeof(float)) != hipSuccess ||
+      hipMalloc((void **)&e->rsin, MT * (d / 2) * sizeof(float)) != hipSuccess)
+    return fail(MTE_E_OOM);
 
   // Repack the weights: fused [Wq; Wk; Wv], gate/up interleaved in blocks
   // of 32 rows, fp32 norm gains.
@@ -308,13 +314,14 @@ hipError_t run_layers(mte_encoder *e, float *h, const int32_t *pos, const std::v
       MTE_TRY(launch_rmsnorm(FMT_F32, af, h, np ? h : nullptr, np ? ws : nullptr, np, W.attn_norm, e->xn, MT * D, T,
                              D, c.rms_eps, s));
     int sp = 0;
+    const QkvEpi qe{e->rcos, e->rsin, c.qk_norm ? W.q_norm : nullptr, c.qk_norm ? W.k_norm : nullptr,
+                    (Hq + Hkv) * d, Hq * d, d, c.rms_eps};
     {
       Timer t(e, 0, s);
-      MTE_TRY(launch_gemm(mode, EPI_STORE, e->xn, xn_lo, W.w_qkv, e->qkv, 0, T, nqkv, D, nqkv, ws, wn,
-                          &sp, s));
+      MTE_TRY(launch_gemm(mode, EPI_QKV, e->xn, xn_lo, W.w_qkv, e->qkv, 0, T, nqkv, D, nqkv, ws, wn,
+                          &sp, &qe, s));
     }
-    MTE_TRY(launch_qk_rope(e->qkv, sp ? ws : nullptr, sp, pos, c.qk_norm ? W.q_norm : nullptr,
-                           W.k_norm, T, Hq, Hkv, d, c.rms_eps, e->rope, s));
+    if (sp) MTE_TRY(launch_qkv_parts(e->qkv, ws, sp, T, Hq, Hkv, qe, s));
     {
       Timer t(e, 1, s);
       MTE_TRY(launch_attention(mode, e->qkv, e->attn, MT * Hq * d, cu.data(), batch, Hq, Hkv, d, s));
@@ -322,19 +329,20 @@ hipError_t run_layers(mte_encoder *e, float *h, const int32_t *pos, const std::v
     {
       Timer t(e, 2, s);
       MTE_TRY(launch_gemm(mode, EPI_RESID, e->attn, attn_lo, W.w_o, h, 0, T, D, Hq * d, D, ws, wn, &np,
-                          s));
+                          nullptr, s));
     }
     MTE_TRY(launch_rmsnorm(FMT_F32, af, h, np ? h : nullptr, np ? ws : nullptr, np, W.mlp_norm, e->xn, MT * D, T, D,
                            c.rms_eps, s));
     {
       Timer t(e, 3, s);
       MTE_TRY(launch_gemm(mode, EPI_SWIGLU, e->xn, xn_lo, W.w_gu, e->act, MT * F, T, 2 * F, D, F, ws,
-                          wn, &sp, s));
+                          wn, &sp, nullptr, s));
     }
     if (sp) MTE_TRY(launch_swiglu_parts(af, ws, sp, T, F, e->act, MT * F, s));
     {
       Timer t(e, 4, s);
-      MTE_TRY(launch_gemm(mode, EPI_RESID, e->act, act_lo, W.w_d, h, 0, T, D, F, D, ws, wn, &np, s));
+      MTE_TRY(launch_gemm(mode, EPI_RESID, e->act, act_lo, W.w_d, h, 0, T, D, F, D, ws, wn, &np, nullptr,
+                          s));
     }
   }
 #undef MTE_TRY
@@ -378,8 +386,10 @@ int mte_encode(mte_encoder *e, const void *embeds, const int32_t *pos_thw, const
                          out_hidden, 0, T, c.hidden, c.rms_eps, stream);
     return err == hipSuccess ? MTE_OK : MTE_E_HIP;
   }
+  err = launch_rope_table(pos_thw, T, c.head_dim / 2, e->rope, e->rcos, e->rsin, stream);
   // Layer 0's attention norm also seeds the fp32 residual stream from the embeddings.
-  err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, embeds, e->h, nullptr, 0, e->layers[0].attn_norm,
+  if (err == hipSuccess)
+    err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, embeds, e->h, nullptr, 0, e->layers[0].attn_norm,
                        e->xn, (size_t)c.max_tokens * c.hidden, T, c.hidden, c.rms_eps, stream);
   int np = 0;
   if (err == hipSuccess)
@@ -406,6 +416,8 @@ int mte_encode_layers(mte_encoder *e, const float *h_in, const int32_t *pos_thw,
   DeviceGuard g(e->device);
   hipError_t err = hipSuccess;
   if (h_out != h_in) err = hipMemcpyAsync(h_out, h_in, bytes, hipMemcpyDeviceToDevice, stream);
+  if (err == hipSuccess)
+    err = launch_rope_table(pos_thw, T, e->cfg.head_dim / 2, e->rope, e->rcos, e->rsin, stream);
   int np = 0;
   if (err == hipSuccess)
     err = run_layers(e, h_out, pos_thw, cu, batch, T, layer_begin, layer_end, false, &np, stream);

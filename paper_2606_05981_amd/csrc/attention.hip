@@ -3,25 +3,27 @@
 // For every sequence, query head h and token i:
 //   o[i, h] = sum_{j <= i} softmax_j(q_i . k_j / sqrt(d)) v_j,
 // with k, v taken from kv head h / (Hq / Hkv) and j ranging over the same
-// sequence only.
+// sequence only (q and k arrive normalised and rotated).
 //
 // One workgroup (4 waves) serves one kv head, one tile of query rows of one
 // sequence and the query heads of that kv head assigned to it; every wave
 // owns 32 query rows of one query head. Key/value tiles of 32 tokens are
 // staged in LDS once and shared by all four waves (K row-major, V
-// transposed). Per wave and kv tile:
+// transposed, its keys permuted so that every MFMA operand fragment is one
+// 16-byte LDS read). Per wave and kv tile:
 //   S^T = K Q^T   (32x32 MFMA; lane l ends up owning query l%32)
 //   online softmax in fp32 over the lane's 16 scores plus one cross-lane
 //   exchange (lane ^ 32)
 //   O^T += V^T P^T  (32x32 MFMA; again query l%32 per lane, so the
 //   rescaling of O by the running-max correction is a per-lane scalar).
 //
-// q, k, v arrive in fp32. MODE_F32 multiplies them on the fp32 matrix
-// cores. MODE_BF16X2 splits every operand x into bf16 hi + lo
-// (lo = bf16(x - hi)) and forms each product from three bf16 MFMAs,
-// hi*hi + lo*hi + hi*lo (the lo*lo term is below fp32 accumulation noise).
-// The sequence table (offsets, first tile of each sequence) is passed by
-// value in the kernel arguments, so nothing is read back to the host.
+// q, k, v arrive in fp32 (the packed QKV projection). MODE_F32 multiplies
+// them on the fp32 matrix cores. MODE_BF16X2 splits every operand x into
+// bf16 hi + lo (lo = bf16(x - hi)) and forms each product from three bf16
+// MFMAs, hi*hi + lo*hi + hi*lo (the lo*lo term is below fp32 accumulation
+// noise). The sequence table (offsets, first tile of each sequence) is
+// passed by value in the kernel arguments, so nothing is read back to the
+// host.
 #include <type_traits>
 
 #include "common.h"
@@ -32,7 +34,7 @@ namespace mte {
 constexpr int kMaxSeqPerLaunch = 256;
 
 struct AttnArgs {
-  const float *qkv;
+  const float *qkv;   // [T, ld_qkv] fp32
   char *o;
   size_t o_plane;  // elements between the hi and lo planes of o (MODE_BF16X2)
   int ld_qkv;      // floats per token row of qkv
@@ -62,6 +64,17 @@ __device__ __forceinline__ void split_vals(const float *x, T (&out)[NP][EC]) {
   }
 }
 
+// Position of key k (0..31) of a tile in a row of the transposed V stage:
+// the P fragment f of lane group g holds the probabilities of keys
+// 8*(i/4) + 4g + i%4 for i = EPF*f .. EPF*f + EPF-1 (the S accumulator
+// layout), so those keys are stored contiguously at (2f + g) * EPF.
+template <int EPF>
+__device__ __forceinline__ int vt_pos(int k) {
+  const int a = k >> 3, g = (k >> 2) & 1, c = k & 3;
+  const int i = 4 * a + c;
+  return (2 * (i / EPF) + g) * EPF + (i % EPF);
+}
+
 template <int MODE, int HD>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   typedef typename std::conditional<MODE == MODE_F32, float, bf16>::type T;
@@ -71,14 +84,21 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   constexpr int NCH = HD / EC;                   // chunks per head row
   constexpr int EPF = Frag<T>::kElems;           // values per fragment (== EC)
   constexpr int NFP = 16 / EPF;                  // P fragments per 32-kv tile
-  constexpr int VTP = KV + 4;                    // padded V^T row (elements)
+  constexpr int VTP = KV + 16 / (int)sizeof(T);  // V^T row pitch: 16-byte aligned, conflict-free
   constexpr int ND = HD / 32;                    // 32-wide d blocks
+  constexpr int OTP = HD + 4;                    // padded output staging row (floats)
+  static_assert(EC == EPF, "chunk = fragment");
   typedef typename Frag<T>::type frag_t;
 
-  constexpr int OTP = HD + 4;                     // padded output staging row (floats)
-  __shared__ u32x4 sK[NP][KV * NCH];
-  __shared__ __attribute__((aligned(16))) T sVt[NP][HD * VTP];
-  __shared__ __attribute__((aligned(16))) float sO[4][32 * OTP];
+  // The K / V^T stages and the output staging are never live together.
+  constexpr int K_BYTES = NP * KV * NCH * 16;
+  constexpr int V_BYTES = NP * HD * VTP * (int)sizeof(T);
+  constexpr int O_BYTES = 4 * 32 * OTP * 4;
+  constexpr int SMEM = (K_BYTES + V_BYTES) > O_BYTES ? (K_BYTES + V_BYTES) : O_BYTES;
+  __shared__ __attribute__((aligned(16))) char smem[SMEM];
+  u32x4 *sK = (u32x4 *)smem;                               // [NP][KV * NCH]
+  T *sVt = (T *)(smem + K_BYTES);                          // [NP][HD * VTP]
+  float *sOall = (float *)smem;                            // [4][32 * OTP]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lrow = lane & 31, lgrp = lane >> 5;
@@ -100,26 +120,22 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const int q_last = min(q0 + QT, L) - 1;          // last valid query row of the workgroup
   const int wave_last = min(qw + 31, L - 1);       // last valid query row of this wave
   const size_t ld = (size_t)a.ld_qkv;
-  const float *base = a.qkv + (size_t)s0 * ld;
+  const size_t base = (size_t)s0 * ld;             // element offset of the sequence's first row
   const int k_off = (a.Hq + g) * HD;
   const int v_off = (a.Hq + a.Hkv + g) * HD;
 
-  // Q fragments of this wave's 32 rows (B operand of S^T = K Q^T).
+  // Q fragments of this wave's 32 rows (B operand of S^T = K Q^T); rows
+  // past the sequence read its last row (their outputs are not stored).
   frag_t qf[NP][NCH / 2];
   {
-    const int qi = qw + lrow;
-    const float *qp = base + (size_t)qi * ld + head * HD;
+    const int qi = min(qw + lrow, L - 1);
 #pragma unroll
     for (int kk = 0; kk < NCH / 2; ++kk) {
       float x[EC];
 #pragma unroll
-      for (int e = 0; e < EC; ++e) x[e] = 0.f;
-      if (qi < L) {
-#pragma unroll
-        for (int e = 0; e < EC; e += 4) {
-          f32x4 v = *(const f32x4 *)(qp + (kk * 2 + lgrp) * EC + e);
-          x[e] = v[0]; x[e + 1] = v[1]; x[e + 2] = v[2]; x[e + 3] = v[3];
-        }
+      for (int e = 0; e < EC; e += 4) {
+        const f32x4 v = *(const f32x4 *)(a.qkv + base + (size_t)qi * ld + head * HD + (kk * 2 + lgrp) * EC + e);
+        x[e] = v[0]; x[e + 1] = v[1]; x[e + 2] = v[2]; x[e + 3] = v[3];
       }
       T sp[NP][EC];
       split_vals<T, NP, EC>(x, sp);
@@ -145,7 +161,9 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   //  K: thread chunk (row r, chunk c) of EC consecutive d -> sK[r][c] (swizzled);
   //  V: thread (column d, row group v) reads EC rows of column d (lanes
   //     take consecutive d, so each load is one coalesced row segment) and
-  //     writes them as a row segment of V^T: sVt[d][v*EC .. v*EC+EC).
+  //     writes them into row d of V^T at their permuted key positions.
+  // Rows past the sequence read its last row: their scores are masked, so
+  // they add exact zeros.
   constexpr int KCH = KV * NCH / 256;             // K chunks per thread
   constexpr int VCH = HD * (KV / EC) / 256;       // V column groups per thread
   static_assert(KCH * 256 == KV * NCH && VCH * 256 == HD * (KV / EC), "staging split");
@@ -153,40 +171,32 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   auto gload = [&](int kv0) {
 #pragma unroll
     for (int t = 0; t < KCH; ++t) {
-      const int idx = tid + t * 256, r = idx / NCH, c = idx % NCH;
-      if (kv0 + r < L) {
-        const float *rp = base + (size_t)(kv0 + r) * ld + k_off + c * EC;
+      const int idx = tid + t * 256, r = min(kv0 + idx / NCH, L - 1), c = idx % NCH;
 #pragma unroll
-        for (int e = 0; e < EC; e += 4) {
-          const f32x4 v = *(const f32x4 *)(rp + e);
-          kx[t][e] = v[0]; kx[t][e + 1] = v[1]; kx[t][e + 2] = v[2]; kx[t][e + 3] = v[3];
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < EC; ++e) kx[t][e] = 0.f;
+      for (int e = 0; e < EC; e += 4) {
+        const f32x4 v = *(const f32x4 *)(a.qkv + base + (size_t)r * ld + k_off + c * EC + e);
+        kx[t][e] = v[0]; kx[t][e + 1] = v[1]; kx[t][e + 2] = v[2]; kx[t][e + 3] = v[3];
       }
     }
 #pragma unroll
     for (int t = 0; t < VCH; ++t) {
       const int idx = tid + t * 256, d = idx % HD, v = idx / HD;
 #pragma unroll
-      for (int e = 0; e < EC; ++e) {
-        const int r = kv0 + v * EC + e;
-        vx[t][e] = r < L ? base[(size_t)r * ld + v_off + d] : 0.f;
-      }
+      for (int e = 0; e < EC; ++e)
+        vx[t][e] = a.qkv[base + (size_t)min(kv0 + v * EC + e, L - 1) * ld + v_off + d];
     }
   };
   auto lstore = [&]() {
 #pragma unroll
     for (int t = 0; t < KCH; ++t) {
       const int idx = tid + t * 256, r = idx / NCH, c = idx % NCH;
-      T ks[NP][EC];
-      split_vals<T, NP, EC>(kx[t], ks);
+      T sp[NP][EC];
+      split_vals<T, NP, EC>(kx[t], sp);
 #pragma unroll
       for (int p = 0; p < NP; ++p) {
         u32x4 w;
-        __builtin_memcpy(&w, ks[p], 16);
-        sK[p][r * NCH + kswz<NCH>(r, c)] = w;
+        __builtin_memcpy(&w, sp[p], 16);
+        sK[p * KV * NCH + r * NCH + kswz<NCH>(r, c)] = w;
       }
     }
 #pragma unroll
@@ -196,12 +206,21 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       split_vals<T, NP, EC>(vx[t], vs);
 #pragma unroll
       for (int p = 0; p < NP; ++p) {
-        u32x2 w0, w1;
-        __builtin_memcpy(&w0, &vs[p][0], 8);
-        __builtin_memcpy(&w1, (const char *)&vs[p][0] + 8, 8);
-        u32x2 *dst = (u32x2 *)(sVt[p] + d * VTP + v * EC);
-        dst[0] = w0;
-        dst[1] = w1;
+        T *row = sVt + p * HD * VTP + d * VTP;
+        // keys v*EC .. v*EC+EC-1 land in runs of 4 consecutive positions
+#pragma unroll
+        for (int e = 0; e < EC; e += 4) {
+          const int pos = vt_pos<EPF>(v * EC + e);
+          if constexpr (sizeof(T) == 2) {
+            u32x2 w;
+            __builtin_memcpy(&w, &vs[p][e], 8);
+            *(u32x2 *)(row + pos) = w;
+          } else {
+            u32x4 w;
+            __builtin_memcpy(&w, &vs[p][e], 16);
+            *(u32x4 *)(row + pos) = w;
+          }
+        }
       }
     }
   };
@@ -219,10 +238,10 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
       for (int kk = 0; kk < NCH / 2; ++kk) {
         const int slot = lrow * NCH + kswz<NCH>(lrow, kk * 2 + lgrp);
-        const frag_t k0 = __builtin_bit_cast(frag_t, sK[0][slot]);
+        const frag_t k0 = __builtin_bit_cast(frag_t, sK[slot]);
         mfma32(s, k0, qf[0][kk]);
         if constexpr (NP == 2) {
-          const frag_t k1 = __builtin_bit_cast(frag_t, sK[1][slot]);
+          const frag_t k1 = __builtin_bit_cast(frag_t, sK[KV * NCH + slot]);
           mfma32(s, k1, qf[0][kk]);
           mfma32(s, k0, qf[1][kk]);
         }
@@ -250,8 +269,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       for (int n = 0; n < ND; ++n)
 #pragma unroll
         for (int r = 0; r < 16; ++r) oacc[n][r] *= alpha;
-      // P fragments: element e of fragment f is P value i = EPF*f + e, which
-      // belongs to key row 8*(i/4) + 4*lgrp + i%4 of this tile.
+      // P fragments: element e of fragment f is P value i = EPF*f + e.
       frag_t pf[NP][NFP];
 #pragma unroll
       for (int f = 0; f < NFP; ++f) {
@@ -268,14 +286,8 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         for (int f = 0; f < NFP; ++f) {
           frag_t vf[NP];
 #pragma unroll
-          for (int q = 0; q < NP; ++q) {
-            const T *vrow = sVt[q] + (n * 32 + lrow) * VTP + 4 * lgrp;
-#pragma unroll
-            for (int e = 0; e < EPF; ++e) {
-              const int i = EPF * f + e;
-              vf[q][e] = vrow[8 * (i >> 2) + (i & 3)];
-            }
-          }
+          for (int q = 0; q < NP; ++q)
+            vf[q] = *(const frag_t *)(sVt + q * HD * VTP + (n * 32 + lrow) * VTP + (2 * f + lgrp) * EPF);
           mfma32(oacc[n], vf[0], pf[0][f]);
           if constexpr (NP == 2) {
             mfma32(oacc[n], vf[1], pf[0][f]);
@@ -288,12 +300,13 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   }
 
   // Output: each wave writes its normalised 32 x HD tile into LDS (row-major
-  // by query), then copies it out row by row so that the global stores are
-  // contiguous along d (a lane owns a query row in the accumulator layout,
-  // which would scatter 2-byte stores across rows).
+  // by query, over the stage buffers, free after the loop's last barrier),
+  // then copies it out row by row so that the global stores are contiguous
+  // along d (a lane owns a query row in the accumulator layout, which would
+  // scatter 2-byte stores across rows).
   const float lt = l_i + __shfl_xor(l_i, 32, kWave);
   const float inv = 1.f / lt;
-  float *so = sO[wave];
+  float *so = sOall + wave * 32 * OTP;
 #pragma unroll
   for (int n = 0; n < ND; ++n)
 #pragma unroll
@@ -330,9 +343,9 @@ hipError_t launch_attention(int mode, const float *qkv, void *o, size_t o_plane,
   const int rep = Hq / Hkv;
   AttnArgs a;
   a.qkv = qkv;
+  a.ld_qkv = (Hq + 2 * Hkv) * d;
   a.o = (char *)o;
   a.o_plane = o_plane;
-  a.ld_qkv = (Hq + 2 * Hkv) * d;
   a.Hq = Hq;
   a.Hkv = Hkv;
   a.rep = rep;

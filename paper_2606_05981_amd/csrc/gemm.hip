@@ -22,10 +22,13 @@
 // at slot c ^ ((r ^ (r >> 3)) & 7), so the 16-byte fragment reads of 8 or 16
 // consecutive rows at one logical chunk hit distinct banks.
 //
-// Epilogues are fused: fp32 store (QKV), SwiGLU over interleaved gate/up
-// rows (MLP up-projection, written in the activation format) and
-// accumulation into the fp32 residual stream (attention output projection
-// and MLP down-projection). With K split over workgroups (small M), each
+// Epilogues are fused: fp32 store with the per-head QK-norm and rotary
+// embedding of the q and k heads (QKV projection; a wave's columns cover
+// whole heads, so a head's sum of squares is a reduction over the wave's
+// lanes and both members of each rotary pair sit in one lane), SwiGLU over
+// interleaved gate/up rows (MLP up-projection, written in the activation
+// format) and accumulation into the fp32 residual stream (attention output
+// projection and MLP down-projection). With K split over workgroups (small M), each
 // split stores its partial sum instead, and the kernel that consumes the
 // product adds the partials up in split order, so results do not depend on
 // the order in which workgroups finish.
@@ -46,6 +49,7 @@ struct GemmArgs {
                       // EPI_PARTIAL: elements between the partial sums of two K splits
   int M, N, K, ldc;
   int k_chunk;        // K range of one split (gridDim.z splits)
+  QkvEpi qe;          // EPI_QKV
 };
 
 // Chunk swizzles for rows of 128 bytes (8 chunks) and 64 bytes (4 chunks):
@@ -95,6 +99,85 @@ __device__ __forceinline__ void dma16(const void *g, uint32_t lds_base) {
       : "=&s"(saved)
       : "v"(g), "s"(lds_base)
       : "memory");
+}
+
+// EPI_QKV epilogue of one wave: rows mw.. (TM blocks of 32), columns cw..
+// (TN blocks of 32 = whole heads of HD columns). For each row and q or k
+// head: RMS-normalise (sum of squares over the head's HD/32 column blocks
+// and the 32 lanes that hold the row) and rotate pair (c, c + HD/2), i.e.
+// column blocks (jb, jb + HD/64) of one lane. Gains are read once; the
+// rotary table values of a block of 32 rows are read before they are used.
+template <int HD, int TM, int TN>
+__device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const GemmArgs &g, int cw,
+                                             int mw, int lane) {
+  constexpr int HJB = HD / 32;                    // column blocks per head
+  constexpr int NH = TN / HJB;                    // heads of the wave
+  constexpr int NR = NH * HJB / 2;                // rotary blocks per row
+  static_assert(TN % HJB == 0, "whole heads per wave");
+  const QkvEpi &q = g.qe;
+  const int lrow = lane & 31;
+  const int M = g.M;
+  float *C = (float *)g.C;
+  bool rot[NH];
+  float gsc[TN];
+#pragma unroll
+  for (int h = 0; h < NH; ++h) {
+    const int cb = cw + h * HD;
+    rot[h] = cb < q.rot_cols;                     // wave-uniform
+    const float *gn = cb < q.nq_cols ? q.qn : q.kn;
+#pragma unroll
+    for (int jj = 0; jj < HJB; ++jj) gsc[h * HJB + jj] = (rot[h] && gn) ? gn[jj * 32 + lrow] : 1.f;
+  }
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+    float tc[16][NR], ts[16][NR];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = min(mw + i * 32 + acc_row(r, lane), M - 1);
+#pragma unroll
+      for (int x = 0; x < NR; ++x) {
+        const int h = x / (HJB / 2), jj = x % (HJB / 2);
+        tc[r][x] = 1.f;
+        ts[r][x] = 0.f;
+        if (rot[h]) {
+          const size_t o = (size_t)m * (HD / 2) + jj * 32 + lrow;
+          tc[r][x] = q.rcos[o];
+          ts[r][x] = q.rsin[o];
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = mw + i * 32 + acc_row(r, lane);
+      float v[TN];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) v[j] = acc[i][j][r];
+#pragma unroll
+      for (int h = 0; h < NH; ++h) {
+        if (!rot[h]) continue;
+        if (q.qn) {
+          float ss = 0.f;
+#pragma unroll
+          for (int jj = 0; jj < HJB; ++jj) ss += v[h * HJB + jj] * v[h * HJB + jj];
+#pragma unroll
+          for (int o = 1; o < 32; o <<= 1) ss += __shfl_xor(ss, o, kWave);
+          const float rs = rsqrtf(ss / (float)HD + q.eps);
+#pragma unroll
+          for (int jj = 0; jj < HJB; ++jj) v[h * HJB + jj] = v[h * HJB + jj] * rs * gsc[h * HJB + jj];
+        }
+#pragma unroll
+        for (int jj = 0; jj < HJB / 2; ++jj) {
+          const int j = h * HJB + jj, jp = j + HJB / 2, x = h * (HJB / 2) + jj;
+          const float u = v[j], w = v[jp];
+          v[j] = u * tc[r][x] - w * ts[r][x];
+          v[jp] = w * tc[r][x] + u * ts[r][x];
+        }
+      }
+      if (m < M)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) C[(size_t)m * g.ldc + cw + j * 32 + lrow] = v[j];
+    }
+  }
 }
 
 // The main loop keeps P stages in an LDS ring filled by direct global->LDS
@@ -273,6 +356,16 @@ __global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, O
   wait_vm<0>();                          // no load may land after the workgroup ends
 
   // Epilogue.
+  if constexpr (EPI == EPI_QKV) {
+    const int cw = n0 + wn * WTN;
+    // (the host only launches tiles whose waves cover whole heads)
+    if (g.qe.hd == 128) {
+      if constexpr (TN % 4 == 0) qkv_epilogue<128, TM, TN>(acc, g, cw, m0 + wm * WTM, lane);
+    } else {
+      if constexpr (TN % 2 == 0) qkv_epilogue<64, TM, TN>(acc, g, cw, m0 + wm * WTM, lane);
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -317,8 +410,8 @@ struct TileCfg {
 
 template <int MODE, int BM, int BN, int WM, int WN, int ROWB, int P, int EPI, int OCC>
 static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
-  if constexpr (EPI == EPI_SWIGLU && (BN / WN) % 64 != 0) {
-    return hipErrorInvalidValue;  // gate/up pairs need 64 columns per wave
+  if constexpr ((EPI == EPI_SWIGLU || EPI == EPI_QKV) && (BN / WN) % 64 != 0) {
+    return hipErrorInvalidValue;  // gate/up pairs (or whole heads) need 64 columns per wave
   } else {
   constexpr int NA = (MODE == MODE_BF16X2) ? 2 : 1;
   constexpr int lds_bytes = P * (NA * BM + BN) * ROWB;
@@ -375,12 +468,15 @@ static hipError_t run_id(int id, const GemmArgs &a, int splits, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
-static bool tile_fits(int id, int N, int K, int esz, int epi, int splits) {
+// col_align: columns a wave must cover in whole units (gate/up pairs for
+// SwiGLU, heads for the QKV epilogue).
+static bool tile_fits(int id, int N, int K, int esz, int epi, int splits, int col_align = 32) {
   const TileCfg &t = kTiles[id];
   if (N % t.bn) return false;
   const int ks = t.rowb / esz;
   if (K % splits || (K / splits) % ks) return false;
   if (epi == EPI_SWIGLU && (t.bn / t.wn) % 64) return false;  // gate/up pairs per wave
+  if (epi == EPI_QKV && (t.bn / t.wn) % col_align) return false;
   return true;
 }
 
@@ -400,23 +496,23 @@ struct TileChoice {
   int n, k, epi, m, tile, splits;
 };
 static const TileChoice kChoices[] = {
-    {4096, 2048, EPI_STORE, 96, 13, 4},    {2048, 2048, EPI_RESID, 96, 13, 8},
+    {4096, 2048, EPI_QKV, 96, 13, 4},    {2048, 2048, EPI_RESID, 96, 13, 8},
     {12288, 2048, EPI_SWIGLU, 96, 18, 2},  {2048, 6144, EPI_RESID, 96, 18, 8},
-    {4096, 2048, EPI_STORE, 192, 18, 4},   {2048, 2048, EPI_RESID, 192, 10, 4},
+    {4096, 2048, EPI_QKV, 192, 18, 4},   {2048, 2048, EPI_RESID, 192, 10, 4},
     {12288, 2048, EPI_SWIGLU, 192, 5, 2},  {2048, 6144, EPI_RESID, 192, 18, 8},
-    {4096, 2048, EPI_STORE, 768, 8, 1},    {2048, 2048, EPI_RESID, 768, 10, 1},
+    {4096, 2048, EPI_QKV, 768, 8, 1},    {2048, 2048, EPI_RESID, 768, 10, 1},
     {12288, 2048, EPI_SWIGLU, 768, 1, 1},  {2048, 6144, EPI_RESID, 768, 10, 1},
-    {4096, 2048, EPI_STORE, 1536, 4, 1},   {2048, 2048, EPI_RESID, 1536, 17, 1},
+    {4096, 2048, EPI_QKV, 1536, 4, 1},   {2048, 2048, EPI_RESID, 1536, 17, 1},
     {12288, 2048, EPI_SWIGLU, 1536, 15, 1}, {2048, 6144, EPI_RESID, 1536, 17, 1},
-    {4096, 2048, EPI_STORE, 10240, 4, 1},  {2048, 2048, EPI_RESID, 10240, 1, 1},
+    {4096, 2048, EPI_QKV, 10240, 4, 1},  {2048, 2048, EPI_RESID, 10240, 1, 1},
     {12288, 2048, EPI_SWIGLU, 10240, 4, 1}, {2048, 6144, EPI_RESID, 10240, 9, 1},
 };
 
 // Fallback estimate: rounds of workgroups over the compute units x the time
 // one full round takes at the tile's measured rate. Split-K is only
 // considered for small M, and only where the partial sums fit `ws_elems`.
-static void plan_model(int M, int N, int K, int esz, int epi, size_t ws_elems, int *tile,
-                       int *splits) {
+static void plan_model(int M, int N, int K, int esz, int epi, int col_align, size_t ws_elems,
+                       int *tile, int *splits) {
   const int cus = 256;
   double best = 1e30;
   *tile = -1;
@@ -424,7 +520,7 @@ static void plan_model(int M, int N, int K, int esz, int epi, size_t ws_elems, i
   for (int id = 0; id < kNumTiles; ++id) {
     for (int sp = 1; sp <= 8; sp *= 2) {
       if (sp > 1 && (M > 256 || (size_t)sp * M * N > ws_elems)) continue;
-      if (!tile_fits(id, N, K, esz, sp > 1 ? EPI_PARTIAL : epi, sp)) continue;
+      if (!tile_fits(id, N, K, esz, sp > 1 ? EPI_PARTIAL : epi, sp, col_align)) continue;
       const TileCfg &t = kTiles[id];
       const double tiles = (double)(N / t.bn) * ((M + t.bm - 1) / t.bm) * sp;
       const double slots = (double)cus * t.occ;
@@ -440,7 +536,8 @@ static void plan_model(int M, int N, int K, int esz, int epi, size_t ws_elems, i
   }
 }
 
-static void plan(int M, int N, int K, int esz, int epi, size_t ws_elems, int *tile, int *splits) {
+static void plan(int M, int N, int K, int esz, int epi, int col_align, size_t ws_elems, int *tile,
+                 int *splits) {
   const TileChoice *best = nullptr;
   double bd = 1e30;
   if (esz == 2) {
@@ -450,13 +547,14 @@ static void plan(int M, int N, int K, int esz, int epi, size_t ws_elems, int *ti
       if (d < bd) { bd = d; best = &c; }
     }
   }
-  if (best && tile_fits(best->tile, N, K, esz, best->splits > 1 ? EPI_PARTIAL : epi, best->splits) &&
+  if (best &&
+      tile_fits(best->tile, N, K, esz, best->splits > 1 ? EPI_PARTIAL : epi, best->splits, col_align) &&
       (best->splits == 1 || (M <= 256 && (size_t)best->splits * M * N <= ws_elems))) {
     *tile = best->tile;
     *splits = best->splits;
     return;
   }
-  plan_model(M, N, K, esz, epi, ws_elems, tile, splits);
+  plan_model(M, N, K, esz, epi, col_align, ws_elems, tile, splits);
 }
 
 template <int MODE>
@@ -465,37 +563,43 @@ static hipError_t launch_mode(int epi, int tile, int splits, const GemmArgs &a, 
     case EPI_STORE: return run_id<MODE, EPI_STORE>(tile, a, splits, s);
     case EPI_SWIGLU: return run_id<MODE, EPI_SWIGLU>(tile, a, splits, s);
     case EPI_RESID: return run_id<MODE, EPI_RESID>(tile, a, splits, s);
+    case EPI_QKV: return run_id<MODE, EPI_QKV>(tile, a, splits, s);
     default: return run_id<MODE, EPI_PARTIAL>(tile, a, splits, s);
   }
 }
 
 hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void *A, const void *A_lo,
                             const void *W, void *C, size_t c_plane, int M, int N, int K, int ldc,
-                            hipStream_t s) {
+                            const QkvEpi *qe, hipStream_t s) {
   if (M <= 0) return hipSuccess;
   const int esz = mode == MODE_BF16X2 ? 2 : 4;
-  if (tile < 0 || tile >= kNumTiles || splits < 1 || !tile_fits(tile, N, K, esz, epi, splits) ||
+  if (epi == EPI_QKV && (!qe || (qe->hd != 64 && qe->hd != 128))) return hipErrorInvalidValue;
+  if (tile < 0 || tile >= kNumTiles || splits < 1 ||
+      !tile_fits(tile, N, K, esz, epi, splits, epi == EPI_QKV ? qe->hd : 32) ||
       (splits > 1 && epi != EPI_PARTIAL))
     return hipErrorInvalidValue;
-  GemmArgs a{(const char *)A, (const char *)A_lo, (const char *)W, C, c_plane, M, N, K, ldc, K / splits};
+  GemmArgs a{(const char *)A, (const char *)A_lo, (const char *)W, C, c_plane, M, N, K, ldc, K / splits,
+             epi == EPI_QKV ? *qe : QkvEpi{}};
   return mode == MODE_BF16X2 ? launch_mode<MODE_BF16X2>(epi, tile, splits, a, s)
                              : launch_mode<MODE_F32>(epi, tile, splits, a, s);
 }
 
 hipError_t launch_gemm(int mode, int epi, const void *A, const void *A_lo, const void *W, void *C,
                        size_t c_plane, int M, int N, int K, int ldc, float *ws, size_t ws_elems,
-                       int *splits_out, hipStream_t s) {
+                       int *splits_out, const QkvEpi *qe, hipStream_t s) {
   *splits_out = 0;
   if (M <= 0) return hipSuccess;
+  if (epi == EPI_QKV && !qe) return hipErrorInvalidValue;
   int tile, splits;
-  plan(M, N, K, mode == MODE_BF16X2 ? 2 : 4, epi, ws ? ws_elems : 0, &tile, &splits);
+  plan(M, N, K, mode == MODE_BF16X2 ? 2 : 4, epi, epi == EPI_QKV ? qe->hd : 32, ws ? ws_elems : 0,
+       &tile, &splits);
   if (tile < 0) return hipErrorInvalidValue;
   if (splits > 1) {
     *splits_out = splits;
     return launch_gemm_tile(mode, EPI_PARTIAL, tile, splits, A, A_lo, W, ws, (size_t)M * N, M, N, K,
-                            N, s);
+                            N, nullptr, s);
   }
-  return launch_gemm_tile(mode, epi, tile, 1, A, A_lo, W, C, c_plane, M, N, K, ldc, s);
+  return launch_gemm_tile(mode, epi, tile, 1, A, A_lo, W, C, c_plane, M, N, K, ldc, qe, s);
 }
 
 }  // namespace mte

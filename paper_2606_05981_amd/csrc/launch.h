@@ -26,6 +26,18 @@ enum Epilogue {
                    // written as float (MODE_F32) or bf16 hi/lo planes (MODE_BF16X2)
   EPI_RESID = 2,   // C (float residual stream) [m, n] += acc
   EPI_PARTIAL = 3, // C (float) + split * c_plane [m, n] = acc: the partial sum of one K split
+  EPI_QKV = 4,     // C (float) [m, n] = acc, q and k heads RMS-normalised per head and rotated
+};
+
+// Parameters of EPI_QKV: columns [0, nq_cols) are q heads, [nq_cols,
+// rot_cols) k heads (hd columns each), the rest (v) is stored as is. Row m
+// (token m) rotates pair (c, c + hd/2) of a head by the angle whose cos / sin
+// are rcos / rsin [m * hd/2 + c]. qn / kn: per-head RMSNorm gains [hd], or
+// both null (no QK-norm).
+struct QkvEpi {
+  const float *rcos, *rsin, *qn, *kn;
+  int rot_cols, nq_cols, hd;
+  float eps;
 };
 
 // C = A[M, K] * W[N, K]^T. MODE_F32: A, W float. MODE_BF16X2: A = A_hi + A_lo
@@ -37,16 +49,18 @@ enum Epilogue {
 // elements apart) are left in ws, in split order, for the consumer to add
 // up and apply `epi` to (for EPI_SWIGLU: the raw interleaved gate/up
 // columns). Otherwise *splits_out = 0 and C holds the result.
+// qe: the EPI_QKV parameters (else ignored, may be null). With a K split,
+// EPI_QKV's normalisation and rotation are left to the consumer as well.
 hipError_t launch_gemm(int mode, int epi, const void *A, const void *A_lo, const void *W, void *C,
                        size_t c_plane, int M, int N, int K, int ldc, float *ws, size_t ws_elems,
-                       int *splits_out, hipStream_t s);
+                       int *splits_out, const QkvEpi *qe, hipStream_t s);
 
 // The same with an explicit tile configuration (index into the GEMM tile
 // table) and number of K splits (> 1 only with EPI_PARTIAL); used for
 // tuning. Returns hipErrorInvalidValue if the tile does not fit the shape.
 hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void *A, const void *A_lo,
                             const void *W, void *C, size_t c_plane, int M, int N, int K, int ldc,
-                            hipStream_t s);
+                            const QkvEpi *qe, hipStream_t s);
 
 // Per-row RMSNorm: out[r, :] = x[r, :] / sqrt(mean(x[r,:]^2) + eps) * g with
 // x = in + parts[0] + ... + parts[nparts-1] (float [rows, D] partial sums,
@@ -75,18 +89,22 @@ struct RopeParams {
   uint8_t axis[64];          // position axis (0 t, 1 h, 2 w) of pair j
 };
 
-// Per-head RMSNorm (when q_norm != nullptr) and multimodal rotary embedding
-// of the q and k heads of a packed fp32 qkv buffer [T, (Hq+2Hkv)*d]: in
-// place, or, with nparts partial sums of the projection in `parts` (T*nqkv
-// elements apart), summed from them into qkv (v heads copied).
-hipError_t launch_qk_rope(float *qkv, const float *parts, int nparts, const int32_t *pos_thw,
-                          const float *q_norm, const float *k_norm, int T, int Hq, int Hkv, int d,
-                          float eps, const RopeParams &rp, hipStream_t s);
+// Rotary table of T tokens: rcos / rsin [T, half] = cos / sin of
+// pos_thw[axis(j)][t] * inv_freq[j] (float64 angle and sincos, rounded).
+hipError_t launch_rope_table(const int32_t *pos_thw, int T, int half, const RopeParams &rp, float *rcos,
+                             float *rsin, hipStream_t s);
 
-// Causal GQA attention over packed sequences. qkv: fp32 [T, (Hq+2Hkv)*d], q
-// heads first, then k, then v; o: [T, Hq*d] as float (MODE_F32) or bf16
-// hi/lo planes o_plane elements apart (MODE_BF16X2). cu: host
-// int32[batch+1] sequence offsets. Launches in chunks of <= 256 sequences.
+// QKV projection finished from nparts partial sums [T, (Hq+2Hkv)*d]
+// (T*(Hq+2Hkv)*d elements apart, added in order) into qkv, with the q and k
+// heads normalised and rotated as by EPI_QKV (qe; v copied).
+hipError_t launch_qkv_parts(float *qkv, const float *parts, int nparts, int T, int Hq, int Hkv,
+                            const QkvEpi &qe, hipStream_t s);
+
+// Causal GQA attention over packed sequences. qkv: fp32 [T, (Hq+2Hkv)*d],
+// q heads first, then k, then v (q and k already normalised and rotated).
+// o: [T, Hq*d] as float (MODE_F32) or bf16 hi/lo planes o_plane elements
+// apart (MODE_BF16X2). cu: host int32[batch+1] sequence offsets. Launches in
+// chunks of <= 256 sequences.
 hipError_t launch_attention(int mode, const float *qkv, void *o, size_t o_plane, const int32_t *cu,
                             int batch, int Hq, int Hkv, int d, hipStream_t s);
 

@@ -196,6 +196,62 @@ hipError_t launch_resid_add(float *h, const float *parts, int nparts, int rows, 
   return hipGetLastError();
 }
 
+// Grid (token, item block). Items are the token's rotary pairs, head-major
+// (pair j of q/k head h is item h*d/2 + j; a head's d/2 items sit in one
+// wave, so the per-head sum of squares of the QK-norm is a butterfly over
+// those lanes), followed by its v elements. Every value is first summed
+// from the partial sums (in split order).
+__global__ __launch_bounds__(256) void k_qkv_parts(float *__restrict__ qkv, Parts pt, int Hq, int Hkv,
+                                                   QkvEpi qe) {
+  const int tok = blockIdx.x, tid = threadIdx.x;
+  const int d = qe.hd, half = d >> 1;
+  const int nh = Hq + Hkv, nqkv = (Hq + 2 * Hkv) * d;
+  float *row = qkv + (size_t)tok * nqkv;
+  const float *prow = pt.p + (size_t)tok * nqkv;
+  auto ld = [&](int c) -> float {
+    float q[kMaxParts];
+#pragma unroll
+    for (int k = 0; k < kMaxParts; ++k)
+      if (k < pt.np) q[k] = prow[(size_t)k * pt.stride + c];
+    float v = q[0];
+#pragma unroll
+    for (int k = 1; k < kMaxParts; ++k)
+      if (k < pt.np) v += q[k];
+    return v;
+  };
+  const int it = blockIdx.y * 256 + tid;
+  if (it < nh * half) {
+    const int h = it / half, j = it % half;
+    const int c0 = h * d + j;
+    float u = ld(c0), w = ld(c0 + half);
+    if (qe.qn) {
+      const float *gn = (h < Hq) ? qe.qn : qe.kn;
+      float ss = u * u + w * w;
+      for (int m = half >> 1; m >= 1; m >>= 1) ss = warp_sum_xor(ss, m);
+      const float rs = rsqrtf(ss / (float)d + qe.eps);
+      u = u * rs * gn[j];
+      w = w * rs * gn[j + half];
+    }
+    const float c = qe.rcos[(size_t)tok * half + j], s = qe.rsin[(size_t)tok * half + j];
+    row[c0] = u * c - w * s;
+    row[c0 + half] = w * c + u * s;
+  } else if (it < nh * half + Hkv * d) {
+    const int c = nh * d + (it - nh * half);
+    row[c] = ld(c);
+  }
+}
+
+hipError_t launch_qkv_parts(float *qkv, const float *parts, int nparts, int T, int Hq, int Hkv,
+                            const QkvEpi &qe, hipStream_t s) {
+  if (T <= 0) return hipSuccess;
+  if (!parts || nparts < 1 || nparts > kMaxParts) return hipErrorInvalidValue;
+  const int d = qe.hd;
+  const Parts pt{parts, nparts, (size_t)T * (Hq + 2 * Hkv) * d};
+  const int items = (Hq + Hkv) * (d / 2) + Hkv * d;
+  hipLaunchKernelGGL(k_qkv_parts, dim3(T, (items + 255) / 256), dim3(256), 0, s, qkv, pt, Hq, Hkv, qe);
+  return hipGetLastError();
+}
+
 // SwiGLU of summed gate/up partial sums. parts: np x [rows, 2F], gate and up
 // columns interleaved in blocks of 32 (block b: gate 32b.., then up 32b..).
 // out [rows, F]: float (OUT_FMT FMT_F32) or bf16 hi / lo planes `plane` apart.
@@ -245,78 +301,30 @@ hipError_t launch_swiglu_parts(int out_fmt, const float *parts, int nparts, int 
   return hipGetLastError();
 }
 
-// ------------------------------------------------- QK-norm + M-RoPE
-// Grid (token, item block). Items are the token's rotary pairs, head-major
-// (pair j of q/k head h is item h*d/2 + j; a head's d/2 items sit in one
-// wave, so the per-head sum of squares of the QK-norm is a butterfly over
-// those lanes), followed, when the projection arrives as partial sums
-// (split-K), by its v elements, which are summed (in split order) and
-// copied; without partial sums qkv is updated in place. Each block computes
-// the token's d/2 rotation angles (float64 angle and sincos, rounded to
-// fp32).
-__global__ __launch_bounds__(256) void k_qk_rope(float *__restrict__ qkv, Parts pt,
-                                                 const int32_t *__restrict__ pos,
-                                                 const float *__restrict__ qn, const float *__restrict__ kn,
-                                                 int T_tokens, int Hq, int Hkv, int d, float eps,
-                                                 RopeParams rp) {
-  __shared__ float cs[64], sn[64];
-  const int tok = blockIdx.x, tid = threadIdx.x;
-  const int half = d >> 1;
-  if (tid < half) {
-    const int ax = rp.axis[tid];
-    const double ang = (double)pos[(size_t)ax * T_tokens + tok] * rp.inv_freq[tid];
-    double sv, cv;
-    sincos(ang, &sv, &cv);
-    cs[tid] = (float)cv;
-    sn[tid] = (float)sv;
-  }
-  __syncthreads();
-  const int nh = Hq + Hkv, nqkv = (Hq + 2 * Hkv) * d;
-  float *row = qkv + (size_t)tok * nqkv;
-  const float *prow = pt.p + (size_t)tok * nqkv;
-  auto ld = [&](int c) -> float {
-    if (pt.np == 0) return row[c];
-    float q[kMaxParts];
-#pragma unroll
-    for (int k = 0; k < kMaxParts; ++k)
-      if (k < pt.np) q[k] = prow[(size_t)k * pt.stride + c];
-    float v = q[0];
-#pragma unroll
-    for (int k = 1; k < kMaxParts; ++k)
-      if (k < pt.np) v += q[k];
-    return v;
-  };
-  const int it = blockIdx.y * 256 + tid;
-  if (it < nh * half) {
-    const int h = it / half, j = it % half;
-    const int c0 = h * d + j;
-    float u = ld(c0), w = ld(c0 + half);
-    if (qn) {
-      const float *gn = (h < Hq) ? qn : kn;
-      float ss = u * u + w * w;
-      for (int m = half >> 1; m >= 1; m >>= 1) ss = warp_sum_xor(ss, m);
-      const float rs = rsqrtf(ss / (float)d + eps);
-      u = u * rs * gn[j];
-      w = w * rs * gn[j + half];
-    }
-    const float c = cs[j], s = sn[j];
-    row[c0] = u * c - w * s;
-    row[c0 + half] = w * c + u * s;
-  } else if (pt.np > 0 && it < nh * half + Hkv * d) {
-    const int c = nh * d + (it - nh * half);
-    row[c] = ld(c);
-  }
+// ---------------------------------------------------- rotary table
+// cos / sin of the rotation angle of every (token, pair): pair j of token
+// t turns by pos[axis(j)][t] * inv_freq[j]; the angle and its sincos are
+// evaluated in float64 and rounded to fp32. Built once per forward and
+// shared by the q and k heads of all layers.
+__global__ __launch_bounds__(256) void k_rope_table(const int32_t *__restrict__ pos, int T_tokens,
+                                                    int half, RopeParams rp, float *__restrict__ rcos,
+                                                    float *__restrict__ rsin) {
+  const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (size_t)T_tokens * half) return;
+  const int tok = (int)(i / half), j = (int)(i % half);
+  const double ang = (double)pos[(size_t)rp.axis[j] * T_tokens + tok] * rp.inv_freq[j];
+  double sv, cv;
+  sincos(ang, &sv, &cv);
+  rcos[i] = (float)cv;
+  rsin[i] = (float)sv;
 }
 
-hipError_t launch_qk_rope(float *qkv, const float *parts, int nparts, const int32_t *pos_thw,
-                          const float *q_norm, const float *k_norm, int T, int Hq, int Hkv, int d,
-                          float eps, const RopeParams &rp, hipStream_t s) {
-  if (T <= 0) return hipSuccess;
-  if (nparts > kMaxParts) return hipErrorInvalidValue;
-  const Parts pt{parts ? parts : qkv, parts ? nparts : 0, (size_t)T * (Hq + 2 * Hkv) * d};
-  const int items = (Hq + Hkv) * (d / 2) + (pt.np ? Hkv * d : 0);
-  hipLaunchKernelGGL(k_qk_rope, dim3(T, (items + 255) / 256), dim3(256), 0, s, qkv, pt, pos_thw,
-                     q_norm, k_norm, T, Hq, Hkv, d, eps, rp);
+hipError_t launch_rope_table(const int32_t *pos_thw, int T, int half, const RopeParams &rp, float *rcos,
+                             float *rsin, hipStream_t s) {
+  const size_t n = (size_t)T * half;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_rope_table, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, pos_thw, T, half,
+                     rp, rcos, rsin);
   return hipGetLastError();
 }
 
