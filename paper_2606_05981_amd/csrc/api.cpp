@@ -19,17 +19,34 @@ using namespace mte;
 
 namespace {
 
-typedef uint16_t bf16_storage;
 constexpr int64_t kMaxTokens = (1 << 24) - 1;  // positions and offsets stay exact in fp32 / int32
 constexpr int kNumClasses = 5;
 
 struct LayerW {
-  void *w_qkv, *w_o, *w_gu, *w_d;              // storage type, repacked
+  void *w_qkv, *w_o, *w_gu, *w_d;              // operand type (fp16 or fp32), repacked
   float *attn_norm, *mlp_norm, *q_norm, *k_norm;
+  // Products are multiplied by s_* (the inverse of the weight's and the
+  // activation's power-of-two pre-scales); the attention output and the
+  // SwiGLU output are pre-scaled by o_pre / y_pre before rounding to fp16.
+  float s_qkv = 1.f, s_o = 1.f, s_gu = 1.f, s_d = 1.f, o_pre = 1.f, y_pre = 1.f;
 };
 
 size_t esize(int dtype) { return dtype == MTE_BF16 ? 2 : 4; }
 int in_fmt(int dtype) { return dtype == MTE_BF16 ? FMT_BF16 : FMT_F32; }
+
+// Exponent e with x in [2^(e-1), 2^e) (frexp), 0 for x <= 0.
+int exp2_of(double x) {
+  if (!(x > 0.0)) return 0;
+  int e = 0;
+  std::frexp(x, &e);
+  return e;
+}
+// Weight pre-scale exponent: the largest magnitude lands in [2^14, 2^15),
+// where every bf16 value down to 2^-31 of it converts to fp16 exactly.
+int weight_shift(double maxabs) { return maxabs > 0.0 ? 15 - exp2_of(maxabs) : 0; }
+// Activation pre-scale exponent (>= 0, applied as 2^-k): values bounded by
+// `bound` stay within 2^15 after scaling, well inside fp16's range.
+int act_shift(double bound) { return std::max(0, exp2_of(bound) - 15); }
 
 }  // namespace
 
@@ -40,8 +57,7 @@ struct mte_encoder {
   void *wbuf = nullptr;      // all GEMM weights
   float *gbuf = nullptr;     // all norm gains (fp32)
   float *final_norm = nullptr;
-  // Activations feeding the matrix cores are fp32 (MODE_F32) or bf16 hi/lo
-  // planes (MODE_BF16X2); both take 4 bytes per element.
+  // Activations feeding the matrix cores are fp32 (MODE_F32) or fp16 (MODE_F16).
   int mode = MODE_F32;
   int act_fmt = FMT_F32;
   float *h = nullptr;        // [max_tokens, D] fp32 residual stream
@@ -185,7 +201,7 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
   e->cfg = c;
   if (hipGetDevice(&e->device) != hipSuccess) { delete e; return MTE_E_HIP; }
 
-  const size_t es = esize(c.dtype);
+  const size_t es = esize(c.dtype);              // weights and activations: fp16 or fp32
   const size_t D = c.hidden, F = c.ffn, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads;
   const size_t nqkv = (Hq + 2 * Hkv) * d;
   const size_t b_qkv = nqkv * D * es, b_o = D * Hq * d * es, b_gu = 2 * F * D * es, b_d = D * F * es;
@@ -197,13 +213,13 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
   if (c.n_layers > 0 && hipMalloc(&e->wbuf, per_layer * c.n_layers) != hipSuccess) return fail(MTE_E_OOM);
   if (hipMalloc((void **)&e->gbuf, (g_per_layer * c.n_layers + D) * sizeof(float)) != hipSuccess)
     return fail(MTE_E_OOM);
-  e->mode = c.dtype == MTE_BF16 ? MODE_BF16X2 : MODE_F32;
-  e->act_fmt = c.dtype == MTE_BF16 ? FMT_BF16X2 : FMT_F32;
+  e->mode = c.dtype == MTE_BF16 ? MODE_F16 : MODE_F32;
+  e->act_fmt = c.dtype == MTE_BF16 ? FMT_F16 : FMT_F32;
   if (hipMalloc((void **)&e->h, MT * D * sizeof(float)) != hipSuccess ||
-      hipMalloc(&e->xn, MT * D * 4) != hipSuccess ||
+      hipMalloc(&e->xn, MT * D * es) != hipSuccess ||
       hipMalloc((void **)&e->qkv, MT * nqkv * sizeof(float)) != hipSuccess ||
-      hipMalloc(&e->attn, MT * Hq * d * 4) != hipSuccess ||
-      hipMalloc(&e->act, MT * F * 4) != hipSuccess)
+      hipMalloc(&e->attn, MT * Hq * d * es) != hipSuccess ||
+      hipMalloc(&e->act, MT * F * es) != hipSuccess)
     return fail(MTE_E_OOM);
   // K splits are planned for at most 256 rows and 8 splits.
   e->ws_elems = 8 * std::min<size_t>(MT, 256) * std::max(std::max(nqkv, 2 * F), D);
@@ -212,10 +228,41 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
       hipMalloc((void **)&e->rsin, MT * (d / 2) * sizeof(float)) != hipSuccess)
     return fail(MTE_E_OOM);
 
-  // Repack the weights: fused [Wq; Wk; Wv], gate/up interleaved in blocks
-  // of 32 rows, fp32 norm gains.
+  const int sf = in_fmt(c.dtype);
+  const bool f16 = c.dtype == MTE_BF16;
   e->layers.resize(c.n_layers);
   hipError_t he = hipSuccess;
+  // Range analysis (bf16 weights only): per layer the max |w| of each
+  // projection, the largest row norms of Wv, Wgate and Wup, and the largest
+  // norm gains, from which the power-of-two pre-scales follow.
+  enum { S_Q, S_K, S_V, S_O, S_G, S_U, S_D, S_AN, S_MN, S_N };
+  std::vector<float> st_h;
+  if (f16 && c.n_layers > 0) {
+    float *st = nullptr;
+    const size_t nst = (size_t)c.n_layers * S_N * 2;
+    if (hipMalloc((void **)&st, nst * sizeof(float)) != hipSuccess) return fail(MTE_E_OOM);
+    he = hipMemsetAsync(st, 0, nst * sizeof(float), stream);
+    for (int l = 0; l < c.n_layers && he == hipSuccess; ++l) {
+      const mte_layer_weights &L = w->layers[l];
+      float *sl = st + (size_t)l * S_N * 2;
+      const struct { const void *p; size_t rows, cols; } m[S_N] = {
+          {L.w_q, Hq * d, D}, {L.w_k, Hkv * d, D}, {L.w_v, Hkv * d, D}, {L.w_o, D, Hq * d},
+          {L.w_gate, F, D},   {L.w_up, F, D},      {L.w_down, D, F},    {L.attn_norm, 1, D},
+          {L.mlp_norm, 1, D}};
+      for (int k = 0; k < S_N && he == hipSuccess; ++k)
+        he = launch_matrix_stats(sf, m[k].p, (int)m[k].rows, (int)m[k].cols, sl + 2 * k, stream);
+    }
+    st_h.resize(nst);
+    if (he == hipSuccess) he = hipMemcpyAsync(st_h.data(), st, nst * sizeof(float), hipMemcpyDeviceToHost, stream);
+    if (he == hipSuccess) he = hipStreamSynchronize(stream);
+    hipFree(st);
+    if (he != hipSuccess) return fail(MTE_E_HIP);
+  }
+
+  // Repack: fused [Wq; Wk; Wv], gate/up interleaved in blocks of 16 rows,
+  // converted to the operand type with the weight pre-scales; fp32 norm
+  // gains with the activation pre-scales folded in.
+  const double sqrtD = std::sqrt((double)D);
   for (int l = 0; l < c.n_layers && he == hipSuccess; ++l) {
     const mte_layer_weights &L = w->layers[l];
     char *base = (char *)e->wbuf + per_layer * l;
@@ -229,20 +276,55 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
     o.mlp_norm = gb + D;
     o.q_norm = gb + 2 * D;
     o.k_norm = gb + 2 * D + d;
+    int w_qkv = 0, w_o = 0, w_gu = 0, w_d = 0, ka = 0, km = 0, ko = 0, ky = 0;
+    if (f16) {
+      const float *sl = &st_h[(size_t)l * S_N * 2];
+      auto mx = [&](int k) { return (double)sl[2 * k]; };
+      auto rn = [&](int k) { return (double)sl[2 * k + 1] * 1.001; };   // fp32 norm rounding margin
+      w_qkv = weight_shift(std::max(mx(S_Q), std::max(mx(S_K), mx(S_V))));
+      w_o = weight_shift(mx(S_O));
+      w_gu = weight_shift(std::max(mx(S_G), mx(S_U)));
+      w_d = weight_shift(mx(S_D));
+      // |RMSNorm(x) * g|_2 <= sqrt(D) max|g|, so every element of the norm
+      // output, of v (hence of the attention output, a convex combination
+      // of v rows) and of gate / up is bounded by that times the row norm
+      // of its weight; |silu(z)| <= |z|.
+      const double ba = sqrtD * mx(S_AN), bm = sqrtD * mx(S_MN);
+      ka = act_shift(ba);
+      km = act_shift(bm);
+      ko = act_shift(ba * rn(S_V));
+      ky = act_shift((bm * rn(S_G)) * (bm * rn(S_U)));
+    }
+    o.s_qkv = std::ldexp(1.f, ka - w_qkv);
+    o.s_o = std::ldexp(1.f, ko - w_o);
+    o.s_gu = std::ldexp(1.f, km - w_gu);
+    o.s_d = std::ldexp(1.f, ky - w_d);
+    o.o_pre = std::ldexp(1.f, -ko);
+    o.y_pre = std::ldexp(1.f, -ky);
+    const int df = f16 ? FMT_F16 : FMT_F32;
     const size_t bq = Hq * d * D * es, bk = Hkv * d * D * es;
-    he = hipMemcpyAsync(o.w_qkv, L.w_q, bq, hipMemcpyDeviceToDevice, stream);
-    if (he == hipSuccess) he = hipMemcpyAsync((char *)o.w_qkv + bq, L.w_k, bk, hipMemcpyDeviceToDevice, stream);
-    if (he == hipSuccess) he = hipMemcpyAsync((char *)o.w_qkv + bq + bk, L.w_v, bk, hipMemcpyDeviceToDevice, stream);
-    if (he == hipSuccess) he = hipMemcpyAsync(o.w_o, L.w_o, b_o, hipMemcpyDeviceToDevice, stream);
-    if (he == hipSuccess) he = hipMemcpyAsync(o.w_d, L.w_down, b_d, hipMemcpyDeviceToDevice, stream);
-    if (he == hipSuccess) he = launch_interleave_gate_up((int)es, L.w_gate, L.w_up, o.w_gu, (int)F, (int)D, stream);
-    if (he == hipSuccess) he = launch_to_f32(in_fmt(c.dtype), L.attn_norm, o.attn_norm, (int)D, stream);
-    if (he == hipSuccess) he = launch_to_f32(in_fmt(c.dtype), L.mlp_norm, o.mlp_norm, (int)D, stream);
-    if (he == hipSuccess && c.qk_norm) he = launch_to_f32(in_fmt(c.dtype), L.q_norm, o.q_norm, (int)d, stream);
-    if (he == hipSuccess && c.qk_norm) he = launch_to_f32(in_fmt(c.dtype), L.k_norm, o.k_norm, (int)d, stream);
+    const float sq = std::ldexp(1.f, w_qkv);
+    he = launch_convert_rows(sf, L.w_q, df, o.w_qkv, (int)(Hq * d), (int)D, sq, 0, 0, stream);
+    if (he == hipSuccess)
+      he = launch_convert_rows(sf, L.w_k, df, (char *)o.w_qkv + bq, (int)(Hkv * d), (int)D, sq, 0, 0, stream);
+    if (he == hipSuccess)
+      he = launch_convert_rows(sf, L.w_v, df, (char *)o.w_qkv + bq + bk, (int)(Hkv * d), (int)D, sq, 0, 0,
+                               stream);
+    if (he == hipSuccess)
+      he = launch_convert_rows(sf, L.w_o, df, o.w_o, (int)D, (int)(Hq * d), std::ldexp(1.f, w_o), 0, 0, stream);
+    if (he == hipSuccess)
+      he = launch_convert_rows(sf, L.w_gate, df, o.w_gu, (int)F, (int)D, std::ldexp(1.f, w_gu), 1, 0, stream);
+    if (he == hipSuccess)
+      he = launch_convert_rows(sf, L.w_up, df, o.w_gu, (int)F, (int)D, std::ldexp(1.f, w_gu), 1, 1, stream);
+    if (he == hipSuccess)
+      he = launch_convert_rows(sf, L.w_down, df, o.w_d, (int)D, (int)F, std::ldexp(1.f, w_d), 0, 0, stream);
+    if (he == hipSuccess) he = launch_to_f32(sf, L.attn_norm, o.attn_norm, (int)D, std::ldexp(1.f, -ka), stream);
+    if (he == hipSuccess) he = launch_to_f32(sf, L.mlp_norm, o.mlp_norm, (int)D, std::ldexp(1.f, -km), stream);
+    if (he == hipSuccess && c.qk_norm) he = launch_to_f32(sf, L.q_norm, o.q_norm, (int)d, 1.f, stream);
+    if (he == hipSuccess && c.qk_norm) he = launch_to_f32(sf, L.k_norm, o.k_norm, (int)d, 1.f, stream);
   }
   e->final_norm = e->gbuf + g_per_layer * c.n_layers;
-  if (he == hipSuccess) he = launch_to_f32(in_fmt(c.dtype), w->final_norm, e->final_norm, (int)D, stream);
+  if (he == hipSuccess) he = launch_to_f32(sf, w->final_norm, e->final_norm, (int)D, 1.f, stream);
   if (he == hipSuccess) he = hipStreamSynchronize(stream);
   if (he != hipSuccess) return fail(MTE_E_HIP);
 
@@ -285,22 +367,13 @@ struct Timer {
   }
 };
 
-// Second plane of a bf16x2 activation buffer with `cols` columns.
-void *lo_plane(const mte_encoder *e, void *buf, size_t cols) {
-  return e->mode == MODE_BF16X2 ? (void *)((bf16_storage *)buf + (size_t)e->cfg.max_tokens * cols) : nullptr;
-}
-
 // Runs layers [l0, l1) on the fp32 residual stream `h` (T rows).
-hipError_t run_layers(mte_encoder *e, float *h, const int32_t *pos, const std::vector<int32_t> &cu,
-                      int batch, int T, int l0, int l1, bool first_norm_done, int *pending,
-                      hipStream_t s) {
+hipError_t run_layers(mte_encoder *e, float *h, const std::vector<int32_t> &cu, int batch, int T, int l0,
+                      int l1, bool first_norm_done, int *pending, hipStream_t s) {
   const mte_config &c = e->cfg;
   const int D = c.hidden, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
   const int nqkv = (Hq + 2 * Hkv) * d;
-  const size_t MT = c.max_tokens;
   const int mode = e->mode, af = e->act_fmt;
-  void *xn_lo = lo_plane(e, e->xn, D), *attn_lo = lo_plane(e, e->attn, (size_t)Hq * d),
-       *act_lo = lo_plane(e, e->act, F);
   float *ws = e->ws;
   const size_t wn = e->ws_elems;
   // `*pending` counts the partial sums of a K-split residual projection
@@ -311,38 +384,37 @@ hipError_t run_layers(mte_encoder *e, float *h, const int32_t *pos, const std::v
   for (int l = l0; l < l1; ++l) {
     const LayerW &W = e->layers[l];
     if (!(l == l0 && first_norm_done))
-      MTE_TRY(launch_rmsnorm(FMT_F32, af, h, np ? h : nullptr, np ? ws : nullptr, np, W.attn_norm, e->xn, MT * D, T,
+      MTE_TRY(launch_rmsnorm(FMT_F32, af, h, np ? h : nullptr, np ? ws : nullptr, np, W.attn_norm, e->xn, T,
                              D, c.rms_eps, s));
     int sp = 0;
     const QkvEpi qe{e->rcos, e->rsin, c.qk_norm ? W.q_norm : nullptr, c.qk_norm ? W.k_norm : nullptr,
                     (Hq + Hkv) * d, Hq * d, d, c.rms_eps};
     {
       Timer t(e, 0, s);
-      MTE_TRY(launch_gemm(mode, EPI_QKV, e->xn, xn_lo, W.w_qkv, e->qkv, 0, T, nqkv, D, nqkv, ws, wn,
+      MTE_TRY(launch_gemm(mode, EPI_QKV, e->xn, W.w_qkv, e->qkv, T, nqkv, D, nqkv, W.s_qkv, 1.f, ws, wn,
                           &sp, &qe, s));
     }
     if (sp) MTE_TRY(launch_qkv_parts(e->qkv, ws, sp, T, Hq, Hkv, qe, s));
     {
       Timer t(e, 1, s);
-      MTE_TRY(launch_attention(mode, e->qkv, e->attn, MT * Hq * d, cu.data(), batch, Hq, Hkv, d, s));
+      MTE_TRY(launch_attention(mode, e->qkv, e->attn, W.o_pre, cu.data(), batch, Hq, Hkv, d, s));
     }
     {
       Timer t(e, 2, s);
-      MTE_TRY(launch_gemm(mode, EPI_RESID, e->attn, attn_lo, W.w_o, h, 0, T, D, Hq * d, D, ws, wn, &np,
+      MTE_TRY(launch_gemm(mode, EPI_RESID, e->attn, W.w_o, h, T, D, Hq * d, D, W.s_o, 1.f, ws, wn, &np,
                           nullptr, s));
     }
-    MTE_TRY(launch_rmsnorm(FMT_F32, af, h, np ? h : nullptr, np ? ws : nullptr, np, W.mlp_norm, e->xn, MT * D, T, D,
+    MTE_TRY(launch_rmsnorm(FMT_F32, af, h, np ? h : nullptr, np ? ws : nullptr, np, W.mlp_norm, e->xn, T, D,
                            c.rms_eps, s));
     {
       Timer t(e, 3, s);
-      MTE_TRY(launch_gemm(mode, EPI_SWIGLU, e->xn, xn_lo, W.w_gu, e->act, MT * F, T, 2 * F, D, F, ws,
-                          wn, &sp, nullptr, s));
+      MTE_TRY(launch_gemm(mode, EPI_SWIGLU, e->xn, W.w_gu, e->act, T, 2 * F, D, F, W.s_gu, W.y_pre, ws, wn,
+                          &sp, nullptr, s));
     }
-    if (sp) MTE_TRY(launch_swiglu_parts(af, ws, sp, T, F, e->act, MT * F, s));
+    if (sp) MTE_TRY(launch_swiglu_parts(af, ws, sp, T, F, e->act, W.y_pre, s));
     {
       Timer t(e, 4, s);
-      MTE_TRY(launch_gemm(mode, EPI_RESID, e->act, act_lo, W.w_d, h, 0, T, D, F, D, ws, wn, &np, nullptr,
-                          s));
+      MTE_TRY(launch_gemm(mode, EPI_RESID, e->act, W.w_d, h, T, D, F, D, W.s_d, 1.f, ws, wn, &np, nullptr, s));
     }
   }
 #undef MTE_TRY
@@ -383,20 +455,20 @@ int mte_encode(mte_encoder *e, const void *embeds, const int32_t *pos_thw, const
   const int out_fmt = in_fmt(c.out_dtype);
   if (c.n_layers == 0) {
     err = launch_rmsnorm(in_fmt(c.dtype), out_fmt, embeds, nullptr, nullptr, 0, e->final_norm,
-                         out_hidden, 0, T, c.hidden, c.rms_eps, stream);
+                         out_hidden, T, c.hidden, c.rms_eps, stream);
     return err == hipSuccess ? MTE_OK : MTE_E_HIP;
   }
   err = launch_rope_table(pos_thw, T, c.head_dim / 2, e->rope, e->rcos, e->rsin, stream);
   // Layer 0's attention norm also seeds the fp32 residual stream from the embeddings.
   if (err == hipSuccess)
     err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, embeds, e->h, nullptr, 0, e->layers[0].attn_norm,
-                       e->xn, (size_t)c.max_tokens * c.hidden, T, c.hidden, c.rms_eps, stream);
+                         e->xn, T, c.hidden, c.rms_eps, stream);
   int np = 0;
   if (err == hipSuccess)
-    err = run_layers(e, e->h, pos_thw, cu, batch, T, 0, c.n_layers, true, &np, stream);
+    err = run_layers(e, e->h, cu, batch, T, 0, c.n_layers, true, &np, stream);
   if (err == hipSuccess)
     err = launch_rmsnorm(FMT_F32, out_fmt, e->h, nullptr, np ? e->ws : nullptr, np, e->final_norm,
-                         out_hidden, 0, T, c.hidden, c.rms_eps, stream);
+                         out_hidden, T, c.hidden, c.rms_eps, stream);
   return err == hipSuccess ? MTE_OK : MTE_E_HIP;
 }
 
@@ -420,7 +492,7 @@ int mte_encode_layers(mte_encoder *e, const float *h_in, const int32_t *pos_thw,
     err = launch_rope_table(pos_thw, T, e->cfg.head_dim / 2, e->rope, e->rcos, e->rsin, stream);
   int np = 0;
   if (err == hipSuccess)
-    err = run_layers(e, h_out, pos_thw, cu, batch, T, layer_begin, layer_end, false, &np, stream);
+    err = run_layers(e, h_out, cu, batch, T, layer_begin, layer_end, false, &np, stream);
   if (err == hipSuccess && np) err = launch_resid_add(h_out, e->ws, np, T, e->cfg.hidden, stream);
   return err == hipSuccess ? MTE_OK : MTE_E_HIP;
 }

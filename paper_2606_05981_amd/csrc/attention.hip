@@ -18,12 +18,13 @@
 //   rescaling of O by the running-max correction is a per-lane scalar).
 //
 // q, k, v arrive in fp32 (the packed QKV projection). MODE_F32 multiplies
-// them on the fp32 matrix cores. MODE_BF16X2 splits every operand x into
-// bf16 hi + lo (lo = bf16(x - hi)) and forms each product from three bf16
-// MFMAs, hi*hi + lo*hi + hi*lo (the lo*lo term is below fp32 accumulation
-// noise). The sequence table (offsets, first tile of each sequence) is
-// passed by value in the kernel arguments, so nothing is read back to the
-// host.
+// them on the fp32 matrix cores and writes fp32. MODE_F16 splits every
+// operand x into bf16 hi + lo (lo = bf16(x - hi)) and forms each product
+// from three bf16 MFMAs, hi*hi + lo*hi + hi*lo (the lo*lo term is below fp32
+// accumulation noise), and writes o times a power-of-two pre-scale as fp16,
+// the operand type of the output projection. The sequence table (offsets,
+// first tile of each sequence) is passed by value in the kernel arguments,
+// so nothing is read back to the host.
 #include <type_traits>
 
 #include "common.h"
@@ -36,7 +37,7 @@ constexpr int kMaxSeqPerLaunch = 256;
 struct AttnArgs {
   const float *qkv;   // [T, ld_qkv] fp32
   char *o;
-  size_t o_plane;  // elements between the hi and lo planes of o (MODE_BF16X2)
+  float o_scale;   // output multiplier (MODE_F16)
   int ld_qkv;      // floats per token row of qkv
   int Hq, Hkv, rep;
   int wph;         // waves per query head (query rows per workgroup = 32 * wph)
@@ -78,7 +79,7 @@ __device__ __forceinline__ int vt_pos(int k) {
 template <int MODE, int HD>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   typedef typename std::conditional<MODE == MODE_F32, float, bf16>::type T;
-  constexpr int NP = (MODE == MODE_BF16X2) ? 2 : 1;   // planes per operand
+  constexpr int NP = (MODE == MODE_F16) ? 2 : 1;   // bf16 planes per operand
   constexpr int KV = 32;
   constexpr int EC = 16 / (int)sizeof(T);        // elements per 16-byte chunk
   constexpr int NCH = HD / EC;                   // chunks per head row
@@ -305,7 +306,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   // along d (a lane owns a query row in the accumulator layout, which would
   // scatter 2-byte stores across rows).
   const float lt = l_i + __shfl_xor(l_i, 32, kWave);
-  const float inv = 1.f / lt;
+  const float inv = (MODE == MODE_F32 ? 1.f : a.o_scale) / lt;
   float *so = sOall + wave * 32 * OTP;
 #pragma unroll
   for (int n = 0; n < ND; ++n)
@@ -325,27 +326,23 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       if constexpr (MODE == MODE_F32) {
         *(f32x4 *)((float *)a.o + o) = y;
       } else {
-        bf16x4 h, l;
+        f16x4 h;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          h[e] = (bf16)y[e];
-          l[e] = (bf16)(y[e] - (float)h[e]);
-        }
-        *(bf16x4 *)((bf16 *)a.o + o) = h;
-        *(bf16x4 *)((bf16 *)a.o + o + a.o_plane) = l;
+        for (int e = 0; e < 4; ++e) h[e] = (f16)y[e];
+        *(f16x4 *)((f16 *)a.o + o) = h;
       }
     }
   }
 }
 
-hipError_t launch_attention(int mode, const float *qkv, void *o, size_t o_plane, const int32_t *cu,
+hipError_t launch_attention(int mode, const float *qkv, void *o, float out_scale, const int32_t *cu,
                             int batch, int Hq, int Hkv, int d, hipStream_t s) {
   const int rep = Hq / Hkv;
   AttnArgs a;
   a.qkv = qkv;
   a.ld_qkv = (Hq + 2 * Hkv) * d;
   a.o = (char *)o;
-  a.o_plane = o_plane;
+  a.o_scale = out_scale;
   a.Hq = Hq;
   a.Hkv = Hkv;
   a.rep = rep;
@@ -366,9 +363,9 @@ hipError_t launch_attention(int mode, const float *qkv, void *o, size_t o_plane,
     a.tile0[n] = tiles;
     if (tiles == 0) continue;
     dim3 grid(tiles, Hkv * a.head_blocks);
-    if (mode == MODE_BF16X2) {
-      if (d == 128) hipLaunchKernelGGL((k_attn<MODE_BF16X2, 128>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((k_attn<MODE_BF16X2, 64>), grid, dim3(256), 0, s, a);
+    if (mode == MODE_F16) {
+      if (d == 128) hipLaunchKernelGGL((k_attn<MODE_F16, 128>), grid, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((k_attn<MODE_F16, 64>), grid, dim3(256), 0, s, a);
     } else {
       if (d == 128) hipLaunchKernelGGL((k_attn<MODE_F32, 128>), grid, dim3(256), 0, s, a);
       else hipLaunchKernelGGL((k_attn<MODE_F32, 64>), grid, dim3(256), 0, s, a);

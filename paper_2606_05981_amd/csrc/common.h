@@ -9,6 +9,9 @@ namespace mte {
 typedef __bf16 bf16;
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16;
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -18,13 +21,16 @@ constexpr int kWave = 64;
 
 __device__ __forceinline__ float to_f32(float x) { return x; }
 __device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
+__device__ __forceinline__ float to_f32(f16 x) { return (float)x; }
 template <typename T> __device__ __forceinline__ T from_f32(float x);
 template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
 // float -> bf16 conversion rounds to nearest, ties to even (gfx950 v_cvt_pk_bf16_f32).
 template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
+// float -> fp16 rounds to nearest, ties to even (v_cvt_f16_f32).
+template <> __device__ __forceinline__ f16 from_f32<f16>(float x) { return (f16)x; }
 
-// A 16-byte per-lane MFMA operand fragment. For bf16 it is one
-// v_mfma_f32_32x32x16_bf16 operand (8 values, k-extent 16); for f32 it is four
+// A 16-byte per-lane MFMA operand fragment. For bf16 / fp16 it is one
+// v_mfma_f32_32x32x16_{bf16,f16} operand (8 values, k-extent 16); for f32 it is four
 // v_mfma_f32_32x32x2_f32 operands (one value each, k-extent 8 in total).
 // In both cases lane l supplies row (l % 32) and k-slot group (l / 32); A and
 // B fragments use the same (group, element) -> k assignment, so the dot
@@ -34,6 +40,10 @@ template <> struct Frag<bf16> {
   typedef bf16x8 type;
   static constexpr int kElems = 8;
 };
+template <> struct Frag<f16> {
+  typedef f16x8 type;
+  static constexpr int kElems = 8;
+};
 template <> struct Frag<float> {
   typedef f32x4 type;
   static constexpr int kElems = 4;
@@ -41,6 +51,9 @@ template <> struct Frag<float> {
 
 __device__ __forceinline__ void mfma32(f32x16 &acc, const bf16x8 &a, const bf16x8 &b) {
   acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mfma32(f32x16 &acc, const f16x8 &a, const f16x8 &b) {
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, acc, 0, 0, 0);
 }
 __device__ __forceinline__ void mfma32(f32x16 &acc, const f32x4 &a, const f32x4 &b) {
   acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b[0], acc, 0, 0, 0);

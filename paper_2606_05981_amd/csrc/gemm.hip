@@ -4,13 +4,15 @@
 // W = weights in nn.Linear layout (row-major, K contiguous).
 //
 // Precision modes:
-//  MODE_F32:   A and W fp32, v_mfma_f32_32x32x2_f32.
-//  MODE_BF16X2: W bf16; A carried as two bf16 planes, A = A_hi + A_lo with
-//   A_hi = bf16(A), A_lo = bf16(A - A_hi) (a ~16-bit significand). Each
-//   fragment costs two v_mfma_f32_32x32x16_bf16 (A_hi W + A_lo W) into one
-//   fp32 accumulator. bf16 activations alone (8-bit significand) put the
-//   per-layer error well above 1e-2 of the hidden-state RMS; the split keeps
-//   it near 1e-4 while the weights stay bf16.
+//  MODE_F32: A and W fp32, v_mfma_f32_32x32x2_f32.
+//  MODE_F16: A and W fp16, v_mfma_f32_32x32x16_f16, fp32 accumulation. The
+//   weights are bf16 values held as fp16 times a power of two chosen per
+//   matrix so that its largest magnitude lands in [2^14, 2^15): every bf16
+//   value down to 2^-31 of that maximum converts exactly. Activations are
+//   rounded once to fp16 (an 11-bit significand, against bf16's 8) after a
+//   power-of-two pre-scale that a static bound keeps in fp16 range; the
+//   epilogue multiplies the product by the inverse of both scales (`scale`,
+//   exact). One MFMA per fragment at the same dense rate as bf16.
 //
 // Each workgroup (4 waves) owns a BM x BN output tile; each wave a
 // (BM/WM) x (BN/WN) block of 32x32 MFMA tiles. K is walked in stages of 128
@@ -26,9 +28,11 @@
 // embedding of the q and k heads (QKV projection; a wave's columns cover
 // whole heads, so a head's sum of squares is a reduction over the wave's
 // lanes and both members of each rotary pair sit in one lane), SwiGLU over
-// interleaved gate/up rows (MLP up-projection, written in the activation
-// format) and accumulation into the fp32 residual stream (attention output
-// projection and MLP down-projection). With K split over workgroups (small M), each
+// gate/up rows interleaved in blocks of 16 (MLP up-projection: a 32-column
+// MFMA tile holds 16 gate and the 16 matching up columns, paired by one
+// lane exchange; written in the activation format) and accumulation into
+// the fp32 residual stream (attention output projection and MLP
+// down-projection). With K split over workgroups (small M), each
 // split stores its partial sum instead, and the kernel that consumes the
 // product adds the partials up in split order, so results do not depend on
 // the order in which workgroups finish.
@@ -41,14 +45,14 @@
 namespace mte {
 
 struct GemmArgs {
-  const char *A;      // A (MODE_F32) or A_hi (MODE_BF16X2)
-  const char *A_lo;   // A_lo plane (MODE_BF16X2)
+  const char *A;
   const char *W;
   void *C;            // EPI_STORE / EPI_RESID / EPI_PARTIAL: float; EPI_SWIGLU: activation format
-  size_t c_plane;     // EPI_SWIGLU, MODE_BF16X2: elements between C_hi and C_lo planes;
-                      // EPI_PARTIAL: elements between the partial sums of two K splits
+  size_t c_plane;     // EPI_PARTIAL: elements between the partial sums of two K splits
   int M, N, K, ldc;
   int k_chunk;        // K range of one split (gridDim.z splits)
+  float scale;        // product multiplier (inverse operand pre-scales)
+  float out_scale;    // EPI_SWIGLU output multiplier
   QkvEpi qe;          // EPI_QKV
 };
 
@@ -151,7 +155,7 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const 
       const int m = mw + i * 32 + acc_row(r, lane);
       float v[TN];
 #pragma unroll
-      for (int j = 0; j < TN; ++j) v[j] = acc[i][j][r];
+      for (int j = 0; j < TN; ++j) v[j] = acc[i][j][r] * g.scale;
 #pragma unroll
       for (int h = 0; h < NH; ++h) {
         if (!rot[h]) continue;
@@ -191,17 +195,16 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const 
 // the barrier; the waits are explicit.
 template <int MODE, int BM, int BN, int WM, int WN, int ROWB, int P, int EPI, int OCC>
 __global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void k_gemm(GemmArgs g) {
-  typedef typename std::conditional<MODE == MODE_F32, float, bf16>::type T;
-  constexpr int NA = (MODE == MODE_BF16X2) ? 2 : 1;   // A planes
+  typedef typename std::conditional<MODE == MODE_F32, float, f16>::type T;
   constexpr int KS = ROWB / (int)sizeof(T);       // k elements per stage
   constexpr int CH = ROWB / 16;                   // 16-byte chunks per row per stage
   constexpr int WTM = BM / WM, WTN = BN / WN;     // wave tile
   constexpr int TM = WTM / 32, TN = WTN / 32;     // 32x32 MFMA tiles per wave
-  constexpr int ACH = BM * CH, BCH = BN * CH;     // chunks per stage (one A plane / W)
+  constexpr int ACH = BM * CH, BCH = BN * CH;     // chunks per stage (A / W)
   static_assert(ACH % 256 == 0 && BCH % 256 == 0, "whole DMA rounds");
   constexpr int AR = ACH / 256, BR = BCH / 256;   // DMA instructions per thread per matrix
-  constexpr int LOADS = NA * AR + BR;             // per thread per stage
-  constexpr int STAGE = (NA * BM + BN) * CH;      // u32x4 slots per stage
+  constexpr int LOADS = AR + BR;                  // per thread per stage
+  constexpr int STAGE = (BM + BN) * CH;           // u32x4 slots per stage
   static_assert(WM * WN == 4, "4 waves");
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
   static_assert(LOADS * (P - 2) < 64 && P >= 3 && P <= 6, "vmcnt range, ring depth");
@@ -212,7 +215,7 @@ __global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, O
   const int wm = wave / WN, wn = wave % WN;
   const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
   const int M = g.M;
-  const size_t rowb = (size_t)g.K * sizeof(T);    // row pitch in bytes (A planes and W)
+  const size_t rowb = (size_t)g.K * sizeof(T);    // row pitch in bytes (A and W)
   const size_t kb0 = (size_t)blockIdx.z * g.k_chunk * sizeof(T);
   const int nk = g.k_chunk / KS;
 
@@ -230,20 +233,17 @@ __global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, O
     const int q = (c * 4 + wave) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
     pb[c] = g.W + (size_t)(n0 + r) * rowb + kb0 + ch * 16;
   }
-  const ptrdiff_t lo_off = (MODE == MODE_BF16X2) ? (g.A_lo - g.A) : 0;
-  // Loads K-stage `ks` into ring slot `slot`.
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
   const int uwave = __builtin_amdgcn_readfirstlane(wave);   // wave-uniform in an SGPR
   // DMA load x (0 <= x < LOADS) of K-stage `ks` into ring slot `slot`.
   auto dma_one = [&](int ks, int slot, int x) {
     const uint32_t st = lds0 + (uint32_t)(slot * STAGE) * 16u;
     const size_t ko = (size_t)ks * ROWB;
-    if (x < NA * AR) {
-      const int p = x / AR, c = x % AR;
-      dma16(pa[c] + p * lo_off + ko, st + (uint32_t)(p * ACH + (c * 4 + uwave) * 64) * 16u);
+    if (x < AR) {
+      dma16(pa[x] + ko, st + (uint32_t)((x * 4 + uwave) * 64) * 16u);
     } else {
-      const int c = x - NA * AR;
-      dma16(pb[c] + ko, st + (uint32_t)(NA * ACH + (c * 4 + uwave) * 64) * 16u);
+      const int c = x - AR;
+      dma16(pb[c] + ko, st + (uint32_t)(ACH + (c * 4 + uwave) * 64) * 16u);
     }
   };
 
@@ -255,30 +255,30 @@ __global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, O
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  frag_t fa[2][NA][TM], fb[2][TN];
+  frag_t fa[2][TM], fb[2][TN];
   const int lrow = lane & 31, lgrp = lane >> 5;
   // Fragment read x (0 <= x < NR) of k-step kk of the stage at `st` into
   // buffer b, in the order the MFMAs consume them: the W fragments, then the
-  // A fragments of each plane.
+  // A fragments.
   auto read_one = [&](const u32x4 *st, int kk, int b, int x) {
     const int ch = kk * 2 + lgrp;
     if (x < TN) {
       const int r = wn * WTN + x * 32 + lrow;
-      fb[b][x] = __builtin_bit_cast(frag_t, st[NA * ACH + r * CH + swz<CH>(r, ch)]);
+      fb[b][x] = __builtin_bit_cast(frag_t, st[ACH + r * CH + swz<CH>(r, ch)]);
     } else {
-      const int p = (x - TN) / TM, i = (x - TN) % TM;
+      const int i = x - TN;
       const int r = wm * WTM + i * 32 + lrow;
-      fa[b][p][i] = __builtin_bit_cast(frag_t, st[p * ACH + r * CH + swz<CH>(r, ch)]);
+      fa[b][i] = __builtin_bit_cast(frag_t, st[r * CH + swz<CH>(r, ch)]);
     }
   };
   auto mfma_one = [&](int b, int x) {
-    const int j = x % TN, i = (x / TN) % TM, p = x / (TN * TM);
-    mfma32(acc[i][j], fa[b][p][i], fb[b][j]);
+    const int j = x % TN, i = x / TN;
+    mfma32(acc[i][j], fa[b][i], fb[b][j]);
   };
   constexpr int KK = CH / 2;                      // 16-k steps per stage (even)
   static_assert(KK % 2 == 0, "fragment buffer parity");
-  constexpr int NM = NA * TM * TN;                // MFMAs per k-step
-  constexpr int NR = NA * TM + TN;                // fragment reads per k-step
+  constexpr int NM = TM * TN;                     // MFMAs per k-step
+  constexpr int NR = TM + TN;                     // fragment reads per k-step
   // The loads of one stage are issued in NPART parts: part 0 right after the
   // barrier of stage kt-P+1, parts 1.. in the k-steps before the barrier of
   // stage kt-P+2. With P >= 4 every stage still has P-3 whole stages of loads
@@ -366,89 +366,103 @@ __global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, O
     }
     return;
   }
+  if constexpr (EPI == EPI_SWIGLU) {
+    // Column block j (32 columns) of the interleaved product holds gate
+    // (lanes l%32 < 16) and up (l%32 >= 16) of outputs f = 16*block + l%16.
+    // Of each pair of accumulator rows (r, r+1) the gate lane finishes row r
+    // and the up lane row r+1, each receiving the value it lacks from lane
+    // l ^ 16 (exchanged by all lanes together, outside any row test).
+    const bool upl = lrow >= 16;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int f = ((n0 + wn * WTN + j * 32) >> 1) + (lrow & 15);
+#pragma unroll
+        for (int r = 0; r < 16; r += 2) {
+          const float a0 = acc[i][j][r] * g.scale, a1 = acc[i][j][r + 1] * g.scale;
+          const float recv = __shfl_xor(upl ? a0 : a1, 16, kWave);
+          const float gt = upl ? recv : a0, up = upl ? a1 : recv;
+          const int m = m0 + wm * WTM + i * 32 + acc_row(r + (upl ? 1 : 0), lane);
+          const float y = gt / (1.f + __expf(-gt)) * up * g.out_scale;
+          if (m < M) {
+            const size_t o = (size_t)m * g.ldc + f;
+            if constexpr (MODE == MODE_F32) ((float *)g.C)[o] = y;
+            else ((f16 *)g.C)[o] = (f16)y;
+          }
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int m = m0 + wm * WTM + i * 32 + acc_row(r, lane);
       if (m >= M) continue;
-      if constexpr (EPI == EPI_STORE || EPI == EPI_RESID || EPI == EPI_PARTIAL) {
-        float *C = (float *)g.C + (EPI == EPI_PARTIAL ? (size_t)blockIdx.z * g.c_plane : 0);
+      float *C = (float *)g.C + (EPI == EPI_PARTIAL ? (size_t)blockIdx.z * g.c_plane : 0);
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-          const size_t o = (size_t)m * g.ldc + n0 + wn * WTN + j * 32 + lrow;
-          if constexpr (EPI == EPI_RESID) C[o] += acc[i][j][r];
-          else C[o] = acc[i][j][r];
-        }
-      } else {
-#pragma unroll
-        for (int j = 0; j < TN; j += 2) {
-          const int f = (n0 + wn * WTN + j * 32) / 2 + lrow;
-          const float gt = acc[i][j][r], up = acc[i][j + 1][r];
-          const float y = gt / (1.f + __expf(-gt)) * up;
-          const size_t o = (size_t)m * g.ldc + f;
-          if constexpr (MODE == MODE_F32) {
-            ((float *)g.C)[o] = y;
-          } else {
-            const bf16 hi = (bf16)y;
-            ((bf16 *)g.C)[o] = hi;
-            ((bf16 *)g.C)[o + g.c_plane] = (bf16)(y - (float)hi);
-          }
-        }
+      for (int j = 0; j < TN; ++j) {
+        const size_t o = (size_t)m * g.ldc + n0 + wn * WTN + j * 32 + lrow;
+        if constexpr (EPI == EPI_RESID) C[o] += acc[i][j][r] * g.scale;
+        else C[o] = acc[i][j][r] * g.scale;
       }
     }
   }
 }
 
+
 // ------------------------------------------------------------- planning
 // A tile configuration is a compile-time instantiation; the planner picks
-// one per (M, N, K, epilogue) from the number of workgroups it yields and
-// the work per workgroup.
+// one per (M, N, K, epilogue): from a table of measured choices for the
+// decoder's projections, else from the number of workgroups a tile yields
+// and its measured steady-state rate.
 struct TileCfg {
   int bm, bn, wm, wn, rowb, occ;
 };
 
 template <int MODE, int BM, int BN, int WM, int WN, int ROWB, int P, int EPI, int OCC>
 static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
-  if constexpr ((EPI == EPI_SWIGLU || EPI == EPI_QKV) && (BN / WN) % 64 != 0) {
-    return hipErrorInvalidValue;  // gate/up pairs (or whole heads) need 64 columns per wave
+  if constexpr (EPI == EPI_QKV && (BN / WN) % 64 != 0) {
+    return hipErrorInvalidValue;  // the QK-norm epilogue needs whole heads per wave
   } else {
-  constexpr int NA = (MODE == MODE_BF16X2) ? 2 : 1;
-  constexpr int lds_bytes = P * (NA * BM + BN) * ROWB;
-  auto kern = k_gemm<MODE, BM, BN, WM, WN, ROWB, P, EPI, OCC>;
-  static const hipError_t attr = hipFuncSetAttribute(
-      (const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
-  if (attr != hipSuccess) return attr;
-  dim3 grid(a.N / BN, (a.M + BM - 1) / BM, splits);
-  hipLaunchKernelGGL(kern, grid, dim3(256), lds_bytes, s, a);
-  return hipGetLastError();
+    constexpr int lds_bytes = P * (BM + BN) * ROWB;
+    auto kern = k_gemm<MODE, BM, BN, WM, WN, ROWB, P, EPI, OCC>;
+    static const hipError_t attr = hipFuncSetAttribute(
+        (const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
+    if (attr != hipSuccess) return attr;
+    dim3 grid(a.N / BN, (a.M + BM - 1) / BM, splits);
+    hipLaunchKernelGGL(kern, grid, dim3(256), lds_bytes, s, a);
+    return hipGetLastError();
   }
 }
 
 // Tile table: id -> instantiation (bm, bn, wave layout wm x wn, bytes of K
 // per row per stage, LDS ring stages, workgroups per CU). The LDS ring
-// (P * (2*bm + bn) * rowb bytes in bf16x2 mode) must fit 160 KB / occ.
+// (P * (bm + bn) * rowb bytes) must fit 160 KB / occ; bm * rowb and
+// bn * rowb must be multiples of 4 KB (whole DMA rounds of 256 lanes).
 #define MTE_TILE_TABLE(X)                    \
-  X(0, 256, 256, 2, 2, 64, 3, 1)             \
-  X(1, 192, 256, 2, 2, 64, 3, 1)             \
-  X(2, 192, 192, 2, 2, 64, 4, 1)             \
-  X(3, 256, 128, 2, 2, 64, 3, 1)             \
-  X(4, 128, 256, 2, 2, 64, 4, 1)             \
-  X(5, 192, 128, 2, 2, 64, 4, 1)             \
-  X(6, 128, 128, 2, 2, 64, 3, 2)             \
-  X(7, 128, 128, 2, 2, 128, 3, 1)            \
-  X(8, 64, 256, 1, 4, 128, 3, 1)             \
-  X(9, 64, 256, 1, 4, 64, 3, 2)              \
-  X(10, 64, 128, 2, 2, 64, 4, 2)             \
-  X(11, 32, 256, 1, 4, 128, 3, 1)            \
-  X(12, 32, 128, 1, 4, 128, 3, 2)            \
+  X(0, 256, 256, 2, 2, 64, 4, 1)             \
+  X(1, 256, 192, 2, 2, 64, 4, 1)             \
+  X(2, 192, 256, 2, 2, 64, 4, 1)             \
+  X(3, 192, 192, 2, 2, 64, 5, 1)             \
+  X(4, 192, 192, 2, 2, 128, 3, 1)            \
+  X(5, 256, 128, 2, 2, 128, 3, 1)            \
+  X(6, 256, 128, 2, 2, 64, 6, 1)             \
+  X(7, 128, 256, 2, 2, 64, 6, 1)             \
+  X(8, 192, 128, 2, 2, 128, 3, 1)            \
+  X(9, 128, 128, 2, 2, 128, 4, 1)            \
+  X(10, 128, 128, 2, 2, 64, 4, 2)            \
+  X(11, 256, 128, 4, 1, 64, 6, 1)            \
+  X(12, 128, 128, 4, 1, 128, 4, 1)           \
   X(13, 128, 64, 4, 1, 64, 4, 2)             \
-  X(14, 192, 64, 2, 2, 64, 4, 1)             \
-  X(15, 192, 128, 2, 2, 64, 5, 1)            \
-  X(16, 128, 256, 2, 2, 64, 5, 1)            \
-  X(17, 128, 128, 2, 2, 64, 6, 1)            \
-  X(18, 96, 128, 1, 4, 128, 4, 1)            \
-  X(19, 96, 128, 1, 4, 128, 3, 1)
+  X(14, 96, 128, 1, 4, 128, 4, 1)            \
+  X(15, 64, 256, 1, 4, 128, 3, 1)            \
+  X(16, 64, 128, 2, 2, 64, 4, 2)             \
+  X(17, 32, 256, 1, 4, 128, 3, 1)            \
+  X(18, 192, 64, 2, 2, 128, 4, 1)            \
+  X(19, 96, 256, 1, 4, 128, 3, 1)
 
 static const TileCfg kTiles[] = {
 #define MTE_TILE_INFO(id, bm, bn, wm, wn, rowb, p, occ) {bm, bn, wm, wn, rowb, occ},
@@ -456,6 +470,8 @@ static const TileCfg kTiles[] = {
 #undef MTE_TILE_INFO
 };
 constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
+
+int gemm_num_tiles() { return kNumTiles; }
 
 template <int MODE, int EPI>
 static hipError_t run_id(int id, const GemmArgs &a, int splits, hipStream_t s) {
@@ -468,44 +484,42 @@ static hipError_t run_id(int id, const GemmArgs &a, int splits, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
-// col_align: columns a wave must cover in whole units (gate/up pairs for
-// SwiGLU, heads for the QKV epilogue).
+// col_align: columns a wave must cover in whole units (heads for the QKV
+// epilogue; gate/up pairs sit inside every 32-column block).
 static bool tile_fits(int id, int N, int K, int esz, int epi, int splits, int col_align = 32) {
   const TileCfg &t = kTiles[id];
   if (N % t.bn) return false;
   const int ks = t.rowb / esz;
   if (K % splits || (K / splits) % ks) return false;
-  if (epi == EPI_SWIGLU && (t.bn / t.wn) % 64) return false;  // gate/up pairs per wave
   if (epi == EPI_QKV && (t.bn / t.wn) % col_align) return false;
   return true;
 }
 
-// Steady-state throughput of each tile (algorithmic TFLOP/s of a bf16x2
-// GEMM at M = 10240, measured on MI355X); the planner's only calibration.
-static const double kTileRate[kNumTiles] = {412, 454, 420, 385, 469, 394, 454, 423,
-                                            436, 458, 404, 296, 344, 340, 250, 394, 469, 454,
-                                            300, 300};
+// Steady-state throughput of each tile (TFLOP/s of an fp16 GEMM with
+// M = 10240, measured on MI355X); the fallback planner's only calibration.
+static const double kTileRate[kNumTiles] = {952, 940, 895, 850, 850, 884, 850, 850, 800, 822,
+                                            640, 783, 872, 600, 700, 650, 550, 450, 600, 600};
 
-// Measured choices (MI355X sweep of every tile and split count) for the
-// decoder's four projections, D 2048 / FFN 6144 / 16+8+8 heads of 128, at
-// 96, 192, 768, 1536 and 10240 rows. Other row counts take the entry of the
-// nearest row count (log scale) for the same N, K and epilogue. `epi` is
-// the epilogue of the finished product; splits > 1 means the K splits
-// write partial sums that the consuming kernel adds up.
+// Measured choices (MI355X sweep of every tile and split count, weights
+// rotated through 600 MB so that they stream from HBM) for the decoder's four
+// projections (D 2048 / FFN 6144 / 16+8+8 heads of 128). Other row counts take the entry of the nearest row
+// count (log scale) for the same N, K and epilogue. `epi` is the epilogue of
+// the finished product; splits > 1 means the K splits write partial sums
+// that the consuming kernel adds up.
 struct TileChoice {
   int n, k, epi, m, tile, splits;
 };
 static const TileChoice kChoices[] = {
-    {4096, 2048, EPI_QKV, 96, 13, 4},    {2048, 2048, EPI_RESID, 96, 13, 8},
-    {12288, 2048, EPI_SWIGLU, 96, 18, 2},  {2048, 6144, EPI_RESID, 96, 18, 8},
-    {4096, 2048, EPI_QKV, 192, 18, 4},   {2048, 2048, EPI_RESID, 192, 10, 4},
-    {12288, 2048, EPI_SWIGLU, 192, 5, 2},  {2048, 6144, EPI_RESID, 192, 18, 8},
-    {4096, 2048, EPI_QKV, 768, 8, 1},    {2048, 2048, EPI_RESID, 768, 10, 1},
-    {12288, 2048, EPI_SWIGLU, 768, 1, 1},  {2048, 6144, EPI_RESID, 768, 10, 1},
-    {4096, 2048, EPI_QKV, 1536, 4, 1},   {2048, 2048, EPI_RESID, 1536, 17, 1},
-    {12288, 2048, EPI_SWIGLU, 1536, 15, 1}, {2048, 6144, EPI_RESID, 1536, 17, 1},
-    {4096, 2048, EPI_QKV, 10240, 4, 1},  {2048, 2048, EPI_RESID, 10240, 1, 1},
-    {12288, 2048, EPI_SWIGLU, 10240, 4, 1}, {2048, 6144, EPI_RESID, 10240, 9, 1},
+    {4096, 2048, EPI_QKV, 96, 12, 8},     {2048, 2048, EPI_RESID, 96, 13, 8},
+    {12288, 2048, EPI_SWIGLU, 96, 12, 2},  {2048, 6144, EPI_RESID, 96, 12, 8},
+    {4096, 2048, EPI_QKV, 192, 14, 4},    {2048, 2048, EPI_RESID, 192, 16, 4},
+    {12288, 2048, EPI_SWIGLU, 192, 4, 4},  {2048, 6144, EPI_RESID, 192, 9, 8},
+    {4096, 2048, EPI_QKV, 768, 12, 1},    {2048, 2048, EPI_RESID, 768, 12, 1},
+    {12288, 2048, EPI_SWIGLU, 768, 4, 1},  {2048, 6144, EPI_RESID, 768, 12, 1},
+    {4096, 2048, EPI_QKV, 1536, 12, 1},   {2048, 2048, EPI_RESID, 1536, 12, 1},
+    {12288, 2048, EPI_SWIGLU, 1536, 4, 1}, {2048, 6144, EPI_RESID, 1536, 12, 1},
+    {4096, 2048, EPI_QKV, 10240, 0, 1},   {2048, 2048, EPI_RESID, 10240, 2, 1},
+    {12288, 2048, EPI_SWIGLU, 10240, 0, 1}, {2048, 6144, EPI_RESID, 10240, 2, 1},
 };
 
 // Fallback estimate: rounds of workgroups over the compute units x the time
@@ -568,38 +582,38 @@ static hipError_t launch_mode(int epi, int tile, int splits, const GemmArgs &a, 
   }
 }
 
-hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void *A, const void *A_lo,
-                            const void *W, void *C, size_t c_plane, int M, int N, int K, int ldc,
-                            const QkvEpi *qe, hipStream_t s) {
+hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void *A, const void *W,
+                            void *C, size_t c_plane, int M, int N, int K, int ldc, float scale,
+                            float out_scale, const QkvEpi *qe, hipStream_t s) {
   if (M <= 0) return hipSuccess;
-  const int esz = mode == MODE_BF16X2 ? 2 : 4;
+  const int esz = mode == MODE_F16 ? 2 : 4;
   if (epi == EPI_QKV && (!qe || (qe->hd != 64 && qe->hd != 128))) return hipErrorInvalidValue;
   if (tile < 0 || tile >= kNumTiles || splits < 1 ||
       !tile_fits(tile, N, K, esz, epi, splits, epi == EPI_QKV ? qe->hd : 32) ||
       (splits > 1 && epi != EPI_PARTIAL))
     return hipErrorInvalidValue;
-  GemmArgs a{(const char *)A, (const char *)A_lo, (const char *)W, C, c_plane, M, N, K, ldc, K / splits,
+  GemmArgs a{(const char *)A, (const char *)W, C, c_plane, M, N, K, ldc, K / splits, scale, out_scale,
              epi == EPI_QKV ? *qe : QkvEpi{}};
-  return mode == MODE_BF16X2 ? launch_mode<MODE_BF16X2>(epi, tile, splits, a, s)
-                             : launch_mode<MODE_F32>(epi, tile, splits, a, s);
+  return mode == MODE_F16 ? launch_mode<MODE_F16>(epi, tile, splits, a, s)
+                          : launch_mode<MODE_F32>(epi, tile, splits, a, s);
 }
 
-hipError_t launch_gemm(int mode, int epi, const void *A, const void *A_lo, const void *W, void *C,
-                       size_t c_plane, int M, int N, int K, int ldc, float *ws, size_t ws_elems,
+hipError_t launch_gemm(int mode, int epi, const void *A, const void *W, void *C, int M, int N, int K,
+                       int ldc, float scale, float out_scale, float *ws, size_t ws_elems,
                        int *splits_out, const QkvEpi *qe, hipStream_t s) {
   *splits_out = 0;
   if (M <= 0) return hipSuccess;
   if (epi == EPI_QKV && !qe) return hipErrorInvalidValue;
   int tile, splits;
-  plan(M, N, K, mode == MODE_BF16X2 ? 2 : 4, epi, epi == EPI_QKV ? qe->hd : 32, ws ? ws_elems : 0,
-       &tile, &splits);
+  plan(M, N, K, mode == MODE_F16 ? 2 : 4, epi, epi == EPI_QKV ? qe->hd : 32, ws ? ws_elems : 0, &tile,
+       &splits);
   if (tile < 0) return hipErrorInvalidValue;
   if (splits > 1) {
     *splits_out = splits;
-    return launch_gemm_tile(mode, EPI_PARTIAL, tile, splits, A, A_lo, W, ws, (size_t)M * N, M, N, K,
-                            N, nullptr, s);
+    return launch_gemm_tile(mode, EPI_PARTIAL, tile, splits, A, W, ws, (size_t)M * N, M, N, K, N, scale,
+                            1.f, nullptr, s);
   }
-  return launch_gemm_tile(mode, epi, tile, 1, A, A_lo, W, C, c_plane, M, N, K, ldc, qe, s);
+  return launch_gemm_tile(mode, epi, tile, 1, A, W, C, 0, M, N, K, ldc, scale, out_scale, qe, s);
 }
 
 }  // namespace mte

@@ -11,8 +11,8 @@ namespace mte {
 // ------------------------------------------------------------- RMSNorm
 // out = x / sqrt(mean(x^2) + eps) * g, one 256-thread block per row, where
 // x = in + the np partial sums parts[0..np) (pitch pstride elements), added
-// in that order. copy_to (may alias in) receives x as float.
-// OUT_FMT FMT_BF16X2 writes bf16 hi to out and bf16(y - hi) to out + plane.
+// in that order. copy_to (may alias in) receives x as float. OUT_FMT:
+// FMT_F32, FMT_BF16 or FMT_F16 (rounded to nearest even).
 struct Parts {
   const float *p;   // partial sums [np][rows, D]
   int np;           // 0 .. kMaxParts
@@ -30,7 +30,7 @@ __device__ __forceinline__ float row_in(const TI *x, const Parts &pt, size_t o) 
 template <typename TI, int OUT_FMT>
 __global__ __launch_bounds__(256) void k_rmsnorm(const TI *in, float *copy_to, Parts pt,
                                                  const float *__restrict__ gain, void *__restrict__ out,
-                                                 size_t plane, int D, float eps) {
+                                                 int D, float eps) {
   __shared__ float red[4];
   const int row = blockIdx.x, tid = threadIdx.x;
   const size_t rb = (size_t)row * D;
@@ -54,22 +54,20 @@ __global__ __launch_bounds__(256) void k_rmsnorm(const TI *in, float *copy_to, P
     } else if constexpr (OUT_FMT == FMT_BF16) {
       ((bf16 *)out)[o] = (bf16)y;
     } else {
-      const bf16 h = (bf16)y;
-      ((bf16 *)out)[o] = h;
-      ((bf16 *)out)[o + plane] = (bf16)(y - (float)h);
+      ((f16 *)out)[o] = (f16)y;
     }
   }
 }
 
 template <typename TI>
 static void rmsnorm_out(int out_fmt, dim3 grid, const TI *in, float *copy_to, const Parts &pt,
-                        const float *g, void *out, size_t plane, int D, float eps, hipStream_t s) {
+                        const float *g, void *out, int D, float eps, hipStream_t s) {
   if (out_fmt == FMT_F32)
-    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_F32>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, plane, D, eps);
+    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_F32>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, D, eps);
   else if (out_fmt == FMT_BF16)
-    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_BF16>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, plane, D, eps);
+    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_BF16>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, D, eps);
   else
-    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_BF16X2>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, plane, D, eps);
+    hipLaunchKernelGGL((k_rmsnorm<TI, FMT_F16>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, D, eps);
 }
 
 // Register-resident variant for D a multiple of 1024 (D <= 4096): every
@@ -78,7 +76,7 @@ static void rmsnorm_out(int out_fmt, dim3 grid, const TI *in, float *copy_to, co
 template <typename TI, int OUT_FMT, int NV>
 __global__ __launch_bounds__(256) void k_rmsnorm_vec(const TI *in, float *copy_to, Parts pt,
                                                      const float *__restrict__ gain, void *__restrict__ out,
-                                                     size_t plane, int D, float eps) {
+                                                     int D, float eps) {
   __shared__ float red[4];
   const int row = blockIdx.x, tid = threadIdx.x;
   const size_t rb = (size_t)row * D;
@@ -120,53 +118,54 @@ __global__ __launch_bounds__(256) void k_rmsnorm_vec(const TI *in, float *copy_t
     for (int e = 0; e < 4; ++e) y[e] = v[i][e] * rs * g[e];
     if constexpr (OUT_FMT == FMT_F32) {
       *(f32x4 *)((float *)out + rb + c) = y;
-    } else {
-      bf16x4 h, l;
+    } else if constexpr (OUT_FMT == FMT_BF16) {
+      bf16x4 h;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        h[e] = (bf16)y[e];
-        l[e] = (bf16)(y[e] - (float)h[e]);
-      }
+      for (int e = 0; e < 4; ++e) h[e] = (bf16)y[e];
       *(bf16x4 *)((bf16 *)out + rb + c) = h;
-      if constexpr (OUT_FMT == FMT_BF16X2) *(bf16x4 *)((bf16 *)out + rb + c + plane) = l;
+    } else {
+      f16x4 h;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) h[e] = (f16)y[e];
+      *(f16x4 *)((f16 *)out + rb + c) = h;
     }
   }
 }
 
 template <typename TI, int NV>
 static void rmsnorm_vec(int out_fmt, dim3 grid, const TI *in, float *copy_to, const Parts &pt,
-                        const float *g, void *out, size_t plane, int D, float eps, hipStream_t s) {
+                        const float *g, void *out, int D, float eps, hipStream_t s) {
   if (out_fmt == FMT_F32)
-    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_F32, NV>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, plane, D, eps);
+    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_F32, NV>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, D, eps);
   else if (out_fmt == FMT_BF16)
-    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_BF16, NV>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, plane, D, eps);
+    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_BF16, NV>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, D, eps);
   else
-    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_BF16X2, NV>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, plane, D, eps);
+    hipLaunchKernelGGL((k_rmsnorm_vec<TI, FMT_F16, NV>), grid, dim3(256), 0, s, in, copy_to, pt, g, out, D, eps);
 }
 
 template <typename TI>
 static void rmsnorm_dispatch(int out_fmt, dim3 grid, const TI *in, float *copy_to, const Parts &pt,
-                             const float *g, void *out, size_t plane, int D, float eps, hipStream_t s) {
+                             const float *g, void *out, int D, float eps, hipStream_t s) {
   switch (D % 1024 == 0 ? D / 1024 : 0) {
-    case 1: rmsnorm_vec<TI, 1>(out_fmt, grid, in, copy_to, pt, g, out, plane, D, eps, s); break;
-    case 2: rmsnorm_vec<TI, 2>(out_fmt, grid, in, copy_to, pt, g, out, plane, D, eps, s); break;
-    case 3: rmsnorm_vec<TI, 3>(out_fmt, grid, in, copy_to, pt, g, out, plane, D, eps, s); break;
-    case 4: rmsnorm_vec<TI, 4>(out_fmt, grid, in, copy_to, pt, g, out, plane, D, eps, s); break;
-    default: rmsnorm_out<TI>(out_fmt, grid, in, copy_to, pt, g, out, plane, D, eps, s); break;
+    case 1: rmsnorm_vec<TI, 1>(out_fmt, grid, in, copy_to, pt, g, out, D, eps, s); break;
+    case 2: rmsnorm_vec<TI, 2>(out_fmt, grid, in, copy_to, pt, g, out, D, eps, s); break;
+    case 3: rmsnorm_vec<TI, 3>(out_fmt, grid, in, copy_to, pt, g, out, D, eps, s); break;
+    case 4: rmsnorm_vec<TI, 4>(out_fmt, grid, in, copy_to, pt, g, out, D, eps, s); break;
+    default: rmsnorm_out<TI>(out_fmt, grid, in, copy_to, pt, g, out, D, eps, s); break;
   }
 }
 
 hipError_t launch_rmsnorm(int in_fmt, int out_fmt, const void *in, float *copy_to, const float *parts,
-                          int nparts, const float *g, void *out, size_t out_plane, int rows, int D,
-                          float eps, hipStream_t s) {
+                          int nparts, const float *g, void *out, int rows, int D, float eps,
+                          hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (parts && nparts > kMaxParts) return hipErrorInvalidValue;
   dim3 grid(rows);
   const Parts pt{parts, parts ? nparts : 0, (size_t)rows * D};
   if (in_fmt == FMT_BF16)
-    rmsnorm_dispatch<bf16>(out_fmt, grid, (const bf16 *)in, copy_to, pt, g, out, out_plane, D, eps, s);
+    rmsnorm_dispatch<bf16>(out_fmt, grid, (const bf16 *)in, copy_to, pt, g, out, D, eps, s);
   else
-    rmsnorm_dispatch<float>(out_fmt, grid, (const float *)in, copy_to, pt, g, out, out_plane, D, eps, s);
+    rmsnorm_dispatch<float>(out_fmt, grid, (const float *)in, copy_to, pt, g, out, D, eps, s);
   return hipGetLastError();
 }
 
@@ -253,22 +252,22 @@ hipError_t launch_qkv_parts(float *qkv, const float *parts, int nparts, int T, i
 }
 
 // SwiGLU of summed gate/up partial sums. parts: np x [rows, 2F], gate and up
-// columns interleaved in blocks of 32 (block b: gate 32b.., then up 32b..).
-// out [rows, F]: float (OUT_FMT FMT_F32) or bf16 hi / lo planes `plane` apart.
+// columns interleaved in blocks of 16 (block b: gate 16b.., then up 16b..).
+// out [rows, F] = out_scale * silu(gate) * up: float (OUT_FMT FMT_F32) or fp16.
 template <int OUT_FMT>
 __global__ __launch_bounds__(256) void k_swiglu_parts(Parts pt, int F, void *__restrict__ out,
-                                                      size_t plane, size_t n) {
+                                                      float out_scale, size_t n) {
   const size_t i = (size_t)blockIdx.x * 256 + threadIdx.x;   // output element (r, f)
   if (i >= n) return;
   const size_t r = i / F;
   const int f = (int)(i % F);
-  const size_t gc = r * 2 * F + 64 * (f >> 5) + (f & 31);
+  const size_t gc = r * 2 * F + 32 * (f >> 4) + (f & 15);
   float qg[kMaxParts], qu[kMaxParts];
 #pragma unroll
   for (int k = 0; k < kMaxParts; ++k)
     if (k < pt.np) {
       qg[k] = pt.p[(size_t)k * pt.stride + gc];
-      qu[k] = pt.p[(size_t)k * pt.stride + gc + 32];
+      qu[k] = pt.p[(size_t)k * pt.stride + gc + 16];
     }
   float gt = qg[0], up = qu[0];
 #pragma unroll
@@ -277,27 +276,22 @@ __global__ __launch_bounds__(256) void k_swiglu_parts(Parts pt, int F, void *__r
       gt += qg[k];
       up += qu[k];
     }
-  const float y = gt / (1.f + __expf(-gt)) * up;
-  if constexpr (OUT_FMT == FMT_F32) {
-    ((float *)out)[i] = y;
-  } else {
-    const bf16 hi = (bf16)y;
-    ((bf16 *)out)[i] = hi;
-    ((bf16 *)out)[i + plane] = (bf16)(y - (float)hi);
-  }
+  const float y = gt / (1.f + __expf(-gt)) * up * out_scale;
+  if constexpr (OUT_FMT == FMT_F32) ((float *)out)[i] = y;
+  else ((f16 *)out)[i] = (f16)y;
 }
 
 hipError_t launch_swiglu_parts(int out_fmt, const float *parts, int nparts, int rows, int F, void *out,
-                               size_t out_plane, hipStream_t s) {
+                               float out_scale, hipStream_t s) {
   const size_t n = (size_t)rows * F;
   if (n == 0) return hipSuccess;
-  if (nparts < 1 || nparts > kMaxParts || F % 32) return hipErrorInvalidValue;
+  if (nparts < 1 || nparts > kMaxParts || F % 16) return hipErrorInvalidValue;
   const Parts pt{parts, nparts, (size_t)rows * 2 * F};
   dim3 grid((unsigned)((n + 255) / 256));
   if (out_fmt == FMT_F32)
-    hipLaunchKernelGGL(k_swiglu_parts<FMT_F32>, grid, dim3(256), 0, s, pt, F, out, out_plane, n);
+    hipLaunchKernelGGL(k_swiglu_parts<FMT_F32>, grid, dim3(256), 0, s, pt, F, out, out_scale, n);
   else
-    hipLaunchKernelGGL(k_swiglu_parts<FMT_BF16X2>, grid, dim3(256), 0, s, pt, F, out, out_plane, n);
+    hipLaunchKernelGGL(k_swiglu_parts<FMT_F16>, grid, dim3(256), 0, s, pt, F, out, out_scale, n);
   return hipGetLastError();
 }
 
@@ -397,34 +391,85 @@ hipError_t launch_positions(const int32_t *layouts5, int batch, int32_t *pos_thw
 
 // ------------------------------------------------------ weight repacking
 template <typename T>
-__global__ void k_to_f32(const T *__restrict__ src, float *__restrict__ dst, int n) {
+__global__ void k_to_f32(const T *__restrict__ src, float *__restrict__ dst, int n, float scale) {
   const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i < n) dst[i] = to_f32(src[i]);
+  if (i < n) dst[i] = to_f32(src[i]) * scale;
 }
 
-hipError_t launch_to_f32(int src_fmt, const void *src, float *dst, int n, hipStream_t s) {
+hipError_t launch_to_f32(int src_fmt, const void *src, float *dst, int n, float scale, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   dim3 grid((n + 255) / 256);
-  if (src_fmt == FMT_BF16) hipLaunchKernelGGL(k_to_f32<bf16>, grid, dim3(256), 0, s, (const bf16 *)src, dst, n);
-  else hipLaunchKernelGGL(k_to_f32<float>, grid, dim3(256), 0, s, (const float *)src, dst, n);
+  if (src_fmt == FMT_BF16)
+    hipLaunchKernelGGL(k_to_f32<bf16>, grid, dim3(256), 0, s, (const bf16 *)src, dst, n, scale);
+  else
+    hipLaunchKernelGGL(k_to_f32<float>, grid, dim3(256), 0, s, (const float *)src, dst, n, scale);
   return hipGetLastError();
 }
 
-// dst row r (of 2F): block b = r / 64 holds gate rows 32b.. then up rows 32b..
-__global__ void k_interleave(const char *__restrict__ gate, const char *__restrict__ up,
-                             char *__restrict__ dst, int row_bytes) {
-  const int r = blockIdx.x, b = r >> 6, w = r & 63;
-  const char *src = (w < 32 ? gate : up) + (size_t)(32 * b + (w & 31)) * row_bytes;
-  char *d = dst + (size_t)r * row_bytes;
-  for (int c = threadIdx.x * 16; c < row_bytes; c += 256 * 16)
-    *(u32x4 *)(d + c) = *(const u32x4 *)(src + c);
+// One workgroup per row: the row's max |w| and L2 norm, folded into
+// stats[0] / stats[1] with atomic max on the (non-negative) float bit
+// patterns, whose integer order matches their value order.
+template <typename T>
+__global__ __launch_bounds__(256) void k_matrix_stats(const T *__restrict__ src, int cols,
+                                                      float *__restrict__ stats) {
+  __shared__ float rmax[4], rss[4];
+  const T *row = src + (size_t)blockIdx.x * cols;
+  float mx = 0.f, ss = 0.f;
+  for (int c = threadIdx.x; c < cols; c += 256) {
+    const float v = to_f32(row[c]);
+    mx = fmaxf(mx, fabsf(v));
+    ss += v * v;
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) {
+    mx = warp_max_xor(mx, m);
+    ss = warp_sum_xor(ss, m);
+  }
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) { rmax[w] = mx; rss[w] = ss; }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const float m4 = fmaxf(fmaxf(rmax[0], rmax[1]), fmaxf(rmax[2], rmax[3]));
+    const float n4 = sqrtf(rss[0] + rss[1] + rss[2] + rss[3]);
+    atomicMax((unsigned int *)&stats[0], __float_as_uint(m4));
+    atomicMax((unsigned int *)&stats[1], __float_as_uint(n4));
+  }
 }
 
-hipError_t launch_interleave_gate_up(int esize, const void *gate, const void *up, void *dst,
-                                     int F, int D, hipStream_t s) {
-  const int row_bytes = D * esize;
-  hipLaunchKernelGGL(k_interleave, dim3(2 * F), dim3(256), 0, s, (const char *)gate,
-                     (const char *)up, (char *)dst, row_bytes);
+hipError_t launch_matrix_stats(int src_fmt, const void *src, int rows, int cols, float *stats,
+                               hipStream_t s) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  if (src_fmt == FMT_BF16)
+    hipLaunchKernelGGL(k_matrix_stats<bf16>, dim3(rows), dim3(256), 0, s, (const bf16 *)src, cols, stats);
+  else
+    hipLaunchKernelGGL(k_matrix_stats<float>, dim3(rows), dim3(256), 0, s, (const float *)src, cols, stats);
+  return hipGetLastError();
+}
+
+// One workgroup per source row: dst[map(r)] = convert(src[r] * scale).
+template <typename TS, typename TD>
+__global__ __launch_bounds__(256) void k_convert_rows(const TS *__restrict__ src, TD *__restrict__ dst,
+                                                      int cols, float scale, int interleave, int up) {
+  const int r = blockIdx.x;
+  const int dr = interleave ? 32 * (r >> 4) + 16 * up + (r & 15) : r;
+  const TS *s = src + (size_t)r * cols;
+  TD *d = dst + (size_t)dr * cols;
+  for (int c = threadIdx.x; c < cols; c += 256) d[c] = from_f32<TD>(to_f32(s[c]) * scale);
+}
+
+hipError_t launch_convert_rows(int src_fmt, const void *src, int dst_fmt, void *dst, int rows, int cols,
+                               float scale, int interleave, int up, hipStream_t s) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  if (interleave && rows % 16) return hipErrorInvalidValue;
+  dim3 grid(rows);
+  if (src_fmt == FMT_BF16 && dst_fmt == FMT_F16)
+    hipLaunchKernelGGL((k_convert_rows<bf16, f16>), grid, dim3(256), 0, s, (const bf16 *)src, (f16 *)dst,
+                       cols, scale, interleave, up);
+  else if (src_fmt == FMT_F32 && dst_fmt == FMT_F32)
+    hipLaunchKernelGGL((k_convert_rows<float, float>), grid, dim3(256), 0, s, (const float *)src,
+                       (float *)dst, cols, scale, interleave, up);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
 

@@ -126,9 +126,9 @@ def test_layer1_bf16_residual_after_layer(torch):
 
 
 def test_bf16_output_is_rounded_fp32_result(torch):
-    """With a bf16 output, each value is the fp32 result rounded to nearest bf16 (two runs
-    may differ in the last fp32 bits where split-K partial sums are added atomically, so
-    a value next to a rounding boundary may round either way)."""
+    """With a bf16 output, each value is the fp32 result rounded to nearest even bf16: both
+    encoders run the same kernels in the same order (K-split partial sums are added in
+    split order), so the comparison is bit-exact."""
     from paper_2606_05981_amd import binding as B
     wl = W.workload("layer1_b1")
     dims = wl.dims
@@ -139,15 +139,39 @@ def test_bf16_output_is_rounded_fp32_result(torch):
     y16 = _gpu_encode(torch, e16, dims, emb, wl.layouts, raw=True)
     e32.close(); e16.close()
     assert y16.dtype == torch.bfloat16
-    a, b = y16.float(), y32
-    half_ulp = torch.ldexp(torch.ones_like(b), torch.frexp(b)[1] - 9)
-    excess = (a - b).abs() - (half_ulp + 1e-5 * b.pow(2).mean().sqrt())
-    i = int(excess.argmax())
-    _say("  worst", a.reshape(-1)[i].item(), b.reshape(-1)[i].item(), half_ulp.reshape(-1)[i].item())
-    assert excess.max().item() <= 0
-    frac_equal = (y16 == y32.to(torch.bfloat16)).float().mean().item()
-    _say("  equal fraction", frac_equal)
-    assert frac_equal > 0.999
+    assert torch.equal(y16, y32.to(torch.bfloat16))
+
+
+def test_fp16_range_prescales(torch):
+    """Norm gains x4096 push RMSNorm outputs, v and the SwiGLU product far past fp16's
+    range (65504) and a down-projection x2^18 has weights beyond it: the power-of-two
+    pre-scales chosen at creation from the static bounds keep every fp16 operand finite,
+    and the layer still meets the per-layer tolerance."""
+    from paper_2606_05981_amd import binding as B
+    from paper_2606_05981_amd.encoder import TextEncoder, build_positions
+    wl = W.workload("layer1_b1")
+    dims = wl.dims
+    w = dict(layer_w(dims, 0))
+    w["attn_norm"] = w["attn_norm"] * np.float32(4096.0)
+    w["mlp_norm"] = w["mlp_norm"] * np.float32(4096.0)
+    w["w_down"] = w["w_down"] * np.float32(2.0 ** 18)
+    cfg = B.make_config(dims.n_layers, dims.hidden, dims.n_q_heads, dims.n_kv_heads, dims.head_dim,
+                        dims.ffn, rms_eps=dims.rms_eps, rope_theta=dims.rope_theta,
+                        mrope_section=dims.mrope_section, dtype=B.MTE_BF16, out_dtype=B.MTE_F32,
+                        max_tokens=256, max_batch=4, max_seq=256)
+    enc = TextEncoder.from_host(cfg, [w], final_g(dims))
+    emb = W.embeddings(dims, wl.layouts)
+    pos = O.positions(wl.layouts)
+    h = enc.encode_layers(torch.from_numpy(emb.astype(np.float32)).cuda(),
+                          build_positions(layout_tuples(wl.layouts)), W.seq_lens(wl.layouts), 0, 1)
+    torch.cuda.synchronize()
+    enc.close()
+    got = h.cpu().numpy()
+    assert np.isfinite(got).all()
+    ref = O.layer_forward(emb, pos, W.seq_lens(wl.layouts), w, dims)
+    err = rel_err(got, ref)
+    _say("  prescaled layer err", err)
+    assert err <= TOL_LAYER
 
 
 # --------------------------------------------------- 28-layer stacks
@@ -223,8 +247,12 @@ def test_stack_wide_range_inputs(torch, full_enc):
 
 # ------------------------------------------------- GPU-side invariants
 def test_packed_equals_alone_and_permutation(torch):
-    """Each row's result is independent of its neighbours in the packed batch (up to the
-    order in which split-K partial sums are added)."""
+    """No sequence sees another. Permuting the sequences of a packed batch keeps the launch
+    plan (it depends on the token count only) and every row's arithmetic, so the permuted
+    result is bit-identical. A sequence run alone has another token count, hence possibly
+    other tiles and K splits: its sums are added in another order and some fp16 roundings
+    of GEMM inputs flip, so it agrees within the per-layer tolerance, while leakage across
+    sequences would move results by a sizeable fraction of the RMS."""
     dims = W.DIMS_FULL.with_(n_layers=2)
     layouts = (W.FRAME_96, W.SeqLayout(0, 1, 10, 9, 41), W.SeqLayout(0, 1, 8, 8, 1))
     emb = W.embeddings(dims, layouts)
@@ -233,12 +261,14 @@ def test_packed_equals_alone_and_permutation(torch):
     sl = seq_slices(layouts)
     for i, s in enumerate(layouts):
         alone = _gpu_encode(torch, enc, dims, np.ascontiguousarray(emb[sl[i]]), [s])
-        assert rel_err(alone, full[sl[i]]) <= 1e-4
+        e = rel_err(alone, full[sl[i]])
+        _say(f"  alone vs packed, seq {i}: {e:.3e}")
+        assert e <= TOL_LAYER
     perm = [2, 0, 1]
     idx = np.concatenate([np.arange(sl[i].start, sl[i].stop) for i in perm])
     out = _gpu_encode(torch, enc, dims, np.ascontiguousarray(emb[idx]), [layouts[i] for i in perm])
     enc.close()
-    assert rel_err(out, full[idx]) <= 1e-4
+    np.testing.assert_array_equal(out, full[idx])
 
 
 def test_graph_capture_replays_match_eager(torch):
@@ -265,8 +295,7 @@ def test_graph_capture_replays_match_eager(torch):
         g.replay()
         torch.cuda.synchronize()
         assert bool(torch.isfinite(out).all()), r
-        d = (out.float() - eager.float()).abs().max() / eager.float().pow(2).mean().sqrt()
-        assert d.item() <= 1e-5, (r, d.item())
+        assert torch.equal(out, eager), r
         enc.encode(x, pos, lens)   # eager work between replays
         torch.cuda.synchronize()
     enc.close()
