@@ -221,8 +221,9 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
       hipMalloc(&e->attn, MT * Hq * d * es) != hipSuccess ||
       hipMalloc(&e->act, MT * F * es) != hipSuccess)
     return fail(MTE_E_OOM);
-  // K splits are planned for at most 256 rows and 8 splits.
-  e->ws_elems = 8 * std::min<size_t>(MT, 256) * std::max(std::max(nqkv, 2 * F), D);
+  // K splits are planned for at most 8 splits of up to 256 rows, or 2 of up to 2048.
+  e->ws_elems = std::max(8 * std::min<size_t>(MT, 256), 2 * std::min<size_t>(MT, 2048)) *
+                std::max(std::max(nqkv, 2 * F), D);
   if (hipMalloc((void **)&e->ws, e->ws_elems * sizeof(float)) != hipSuccess ||
       hipMalloc((void **)&e->rcos, MT * (d / 2) * sizeof(float)) != hipSuccess ||
       hipMalloc((void **)&e->rsin, MT * (d / 2) * sizeof(float)) != hipSuccess)

@@ -14,8 +14,10 @@
 //   epilogue multiplies the product by the inverse of both scales (`scale`,
 //   exact). One MFMA per fragment at the same dense rate as bf16.
 //
-// Each workgroup (4 waves) owns a BM x BN output tile; each wave a
-// (BM/WM) x (BN/WN) block of 32x32 MFMA tiles. K is walked in stages of 128
+// Each workgroup (4 or 8 waves, WM x WN) owns a BM x BN output tile; each
+// wave a (BM/WM) x (BN/WN) block of 32x32 MFMA tiles. Eight waves, or two
+// four-wave workgroups per CU, put two waves on every SIMD, so one wave's
+// LDS reads and waits overlap the other's MFMAs. K is walked in stages of 128
 // bytes per row, staged through LDS with double buffering (one barrier per
 // stage): the next stage's global loads are in flight while the current one
 // feeds the MFMAs.
@@ -194,18 +196,20 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const 
 // run. Raw s_barrier (no fence) keeps the compiler from forcing vmcnt(0) at
 // the barrier; the waits are explicit.
 template <int MODE, int BM, int BN, int WM, int WN, int ROWB, int P, int EPI, int OCC>
-__global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void k_gemm(GemmArgs g) {
+__global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_eu(OCC * WM * WN / 4, OCC * WM * WN / 4))) void k_gemm(GemmArgs g) {
   typedef typename std::conditional<MODE == MODE_F32, float, f16>::type T;
   constexpr int KS = ROWB / (int)sizeof(T);       // k elements per stage
   constexpr int CH = ROWB / 16;                   // 16-byte chunks per row per stage
   constexpr int WTM = BM / WM, WTN = BN / WN;     // wave tile
   constexpr int TM = WTM / 32, TN = WTN / 32;     // 32x32 MFMA tiles per wave
   constexpr int ACH = BM * CH, BCH = BN * CH;     // chunks per stage (A / W)
-  static_assert(ACH % 256 == 0 && BCH % 256 == 0, "whole DMA rounds");
-  constexpr int AR = ACH / 256, BR = BCH / 256;   // DMA instructions per thread per matrix
+  constexpr int NW = WM * WN;                     // waves per workgroup
+  constexpr int NT = 64 * NW;                     // threads per workgroup
+  static_assert(ACH % NT == 0 && BCH % NT == 0, "whole DMA rounds");
+  constexpr int AR = ACH / NT, BR = BCH / NT;     // DMA instructions per thread per matrix
   constexpr int LOADS = AR + BR;                  // per thread per stage
   constexpr int STAGE = (BM + BN) * CH;           // u32x4 slots per stage
-  static_assert(WM * WN == 4, "4 waves");
+  static_assert(NW == 4 || NW == 8, "4 or 8 waves");
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
   static_assert(LOADS * (P - 2) < 64 && P >= 3 && P <= 6, "vmcnt range, ring depth");
   typedef typename Frag<T>::type frag_t;
@@ -219,18 +223,18 @@ __global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, O
   const size_t kb0 = (size_t)blockIdx.z * g.k_chunk * sizeof(T);
   const int nk = g.k_chunk / KS;
 
-  // DMA sources: instruction c of this thread fills LDS slot q = (c*4 + wave)*64 + lane
+  // DMA sources: instruction c of this thread fills LDS slot q = (c*NW + wave)*64 + lane
   // of its matrix (row q / CH, swizzled slot q % CH, logical chunk slot ^ f(row)).
   const char *pa[AR];
   const char *pb[BR];
 #pragma unroll
   for (int c = 0; c < AR; ++c) {
-    const int q = (c * 4 + wave) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
+    const int q = (c * NW + wave) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
     pa[c] = g.A + (size_t)min(m0 + r, M - 1) * rowb + kb0 + ch * 16;
   }
 #pragma unroll
   for (int c = 0; c < BR; ++c) {
-    const int q = (c * 4 + wave) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
+    const int q = (c * NW + wave) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
     pb[c] = g.W + (size_t)(n0 + r) * rowb + kb0 + ch * 16;
   }
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
@@ -240,10 +244,10 @@ __global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, O
     const uint32_t st = lds0 + (uint32_t)(slot * STAGE) * 16u;
     const size_t ko = (size_t)ks * ROWB;
     if (x < AR) {
-      dma16(pa[x] + ko, st + (uint32_t)((x * 4 + uwave) * 64) * 16u);
+      dma16(pa[x] + ko, st + (uint32_t)((x * NW + uwave) * 64) * 16u);
     } else {
       const int c = x - AR;
-      dma16(pb[c] + ko, st + (uint32_t)(ACH + (c * 4 + uwave) * 64) * 16u);
+      dma16(pb[c] + ko, st + (uint32_t)(ACH + (c * NW + uwave) * 64) * 16u);
     }
   };
 
@@ -419,13 +423,15 @@ __global__ __launch_bounds__(256, OCC) __attribute__((amdgpu_waves_per_eu(OCC, O
 // decoder's projections, else from the number of workgroups a tile yields
 // and its measured steady-state rate.
 struct TileCfg {
-  int bm, bn, wm, wn, rowb, occ;
+  int bm, bn, wm, wn, rowb, occ, f32;
 };
 
-template <int MODE, int BM, int BN, int WM, int WN, int ROWB, int P, int EPI, int OCC>
+template <int MODE, int BM, int BN, int WM, int WN, int ROWB, int P, int EPI, int OCC, int F32>
 static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
   if constexpr (EPI == EPI_QKV && (BN / WN) % 64 != 0) {
     return hipErrorInvalidValue;  // the QK-norm epilogue needs whole heads per wave
+  } else if constexpr (MODE == MODE_F32 && !F32) {
+    return hipErrorInvalidValue;  // fp32 operands are built for a few tiles only
   } else {
     constexpr int lds_bytes = P * (BM + BN) * ROWB;
     auto kern = k_gemm<MODE, BM, BN, WM, WN, ROWB, P, EPI, OCC>;
@@ -433,39 +439,51 @@ static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
         (const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
     if (attr != hipSuccess) return attr;
     dim3 grid(a.N / BN, (a.M + BM - 1) / BM, splits);
-    hipLaunchKernelGGL(kern, grid, dim3(256), lds_bytes, s, a);
+    hipLaunchKernelGGL(kern, grid, dim3(64 * WM * WN), lds_bytes, s, a);
     return hipGetLastError();
   }
 }
 
 // Tile table: id -> instantiation (bm, bn, wave layout wm x wn, bytes of K
-// per row per stage, LDS ring stages, workgroups per CU). The LDS ring
-// (P * (bm + bn) * rowb bytes) must fit 160 KB / occ; bm * rowb and
-// bn * rowb must be multiples of 4 KB (whole DMA rounds of 256 lanes).
+// per row per stage, LDS ring stages, workgroups per CU, built for fp32
+// operands too). The LDS ring (P * (bm + bn) * rowb bytes) must fit
+// 160 KB / occ; bm * rowb / 16 and bn * rowb / 16 must be multiples of the
+// workgroup's thread count (whole DMA rounds).
 #define MTE_TILE_TABLE(X)                    \
-  X(0, 256, 256, 2, 2, 64, 4, 1)             \
-  X(1, 256, 192, 2, 2, 64, 4, 1)             \
-  X(2, 192, 256, 2, 2, 64, 4, 1)             \
-  X(3, 192, 192, 2, 2, 64, 5, 1)             \
-  X(4, 192, 192, 2, 2, 128, 3, 1)            \
-  X(5, 256, 128, 2, 2, 128, 3, 1)            \
-  X(6, 256, 128, 2, 2, 64, 6, 1)             \
-  X(7, 128, 256, 2, 2, 64, 6, 1)             \
-  X(8, 192, 128, 2, 2, 128, 3, 1)            \
-  X(9, 128, 128, 2, 2, 128, 4, 1)            \
-  X(10, 128, 128, 2, 2, 64, 4, 2)            \
-  X(11, 256, 128, 4, 1, 64, 6, 1)            \
-  X(12, 128, 128, 4, 1, 128, 4, 1)           \
-  X(13, 128, 64, 4, 1, 64, 4, 2)             \
-  X(14, 96, 128, 1, 4, 128, 4, 1)            \
-  X(15, 64, 256, 1, 4, 128, 3, 1)            \
-  X(16, 64, 128, 2, 2, 64, 4, 2)             \
-  X(17, 32, 256, 1, 4, 128, 3, 1)            \
-  X(18, 192, 64, 2, 2, 128, 4, 1)            \
-  X(19, 96, 256, 1, 4, 128, 3, 1)
+  X(0, 256, 256, 2, 2, 64, 4, 1, 0)          \
+  X(1, 256, 192, 2, 2, 64, 4, 1, 0)          \
+  X(2, 192, 256, 2, 2, 64, 4, 1, 0)          \
+  X(3, 192, 192, 2, 2, 64, 5, 1, 0)          \
+  X(4, 192, 192, 2, 2, 128, 3, 1, 0)         \
+  X(5, 256, 128, 2, 2, 128, 3, 1, 0)         \
+  X(6, 256, 128, 2, 2, 64, 6, 1, 0)          \
+  X(7, 128, 256, 2, 2, 64, 6, 1, 0)          \
+  X(8, 192, 128, 2, 2, 128, 3, 1, 0)         \
+  X(9, 128, 128, 2, 2, 128, 4, 1, 1)         \
+  X(10, 128, 128, 2, 2, 64, 4, 2, 0)         \
+  X(11, 256, 128, 4, 1, 64, 6, 1, 0)         \
+  X(12, 128, 128, 4, 1, 128, 4, 1, 1)        \
+  X(13, 128, 64, 4, 1, 64, 4, 2, 1)          \
+  X(14, 96, 128, 1, 4, 128, 4, 1, 0)         \
+  X(15, 64, 256, 1, 4, 128, 3, 1, 0)         \
+  X(16, 64, 128, 2, 2, 64, 4, 2, 1)          \
+  X(17, 32, 256, 1, 4, 128, 3, 1, 1)         \
+  X(18, 192, 64, 2, 2, 128, 4, 1, 0)         \
+  X(19, 96, 256, 1, 4, 128, 3, 1, 0)         \
+  X(20, 192, 192, 2, 2, 64, 3, 2, 0)         \
+  X(21, 256, 128, 2, 2, 64, 3, 2, 0)         \
+  X(22, 128, 256, 2, 2, 64, 3, 2, 0)         \
+  X(23, 128, 128, 4, 1, 64, 4, 2, 0)         \
+  X(24, 256, 128, 4, 1, 64, 3, 2, 0)         \
+  X(25, 192, 128, 2, 2, 64, 3, 2, 0)         \
+  X(26, 256, 256, 2, 4, 64, 4, 1, 0)         \
+  X(27, 256, 256, 4, 2, 64, 4, 1, 0)         \
+  X(28, 256, 128, 4, 2, 64, 6, 1, 0)         \
+  X(29, 128, 256, 2, 4, 64, 6, 1, 0)         \
+  X(30, 128, 128, 2, 4, 128, 4, 1, 0)
 
 static const TileCfg kTiles[] = {
-#define MTE_TILE_INFO(id, bm, bn, wm, wn, rowb, p, occ) {bm, bn, wm, wn, rowb, occ},
+#define MTE_TILE_INFO(id, bm, bn, wm, wn, rowb, p, occ, f32) {bm, bn, wm, wn, rowb, occ, f32},
     MTE_TILE_TABLE(MTE_TILE_INFO)
 #undef MTE_TILE_INFO
 };
@@ -476,8 +494,8 @@ int gemm_num_tiles() { return kNumTiles; }
 template <int MODE, int EPI>
 static hipError_t run_id(int id, const GemmArgs &a, int splits, hipStream_t s) {
   switch (id) {
-#define MTE_TILE_CASE(idv, bm, bn, wm, wn, rowb, p, occ) \
-  case idv: return run<MODE, bm, bn, wm, wn, rowb, p, EPI, occ>(a, splits, s);
+#define MTE_TILE_CASE(idv, bm, bn, wm, wn, rowb, p, occ, f32) \
+  case idv: return run<MODE, bm, bn, wm, wn, rowb, p, EPI, occ, f32>(a, splits, s);
     MTE_TILE_TABLE(MTE_TILE_CASE)
 #undef MTE_TILE_CASE
   }
@@ -488,7 +506,7 @@ static hipError_t run_id(int id, const GemmArgs &a, int splits, hipStream_t s) {
 // epilogue; gate/up pairs sit inside every 32-column block).
 static bool tile_fits(int id, int N, int K, int esz, int epi, int splits, int col_align = 32) {
   const TileCfg &t = kTiles[id];
-  if (N % t.bn) return false;
+  if (N % t.bn || (esz == 4 && !t.f32)) return false;
   const int ks = t.rowb / esz;
   if (K % splits || (K / splits) % ks) return false;
   if (epi == EPI_QKV && (t.bn / t.wn) % col_align) return false;
@@ -497,8 +515,10 @@ static bool tile_fits(int id, int N, int K, int esz, int epi, int splits, int co
 
 // Steady-state throughput of each tile (TFLOP/s of an fp16 GEMM with
 // M = 10240, measured on MI355X); the fallback planner's only calibration.
-static const double kTileRate[kNumTiles] = {952, 940, 895, 850, 850, 884, 850, 850, 800, 822,
-                                            640, 783, 872, 600, 700, 650, 550, 450, 600, 600};
+static const double kTileRate[kNumTiles] = {959, 944, 895, 850, 850, 884, 850, 850, 800, 819,
+                                            640, 777, 860, 600, 700, 650, 550, 450, 600, 600,
+                                            921, 850, 850, 714, 766, 800, 1026, 1018, 850, 728,
+                                            803};
 
 // Measured choices (MI355X sweep of every tile and split count, weights
 // rotated through 600 MB so that they stream from HBM) for the decoder's four
@@ -511,20 +531,21 @@ struct TileChoice {
 };
 static const TileChoice kChoices[] = {
     {4096, 2048, EPI_QKV, 96, 12, 8},     {2048, 2048, EPI_RESID, 96, 13, 8},
-    {12288, 2048, EPI_SWIGLU, 96, 12, 2},  {2048, 6144, EPI_RESID, 96, 12, 8},
+    {12288, 2048, EPI_SWIGLU, 96, 12, 2},  {2048, 6144, EPI_RESID, 96, 18, 8},
     {4096, 2048, EPI_QKV, 192, 14, 4},    {2048, 2048, EPI_RESID, 192, 16, 4},
-    {12288, 2048, EPI_SWIGLU, 192, 4, 4},  {2048, 6144, EPI_RESID, 192, 9, 8},
-    {4096, 2048, EPI_QKV, 768, 12, 1},    {2048, 2048, EPI_RESID, 768, 12, 1},
-    {12288, 2048, EPI_SWIGLU, 768, 4, 1},  {2048, 6144, EPI_RESID, 768, 12, 1},
-    {4096, 2048, EPI_QKV, 1536, 12, 1},   {2048, 2048, EPI_RESID, 1536, 12, 1},
-    {12288, 2048, EPI_SWIGLU, 1536, 4, 1}, {2048, 6144, EPI_RESID, 1536, 12, 1},
-    {4096, 2048, EPI_QKV, 10240, 0, 1},   {2048, 2048, EPI_RESID, 10240, 2, 1},
-    {12288, 2048, EPI_SWIGLU, 10240, 0, 1}, {2048, 6144, EPI_RESID, 10240, 2, 1},
+    {12288, 2048, EPI_SWIGLU, 192, 4, 4},  {2048, 6144, EPI_RESID, 192, 14, 8},
+    {4096, 2048, EPI_QKV, 768, 8, 2},     {2048, 2048, EPI_RESID, 768, 12, 2},
+    {12288, 2048, EPI_SWIGLU, 768, 3, 1},  {2048, 6144, EPI_RESID, 768, 14, 2},
+    {4096, 2048, EPI_QKV, 1536, 27, 2},   {2048, 2048, EPI_RESID, 1536, 8, 2},
+    {12288, 2048, EPI_SWIGLU, 1536, 20, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
+    {4096, 2048, EPI_QKV, 10240, 27, 1},  {2048, 2048, EPI_RESID, 10240, 2, 1},
+    {12288, 2048, EPI_SWIGLU, 10240, 26, 1}, {2048, 6144, EPI_RESID, 10240, 12, 1},
 };
 
 // Fallback estimate: rounds of workgroups over the compute units x the time
 // one full round takes at the tile's measured rate. Split-K is only
-// considered for small M, and only where the partial sums fit `ws_elems`.
+// considered up to 2048 rows (2 splits above 256), and only where the
+// partial sums fit `ws_elems`.
 static void plan_model(int M, int N, int K, int esz, int epi, int col_align, size_t ws_elems,
                        int *tile, int *splits) {
   const int cus = 256;
@@ -533,7 +554,7 @@ static void plan_model(int M, int N, int K, int esz, int epi, int col_align, siz
   *splits = 1;
   for (int id = 0; id < kNumTiles; ++id) {
     for (int sp = 1; sp <= 8; sp *= 2) {
-      if (sp > 1 && (M > 256 || (size_t)sp * M * N > ws_elems)) continue;
+      if (sp > 1 && (M > 2048 || (M > 256 && sp > 2) || (size_t)sp * M * N > ws_elems)) continue;
       if (!tile_fits(id, N, K, esz, sp > 1 ? EPI_PARTIAL : epi, sp, col_align)) continue;
       const TileCfg &t = kTiles[id];
       const double tiles = (double)(N / t.bn) * ((M + t.bm - 1) / t.bm) * sp;
@@ -563,7 +584,8 @@ static void plan(int M, int N, int K, int esz, int epi, int col_align, size_t ws
   }
   if (best &&
       tile_fits(best->tile, N, K, esz, best->splits > 1 ? EPI_PARTIAL : epi, best->splits, col_align) &&
-      (best->splits == 1 || (M <= 256 && (size_t)best->splits * M * N <= ws_elems))) {
+      (best->splits == 1 ||
+       ((M <= 256 || (M <= 2048 && best->splits == 2)) && (size_t)best->splits * M * N <= ws_elems))) {
     *tile = best->tile;
     *splits = best->splits;
     return;

@@ -48,7 +48,7 @@ struct QkvEpi {
 // power-of-two pre-scales; exact) before the epilogue; EPI_SWIGLU multiplies
 // its fp16 output by `out_scale` (a power of two keeping it in fp16 range).
 // ldc: C's row pitch in elements.
-// The planner may split K (small M only) when the partial sums fit the
+// The planner may split K (up to 2048 rows) when the partial sums fit the
 // workspace ws (ws_elems floats; ws may be null): the product is then NOT
 // finished -- *splits_out (> 1) scaled partial sums [M, N] (row pitch N,
 // M*N elements apart) are left in ws, in split order, for the consumer to
