@@ -76,7 +76,11 @@ __device__ __forceinline__ int vt_pos(int k) {
   return (2 * (i / EPF) + g) * EPF + (i % EPF);
 }
 
-template <int MODE, int HD>
+// NB: key/value tiles staged at once. NB = 1 keeps a ring of one tile with
+// the next one in flight in registers (any length); NB > 1 loads all of a
+// workgroup's tiles up front (sequences of at most NB * 32 tokens), so the
+// whole key/value range costs one global-load latency and one barrier.
+template <int MODE, int HD, int NB>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   typedef typename std::conditional<MODE == MODE_F32, float, bf16>::type T;
   constexpr int NP = (MODE == MODE_F16) ? 2 : 1;   // bf16 planes per operand
@@ -95,10 +99,12 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   constexpr int K_BYTES = NP * KV * NCH * 16;
   constexpr int V_BYTES = NP * HD * VTP * (int)sizeof(T);
   constexpr int O_BYTES = 4 * 32 * OTP * 4;
-  constexpr int SMEM = (K_BYTES + V_BYTES) > O_BYTES ? (K_BYTES + V_BYTES) : O_BYTES;
+  constexpr int ST_BYTES = K_BYTES + V_BYTES;             // one staged tile
+  constexpr int SMEM = NB * ST_BYTES > O_BYTES ? NB * ST_BYTES : O_BYTES;
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
-  u32x4 *sK = (u32x4 *)smem;                               // [NP][KV * NCH]
-  T *sVt = (T *)(smem + K_BYTES);                          // [NP][HD * VTP]
+  // tile b: K [NP][KV * NCH] at smem + b * ST_BYTES, V^T [NP][HD * VTP] after it
+  auto sK_of = [&](int b) { return (u32x4 *)(smem + b * ST_BYTES); };
+  auto sVt_of = [&](int b) { return (T *)(smem + b * ST_BYTES + K_BYTES); };
   float *sOall = (float *)smem;                            // [4][32 * OTP]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -168,15 +174,16 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   constexpr int KCH = KV * NCH / 256;             // K chunks per thread
   constexpr int VCH = HD * (KV / EC) / 256;       // V column groups per thread
   static_assert(KCH * 256 == KV * NCH && VCH * 256 == HD * (KV / EC), "staging split");
-  float kx[KCH][EC], vx[VCH][EC];
-  auto gload = [&](int kv0) {
+  float kx[NB][KCH][EC], vx[NB][VCH][EC];
+  // Global loads of the tile at kv0 into register slot b.
+  auto gload = [&](int b, int kv0) {
 #pragma unroll
     for (int t = 0; t < KCH; ++t) {
       const int idx = tid + t * 256, r = min(kv0 + idx / NCH, L - 1), c = idx % NCH;
 #pragma unroll
       for (int e = 0; e < EC; e += 4) {
         const f32x4 v = *(const f32x4 *)(a.qkv + base + (size_t)r * ld + k_off + c * EC + e);
-        kx[t][e] = v[0]; kx[t][e + 1] = v[1]; kx[t][e + 2] = v[2]; kx[t][e + 3] = v[3];
+        kx[b][t][e] = v[0]; kx[b][t][e + 1] = v[1]; kx[b][t][e + 2] = v[2]; kx[b][t][e + 3] = v[3];
       }
     }
 #pragma unroll
@@ -184,30 +191,31 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       const int idx = tid + t * 256, d = idx % HD, v = idx / HD;
 #pragma unroll
       for (int e = 0; e < EC; ++e)
-        vx[t][e] = a.qkv[base + (size_t)min(kv0 + v * EC + e, L - 1) * ld + v_off + d];
+        vx[b][t][e] = a.qkv[base + (size_t)min(kv0 + v * EC + e, L - 1) * ld + v_off + d];
     }
   };
-  auto lstore = [&]() {
+  // Register slot b -> LDS tile sKb / sVtb.
+  auto lstore = [&](int b, u32x4 *sKb, T *sVtb) {
 #pragma unroll
     for (int t = 0; t < KCH; ++t) {
       const int idx = tid + t * 256, r = idx / NCH, c = idx % NCH;
       T sp[NP][EC];
-      split_vals<T, NP, EC>(kx[t], sp);
+      split_vals<T, NP, EC>(kx[b][t], sp);
 #pragma unroll
       for (int p = 0; p < NP; ++p) {
         u32x4 w;
         __builtin_memcpy(&w, sp[p], 16);
-        sK[p * KV * NCH + r * NCH + kswz<NCH>(r, c)] = w;
+        sKb[p * KV * NCH + r * NCH + kswz<NCH>(r, c)] = w;
       }
     }
 #pragma unroll
     for (int t = 0; t < VCH; ++t) {
       const int idx = tid + t * 256, d = idx % HD, v = idx / HD;
       T vs[NP][EC];
-      split_vals<T, NP, EC>(vx[t], vs);
+      split_vals<T, NP, EC>(vx[b][t], vs);
 #pragma unroll
       for (int p = 0; p < NP; ++p) {
-        T *row = sVt + p * HD * VTP + d * VTP;
+        T *row = sVtb + p * HD * VTP + d * VTP;
         // keys v*EC .. v*EC+EC-1 land in runs of 4 consecutive positions
 #pragma unroll
         for (int e = 0; e < EC; e += 4) {
@@ -225,78 +233,106 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       }
     }
   };
-  if (n_blocks > 0) gload(0);
-  for (int kb = 0; kb < n_blocks; ++kb) {
-    const int kv0 = kb * KV;
-    lstore();
-    __syncthreads();
-    if (kb + 1 < n_blocks) gload(kv0 + KV);
-
-    if (qw < L && kv0 <= wave_last) {
-      f32x16 s;
+  // One key/value tile for this wave: scores, online softmax, O update.
+  auto compute = [&](int kv0, const u32x4 *sK, const T *sVt) {
+    if (!(qw < L && kv0 <= wave_last)) return;
+    // Independent accumulators (one per split product, or per k parity
+    // for fp32) so consecutive MFMAs do not wait on each other's results.
+    constexpr int NS = (NP == 2) ? 3 : 2;
+    f32x16 sacc[NS];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[r] = 0.f;
+    for (int u = 0; u < NS; ++u)
 #pragma unroll
-      for (int kk = 0; kk < NCH / 2; ++kk) {
-        const int slot = lrow * NCH + kswz<NCH>(lrow, kk * 2 + lgrp);
-        const frag_t k0 = __builtin_bit_cast(frag_t, sK[slot]);
-        mfma32(s, k0, qf[0][kk]);
-        if constexpr (NP == 2) {
-          const frag_t k1 = __builtin_bit_cast(frag_t, sK[KV * NCH + slot]);
-          mfma32(s, k1, qf[0][kk]);
-          mfma32(s, k0, qf[1][kk]);
-        }
+      for (int r = 0; r < 16; ++r) sacc[u][r] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < NCH / 2; ++kk) {
+      const int slot = lrow * NCH + kswz<NCH>(lrow, kk * 2 + lgrp);
+      const frag_t k0 = __builtin_bit_cast(frag_t, sK[slot]);
+      if constexpr (NP == 2) {
+        const frag_t k1 = __builtin_bit_cast(frag_t, sK[KV * NCH + slot]);
+        mfma32(sacc[0], k0, qf[0][kk]);
+        mfma32(sacc[1], k1, qf[0][kk]);
+        mfma32(sacc[2], k0, qf[1][kk]);
+      } else {
+        mfma32(sacc[kk & 1], k0, qf[0][kk]);
       }
-      float mb = -INFINITY;
+    }
+    f32x16 s = sacc[0] + sacc[1];
+    if constexpr (NS == 3) s += sacc[2];
+    float mb = -INFINITY;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int kv = kv0 + acc_row(r, lane);
-        s[r] = (kv <= my_q && kv < L) ? s[r] * sc : -INFINITY;
-        mb = fmaxf(mb, s[r]);
-      }
-      mb = warp_max_xor(mb, 32);
-      const float m_new = fmaxf(m_i, mb);
-      const float alpha = exp2f(m_i - m_new);
-      m_i = m_new;
-      float p[16];
-      float ps = 0.f;
+    for (int r = 0; r < 16; ++r) {
+      const int kv = kv0 + acc_row(r, lane);
+      s[r] = (kv <= my_q && kv < L) ? s[r] * sc : -INFINITY;
+      mb = fmaxf(mb, s[r]);
+    }
+    mb = warp_max_xor(mb, 32);
+    const float m_new = fmaxf(m_i, mb);
+    const float alpha = exp2f(m_i - m_new);
+    m_i = m_new;
+    float p[16];
+    float ps = 0.f;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        p[r] = exp2f(s[r] - m_new);
-        ps += p[r];
-      }
-      l_i = l_i * alpha + ps;
+    for (int r = 0; r < 16; ++r) {
+      p[r] = exp2f(s[r] - m_new);
+      ps += p[r];
+    }
+    l_i = l_i * alpha + ps;
+#pragma unroll
+    for (int n = 0; n < ND; ++n)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[n][r] *= alpha;
+    // P fragments: element e of fragment f is P value i = EPF*f + e.
+    frag_t pf[NP][NFP];
+#pragma unroll
+    for (int f = 0; f < NFP; ++f) {
+      T sp[NP][EPF];
+      split_vals<T, NP, EPF>(p + EPF * f, sp);
+#pragma unroll
+      for (int q = 0; q < NP; ++q)
+#pragma unroll
+        for (int e = 0; e < EPF; ++e) pf[q][f][e] = sp[q][e];
+    }
+    // Consecutive MFMAs go to the ND different output blocks.
+#pragma unroll
+    for (int f = 0; f < NFP; ++f) {
+      frag_t vf[ND][NP];
 #pragma unroll
       for (int n = 0; n < ND; ++n)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[n][r] *= alpha;
-      // P fragments: element e of fragment f is P value i = EPF*f + e.
-      frag_t pf[NP][NFP];
-#pragma unroll
-      for (int f = 0; f < NFP; ++f) {
-        T sp[NP][EPF];
-        split_vals<T, NP, EPF>(p + EPF * f, sp);
-#pragma unroll
         for (int q = 0; q < NP; ++q)
+          vf[n][q] = *(const frag_t *)(sVt + q * HD * VTP + (n * 32 + lrow) * VTP + (2 * f + lgrp) * EPF);
 #pragma unroll
-          for (int e = 0; e < EPF; ++e) pf[q][f][e] = sp[q][e];
-      }
+      for (int n = 0; n < ND; ++n) mfma32(oacc[n], vf[n][0], pf[0][f]);
+      if constexpr (NP == 2) {
 #pragma unroll
-      for (int n = 0; n < ND; ++n) {
+        for (int n = 0; n < ND; ++n) mfma32(oacc[n], vf[n][1], pf[0][f]);
 #pragma unroll
-        for (int f = 0; f < NFP; ++f) {
-          frag_t vf[NP];
-#pragma unroll
-          for (int q = 0; q < NP; ++q)
-            vf[q] = *(const frag_t *)(sVt + q * HD * VTP + (n * 32 + lrow) * VTP + (2 * f + lgrp) * EPF);
-          mfma32(oacc[n], vf[0], pf[0][f]);
-          if constexpr (NP == 2) {
-            mfma32(oacc[n], vf[1], pf[0][f]);
-            mfma32(oacc[n], vf[0], pf[1][f]);
-          }
-        }
+        for (int n = 0; n < ND; ++n) mfma32(oacc[n], vf[n][0], pf[1][f]);
       }
     }
+  };
+  if constexpr (NB == 1) {
+    if (n_blocks > 0) gload(0, 0);
+    for (int kb = 0; kb < n_blocks; ++kb) {
+      const int kv0 = kb * KV;
+      lstore(0, sK_of(0), sVt_of(0));
+      __syncthreads();
+      if (kb + 1 < n_blocks) gload(0, kv0 + KV);
+      compute(kv0, sK_of(0), sVt_of(0));
+      __syncthreads();
+    }
+  } else {
+    // n_blocks <= NB (the host launches this variant for short sequences only)
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+      if (b < n_blocks) gload(b, b * KV);
+    __builtin_amdgcn_sched_barrier(0);   // every tile's loads in flight before the first LDS write
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+      if (b < n_blocks) lstore(b, sK_of(b), sVt_of(b));
+    __syncthreads();
+    for (int kb = 0; kb < n_blocks; ++kb) compute(kb * KV, sK_of(kb), sVt_of(kb));
     __syncthreads();
   }
 
@@ -352,24 +388,30 @@ hipError_t launch_attention(int mode, const float *qkv, void *o, float out_scale
   for (int first = 0; first < batch; first += kMaxSeqPerLaunch) {
     const int n = batch - first < kMaxSeqPerLaunch ? batch - first : kMaxSeqPerLaunch;
     a.n_seq = n;
-    int tiles = 0;
+    int tiles = 0, max_len = 0;
     for (int i = 0; i < n; ++i) {
       a.cu[i] = cu[first + i];
       a.tile0[i] = tiles;
       const int L = cu[first + i + 1] - cu[first + i];
       tiles += (L + QT - 1) / QT;
+      max_len = L > max_len ? L : max_len;
     }
     a.cu[n] = cu[first + n];
     a.tile0[n] = tiles;
     if (tiles == 0) continue;
     dim3 grid(tiles, Hkv * a.head_blocks);
+    // Sequences of at most 128 tokens: every workgroup stages all of its
+    // (at most 4) key/value tiles at once.
+    const bool all = max_len <= 4 * 32;
+#define MTE_ATTN(M_, D_)                                                             \
+    if (all) hipLaunchKernelGGL((k_attn<M_, D_, 4>), grid, dim3(256), 0, s, a);      \
+    else hipLaunchKernelGGL((k_attn<M_, D_, 1>), grid, dim3(256), 0, s, a);
     if (mode == MODE_F16) {
-      if (d == 128) hipLaunchKernelGGL((k_attn<MODE_F16, 128>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((k_attn<MODE_F16, 64>), grid, dim3(256), 0, s, a);
+      if (d == 128) { MTE_ATTN(MODE_F16, 128) } else { MTE_ATTN(MODE_F16, 64) }
     } else {
-      if (d == 128) hipLaunchKernelGGL((k_attn<MODE_F32, 128>), grid, dim3(256), 0, s, a);
-      else hipLaunchKernelGGL((k_attn<MODE_F32, 64>), grid, dim3(256), 0, s, a);
+      if (d == 128) { MTE_ATTN(MODE_F32, 128) } else { MTE_ATTN(MODE_F32, 64) }
     }
+#undef MTE_ATTN
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -522,7 +522,10 @@ static const double kTileRate[kNumTiles] = {959, 944, 895, 850, 850, 884, 850, 8
 
 // Measured choices (MI355X sweep of every tile and split count, weights
 // rotated through 600 MB so that they stream from HBM) for the decoder's four
-// projections (D 2048 / FFN 6144 / 16+8+8 heads of 128). Other row counts take the entry of the nearest row
+// projections (D 2048 / FFN 6144 / 16+8+8 heads of 128). A K split is only
+// kept where it still wins after the consumer's extra pass over the fp32
+// partial sums (at 1536 rows two QKV partials cost 16 us to add up, more than
+// the split saves). Other row counts take the entry of the nearest row
 // count (log scale) for the same N, K and epilogue. `epi` is the epilogue of
 // the finished product; splits > 1 means the K splits write partial sums
 // that the consuming kernel adds up.
@@ -534,10 +537,10 @@ static const TileChoice kChoices[] = {
     {12288, 2048, EPI_SWIGLU, 96, 12, 2},  {2048, 6144, EPI_RESID, 96, 18, 8},
     {4096, 2048, EPI_QKV, 192, 14, 4},    {2048, 2048, EPI_RESID, 192, 16, 4},
     {12288, 2048, EPI_SWIGLU, 192, 4, 4},  {2048, 6144, EPI_RESID, 192, 14, 8},
-    {4096, 2048, EPI_QKV, 768, 8, 2},     {2048, 2048, EPI_RESID, 768, 12, 2},
+    {4096, 2048, EPI_QKV, 768, 12, 1},    {2048, 2048, EPI_RESID, 768, 12, 2},
     {12288, 2048, EPI_SWIGLU, 768, 3, 1},  {2048, 6144, EPI_RESID, 768, 14, 2},
-    {4096, 2048, EPI_QKV, 1536, 27, 2},   {2048, 2048, EPI_RESID, 1536, 8, 2},
-    {12288, 2048, EPI_SWIGLU, 1536, 20, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
+    {4096, 2048, EPI_QKV, 1536, 23, 1},   {2048, 2048, EPI_RESID, 1536, 12, 1},
+    {12288, 2048, EPI_SWIGLU, 1536, 20, 1}, {2048, 6144, EPI_RESID, 1536, 12, 1},
     {4096, 2048, EPI_QKV, 10240, 27, 1},  {2048, 2048, EPI_RESID, 10240, 2, 1},
     {12288, 2048, EPI_SWIGLU, 10240, 26, 1}, {2048, 6144, EPI_RESID, 10240, 12, 1},
 };
