@@ -174,6 +174,92 @@ def cpu_baseline(min_seconds=10.0):
                       f"forward ({toks} tokens in {dt:.1f} s, fp64 numpy oracle)"}
 
 
+def run_overlap(torch, name, steps, warmup):
+    """Side-stream overlap (the paper's pipelining, Alg. 1: the text encoder on a side stream
+    beside the main-stream denoiser): the captured encoder step replays on a side stream while
+    the main stream runs a dense fp16 GEMM load standing in for the U-Net, joined by events.
+    Returns solo and concurrent wall times and the overlap efficiency
+    (solo_te + solo_load - concurrent) / min(solo_te, solo_load)."""
+    from paper_2606_05981_amd import binding as B
+    from paper_2606_05981_amd.encoder import TextEncoder
+    from synth import workloads as W
+
+    wl = W.workload(name)
+    dims = wl.dims
+    lens = W.seq_lens(wl.layouts)
+    T = sum(lens)
+    cfg = B.make_config(dims.n_layers, dims.hidden, dims.n_q_heads, dims.n_kv_heads,
+                        dims.head_dim, dims.ffn, rms_eps=dims.rms_eps, rope_theta=dims.rope_theta,
+                        mrope_section=dims.mrope_section, mrope_layout=dims.mrope_layout,
+                        qk_norm=dims.qk_norm, dtype=B.MTE_BF16, out_dtype=B.MTE_F32, max_tokens=T,
+                        max_batch=len(lens), max_seq=max(lens))
+    enc = TextEncoder.from_host(cfg, (W.layer_weights(dims, l) for l in range(dims.n_layers)),
+                                W.final_norm_gain(dims))
+    emb = torch.from_numpy(W.embeddings(dims, wl.layouts)).to("cuda", torch.bfloat16)
+    layouts = [(s.n_text_before, s.grid_t, s.grid_h, s.grid_w, s.n_text_after) for s in wl.layouts]
+    out = torch.empty((T, dims.hidden), dtype=torch.float32, device="cuda")
+    pos = torch.empty((3, T), dtype=torch.int32, device="cuda")
+    main = torch.cuda.current_stream()
+    side = torch.cuda.Stream()
+
+    def enc_step(st):
+        B.mte_build_positions(layouts, pos.data_ptr(), st.cuda_stream)
+        B.mte_encode(enc.handle, emb.data_ptr(), pos.data_ptr(), lens, len(lens), out.data_ptr(),
+                     st.cuda_stream)
+
+    side.wait_stream(main)
+    with torch.cuda.stream(side):
+        for _ in range(warmup):
+            enc_step(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=side):
+            enc_step(side)
+    main.wait_stream(side)
+    torch.cuda.synchronize()
+    a = torch.randn(4096, 4096, device="cuda", dtype=torch.float16)
+    b = torch.randn(4096, 4096, device="cuda", dtype=torch.float16)
+    c = torch.empty_like(a)
+
+    def timed(fn):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        fn()
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
+
+    def te_only():
+        with torch.cuda.stream(side):
+            for _ in range(steps):
+                graph.replay()
+
+    for _ in range(warmup):
+        torch.mm(a, b, out=c)
+    te_s = timed(te_only)
+    t_mm = timed(lambda: [torch.mm(a, b, out=c) for _ in range(20)]) / 20
+    n_mm = max(1, int(round(te_s / t_mm)))     # a main-stream load as long as the encoder work
+
+    def load_only():
+        for _ in range(n_mm):
+            torch.mm(a, b, out=c)
+
+    load_s = timed(load_only)
+
+    def both():
+        side.wait_stream(main)
+        te_only()
+        load_only()
+        main.wait_stream(side)
+
+    both_s = timed(both)
+    enc.close()
+    eff = (te_s + load_s - both_s) / min(te_s, load_s)
+    return {"workload": f"{name}: encoder graph x{steps} on a side stream", "main_load":
+            f"{n_mm} x fp16 GEMM 4096^3 on the main stream",
+            "te_ms": round(te_s * 1e3, 3), "load_ms": round(load_s * 1e3, 3),
+            "concurrent_ms": round(both_s * 1e3, 3), "overlap_efficiency": round(eff, 3),
+            "te_ms_per_step_alone": round(te_s * 1e3 / steps, 4)}
+
+
 def copy_calibration(torch, mib=512, reps=5):
     """A plain device-to-device copy of `mib` MiB, `reps` times: the known-size kernel
     that calibrates the FETCH_SIZE / WRITE_SIZE counters (each dispatch moves exactly
@@ -197,6 +283,8 @@ def main():
     ap.add_argument("--no-batch1", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the known-size copy used to calibrate HBM byte counters")
+    ap.add_argument("--overlap", action="store_true",
+                    help="also measure the encoder on a side stream beside a main-stream GEMM load")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); frames are independent, "
@@ -266,6 +354,10 @@ def main():
                                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                           "frac": round(wbytes / t1 / 1e9 / PEAK_HBM_GBS, 4),
                                           "bytes_per_step": wbytes}}
+    if args.overlap:
+        res["side_stream_overlap"] = {
+            "batch16": run_overlap(torch, args.workload, K, args.warmup),
+            "batch1": run_overlap(torch, "stack_b1", K, args.warmup)}
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline()
     print(json.dumps(res), flush=True)

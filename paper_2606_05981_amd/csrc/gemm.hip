@@ -540,7 +540,7 @@ static const TileChoice kChoices[] = {
     {4096, 2048, EPI_QKV, 768, 12, 1},    {2048, 2048, EPI_RESID, 768, 12, 2},
     {12288, 2048, EPI_SWIGLU, 768, 3, 1},  {2048, 6144, EPI_RESID, 768, 14, 2},
     {4096, 2048, EPI_QKV, 1536, 23, 1},   {2048, 2048, EPI_RESID, 1536, 12, 1},
-    {12288, 2048, EPI_SWIGLU, 1536, 20, 1}, {2048, 6144, EPI_RESID, 1536, 12, 1},
+    {12288, 2048, EPI_SWIGLU, 1536, 20, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
     {4096, 2048, EPI_QKV, 10240, 27, 1},  {2048, 2048, EPI_RESID, 10240, 2, 1},
     {12288, 2048, EPI_SWIGLU, 10240, 26, 1}, {2048, 6144, EPI_RESID, 10240, 12, 1},
 };
