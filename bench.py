@@ -260,6 +260,79 @@ def run_overlap(torch, name, steps, warmup):
             "te_ms_per_step_alone": round(te_s * 1e3 / steps, 4)}
 
 
+def run_prefix(torch, prefix, steps, warmup, frames=16):
+    """Shared prefix (the paper's system prompt, Sec. V): `frames` frames whose sequences all
+    start with the same `prefix` text tokens, then an 8x8 image grid and 32 instruction tokens.
+    Times the whole sequences through mte_encode against mte_encode_prefixed (the prefix once,
+    then each frame's own 96 tokens attending to its cached keys / values); both captured as
+    HIP graphs and replayed."""
+    import numpy as np
+    from oracle import te_oracle as O   # positions of the full sequences (input preparation)
+    from paper_2606_05981_amd import binding as B
+    from paper_2606_05981_amd.encoder import TextEncoder
+    from synth import workloads as W
+
+    dims = W.DIMS_FULL
+    full = tuple(W.SeqLayout(prefix, 1, 8, 8, 32) for _ in range(frames))
+    L = full[0].length
+    T = L * frames
+    cfg = B.make_config(dims.n_layers, dims.hidden, dims.n_q_heads, dims.n_kv_heads,
+                        dims.head_dim, dims.ffn, rms_eps=dims.rms_eps, rope_theta=dims.rope_theta,
+                        mrope_section=dims.mrope_section, mrope_layout=dims.mrope_layout,
+                        qk_norm=dims.qk_norm, dtype=B.MTE_BF16, out_dtype=B.MTE_F32, max_tokens=T,
+                        max_batch=frames, max_seq=L)
+    enc = TextEncoder.from_host(cfg, (W.layer_weights(dims, l) for l in range(dims.n_layers)),
+                                W.final_norm_gain(dims))
+    enc.reserve_prefix(prefix)
+    emb_np = W.embeddings(dims, full)
+    pos_np = O.positions(full).astype(np.int32)
+    own = np.concatenate([np.arange(f * L + prefix, (f + 1) * L) for f in range(frames)])
+    dev = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to("cuda", dt)
+    emb, pos = dev(emb_np, torch.bfloat16), dev(pos_np, torch.int32)
+    p_emb, p_pos = dev(emb_np[:prefix], torch.bfloat16), dev(pos_np[:, :prefix], torch.int32)
+    o_emb, o_pos = dev(emb_np[own], torch.bfloat16), dev(pos_np[:, own], torch.int32)
+    out = torch.empty((T, dims.hidden), dtype=torch.float32, device="cuda")
+    out_p = torch.empty((prefix, dims.hidden), dtype=torch.float32, device="cuda")
+    out_o = torch.empty((len(own), dims.hidden), dtype=torch.float32, device="cuda")
+    side = torch.cuda.Stream()
+
+    def full_step(st):
+        B.mte_encode(enc.handle, emb.data_ptr(), pos.data_ptr(), [L] * frames, frames,
+                     out.data_ptr(), st.cuda_stream)
+
+    def prefixed_step(st):
+        B.mte_encode_prefixed(enc.handle, p_emb.data_ptr(), p_pos.data_ptr(), prefix,
+                              o_emb.data_ptr(), o_pos.data_ptr(), [L - prefix] * frames, frames,
+                              out_p.data_ptr(), out_o.data_ptr(), st.cuda_stream)
+
+    res = {}
+    for name, fn in (("full_sequences", full_step), ("prefix_once", prefixed_step)):
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            for _ in range(warmup):
+                fn(side)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=side):
+                fn(side)
+        torch.cuda.current_stream().wait_stream(side)
+        for _ in range(warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            g.replay()
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / steps
+        res[name] = {"ms_per_step": round(dt * 1e3, 4), "frames_per_s": round(frames / dt, 1)}
+    dev_err = float((out[torch.from_numpy(own).cuda()] - out_o).abs().max() / out.pow(2).mean().sqrt())
+    enc.close()
+    res.update({"workload": f"{frames} frames x ({prefix} shared prefix + 8x8 image + 32 instruction) "
+                            "tokens, 28 layers",
+                "speedup": round(res["full_sequences"]["ms_per_step"] / res["prefix_once"]["ms_per_step"], 3),
+                "max_abs_diff_vs_full_over_rms": dev_err})
+    return res
+
+
 def copy_calibration(torch, mib=512, reps=5):
     """A plain device-to-device copy of `mib` MiB, `reps` times: the known-size kernel
     that calibrates the FETCH_SIZE / WRITE_SIZE counters (each dispatch moves exactly
@@ -283,6 +356,8 @@ def main():
     ap.add_argument("--no-batch1", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the known-size copy used to calibrate HBM byte counters")
+    ap.add_argument("--prefix", type=int, default=0,
+                    help="also measure frames sharing a prefix of this many text tokens")
     ap.add_argument("--overlap", action="store_true",
                     help="also measure the encoder on a side stream beside a main-stream GEMM load")
     args = ap.parse_args()
@@ -358,6 +433,8 @@ def main():
         res["side_stream_overlap"] = {
             "batch16": run_overlap(torch, args.workload, K, args.warmup),
             "batch1": run_overlap(torch, "stack_b1", K, args.warmup)}
+    if args.prefix > 0:
+        res["shared_prefix"] = run_prefix(torch, args.prefix, K, args.warmup)
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline()
     print(json.dumps(res), flush=True)

@@ -167,6 +167,43 @@ int mte_encode_layers(mte_encoder *enc, const float *h_in, const int32_t *pos_th
 int mte_build_positions(const mte_seq_layout *layouts, int32_t batch,
                         int32_t *pos_thw, hipStream_t stream);
 
+/* Shared prefix (the paper's system prompt / chat template, identical for
+ * every frame, Sec. V). Under causal attention a prefix's hidden states, keys
+ * and values do not depend on what follows it, so they are computed once per
+ * batch instead of once per sequence.
+ *
+ * mte_encoder_reserve_prefix allocates the per-layer key/value cache for
+ * prefixes of up to max_prefix tokens (n_layers * max_prefix *
+ * (Hq + 2 Hkv) * d floats; replaces an earlier reservation). It may
+ * synchronise the device and allocate; call it next to mte_encoder_create.
+ * Errors: MTE_E_INVALID (null, max_prefix <= 0 or beyond max_tokens /
+ * max_seq), MTE_E_UNSUPPORTED (no layers), MTE_E_OOM. */
+int mte_encoder_reserve_prefix(mte_encoder *enc, int32_t max_prefix);
+
+/* Batched encode of sequences that all start with the same prefix_len-token
+ * prefix. The result equals mte_encode of the full sequences
+ * [prefix ++ own tokens of sequence b]: out_prefix receives the prefix's
+ * rows (identical for every sequence, written once) and out_hidden the
+ * sequences' own rows, packed as in mte_encode.
+ *  prefix_embeds: device [prefix_len, D], config.dtype.
+ *  prefix_pos:    device int32 [3, prefix_len], the prefix's (t,h,w) positions.
+ *  embeds:        device [T, D], the sequences' own tokens, T = sum(seq_lens).
+ *  pos_thw:       device int32 [3, T], their positions within the full
+ *                 sequences (i.e. continuing after the prefix).
+ *  seq_lens:      HOST int32[batch], own-token counts (without the prefix).
+ *  out_prefix:    device [prefix_len, D], config.out_dtype.
+ *  out_hidden:    device [T, D], config.out_dtype.
+ * Only enqueues work on `stream`, like mte_encode; needs a prior
+ * mte_encoder_reserve_prefix. Output buffers must not overlap the inputs or
+ * each other. Errors: MTE_E_INVALID (null, no reservation, prefix_len <= 0,
+ * overlap, bad seq_lens), MTE_E_CAPACITY (prefix_len > the reservation,
+ * prefix_len + a sequence > max_seq, batch / tokens beyond capacity),
+ * MTE_E_HIP. */
+int mte_encode_prefixed(mte_encoder *enc, const void *prefix_embeds, const int32_t *prefix_pos,
+                        int32_t prefix_len, const void *embeds, const int32_t *pos_thw,
+                        const int32_t *seq_lens, int32_t batch, void *out_prefix, void *out_hidden,
+                        hipStream_t stream);
+
 /* Frees the encoder (synchronises the device first). NULL is a no-op. */
 void mte_encoder_destroy(mte_encoder *enc);
 

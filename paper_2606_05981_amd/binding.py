@@ -66,6 +66,9 @@ _sig = {
     "mte_encode_layers": (C.c_int, [_P, _P, _P, C.POINTER(C.c_int32), C.c_int32, C.c_int32,
                                     C.c_int32, _P, _P]),
     "mte_build_positions": (C.c_int, [C.POINTER(mte_seq_layout), C.c_int32, _P, _P]),
+    "mte_encoder_reserve_prefix": (C.c_int, [_P, C.c_int32]),
+    "mte_encode_prefixed": (C.c_int, [_P, _P, _P, C.c_int32, _P, _P, C.POINTER(C.c_int32), C.c_int32, _P,
+                                      _P, _P]),
     "mte_encoder_destroy": (None, [_P]),
     "mte_status_string": (C.c_char_p, [C.c_int]),
     "mte_timing_enable": (C.c_int, [_P, C.c_int32, C.c_int32]),
@@ -148,6 +151,18 @@ def mte_build_positions(layouts: Sequence[Sequence[int]], pos_thw: int, stream: 
     for i, s in enumerate(layouts):
         arr[i] = mte_seq_layout(*[int(v) for v in s])
     return _check(lib.mte_build_positions(arr, len(layouts), pos_thw, stream), "mte_build_positions")
+
+
+def mte_encoder_reserve_prefix(enc: int, max_prefix: int) -> int:
+    return _check(lib.mte_encoder_reserve_prefix(enc, max_prefix), "mte_encoder_reserve_prefix")
+
+
+def mte_encode_prefixed(enc: int, prefix_embeds: int, prefix_pos: int, prefix_len: int, embeds: int,
+                        pos_thw: int, seq_lens: Sequence[int], batch: int, out_prefix: int,
+                        out_hidden: int, stream: int) -> int:
+    return _check(lib.mte_encode_prefixed(enc, prefix_embeds, prefix_pos, prefix_len, embeds, pos_thw,
+                                          _i32(seq_lens), batch, out_prefix, out_hidden, stream),
+                  "mte_encode_prefixed")
 
 
 def mte_encoder_destroy(enc: int) -> None:

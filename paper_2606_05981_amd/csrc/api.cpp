@@ -70,6 +70,10 @@ struct mte_encoder {
   float *ws = nullptr;
   size_t ws_elems = 0;
   float *rcos = nullptr, *rsin = nullptr;   // [max_tokens, d/2] rotary table of the current batch
+  // Shared-prefix cache: per layer the prefix's packed q/k/v rows
+  // [max_prefix, (Hq + 2 Hkv) d] (k and v are what later sequences read).
+  float *pkv = nullptr;
+  int max_prefix = 0;
   RopeParams rope;
   // kernel timing
   int timing_class = -1;
@@ -179,6 +183,7 @@ void mte_encoder_destroy(mte_encoder *e) {
   hipFree(e->ws);
   hipFree(e->rcos);
   hipFree(e->rsin);
+  hipFree(e->pkv);
   hipSetDevice(cur);
   delete e;
 }
@@ -368,9 +373,20 @@ struct Timer {
   }
 };
 
+// Shared-prefix mode of run_layers: `record` copies every layer's packed
+// q/k/v rows (the prefix itself being encoded) into the cache; otherwise
+// attention reads the cache's first P rows as keys / values before each
+// sequence's own.
+struct PrefixCtx {
+  float *cache;      // [n_layers][max_prefix][(Hq + 2 Hkv) d]
+  int P;
+  bool record;
+};
+
 // Runs layers [l0, l1) on the fp32 residual stream `h` (T rows).
 hipError_t run_layers(mte_encoder *e, float *h, const std::vector<int32_t> &cu, int batch, int T, int l0,
-                      int l1, bool first_norm_done, int *pending, hipStream_t s) {
+                      int l1, bool first_norm_done, int *pending, hipStream_t s,
+                      const PrefixCtx *pre = nullptr) {
   const mte_config &c = e->cfg;
   const int D = c.hidden, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
   const int nqkv = (Hq + 2 * Hkv) * d;
@@ -398,7 +414,13 @@ hipError_t run_layers(mte_encoder *e, float *h, const std::vector<int32_t> &cu, 
     if (sp) MTE_TRY(launch_qkv_parts(e->qkv, ws, sp, T, Hq, Hkv, qe, s));
     {
       Timer t(e, 1, s);
-      MTE_TRY(launch_attention(mode, e->qkv, e->attn, W.o_pre, cu.data(), batch, Hq, Hkv, d, s));
+      const size_t lstride = (size_t)e->max_prefix * nqkv;
+      if (pre && pre->record)
+        MTE_TRY(hipMemcpyAsync(pre->cache + l * lstride, e->qkv, (size_t)T * nqkv * sizeof(float),
+                               hipMemcpyDeviceToDevice, s));
+      const bool use = pre && !pre->record;
+      MTE_TRY(launch_attention(mode, e->qkv, use ? pre->cache + l * lstride : nullptr, use ? pre->P : 0,
+                               e->attn, W.o_pre, cu.data(), batch, Hq, Hkv, d, s));
     }
     {
       Timer t(e, 2, s);
@@ -495,6 +517,85 @@ int mte_encode_layers(mte_encoder *e, const float *h_in, const int32_t *pos_thw,
   if (err == hipSuccess)
     err = run_layers(e, h_out, cu, batch, T, layer_begin, layer_end, false, &np, stream);
   if (err == hipSuccess && np) err = launch_resid_add(h_out, e->ws, np, T, e->cfg.hidden, stream);
+  return err == hipSuccess ? MTE_OK : MTE_E_HIP;
+}
+
+int mte_encoder_reserve_prefix(mte_encoder *e, int32_t max_prefix) {
+  if (!e || max_prefix <= 0 || max_prefix > e->cfg.max_tokens || max_prefix > e->cfg.max_seq)
+    return MTE_E_INVALID;
+  if (e->cfg.n_layers == 0) return MTE_E_UNSUPPORTED;
+  DeviceGuard g(e->device);
+  const mte_config &c = e->cfg;
+  const size_t nqkv = (size_t)(c.n_q_heads + 2 * c.n_kv_heads) * c.head_dim;
+  if (hipDeviceSynchronize() != hipSuccess) return MTE_E_HIP;
+  hipFree(e->pkv);
+  e->pkv = nullptr;
+  e->max_prefix = 0;
+  if (hipMalloc((void **)&e->pkv, (size_t)c.n_layers * max_prefix * nqkv * sizeof(float)) != hipSuccess)
+    return MTE_E_OOM;
+  e->max_prefix = max_prefix;
+  return MTE_OK;
+}
+
+int mte_encode_prefixed(mte_encoder *e, const void *prefix_embeds, const int32_t *prefix_pos,
+                        int32_t prefix_len, const void *embeds, const int32_t *pos_thw,
+                        const int32_t *seq_lens, int32_t batch, void *out_prefix, void *out_hidden,
+                        hipStream_t stream) {
+  if (!e || !prefix_embeds || !prefix_pos || !embeds || !pos_thw || !out_prefix || !out_hidden)
+    return MTE_E_INVALID;
+  const mte_config &c = e->cfg;
+  if (c.n_layers == 0 || !e->pkv) return MTE_E_INVALID;     // mte_encoder_reserve_prefix first
+  if (prefix_len <= 0) return MTE_E_INVALID;
+  if (prefix_len > e->max_prefix) return MTE_E_CAPACITY;
+  int32_t T = 0;
+  int st = mte_check_batch(&c, seq_lens, batch, &T);
+  if (st != MTE_OK) return st;
+  for (int i = 0; i < batch; ++i)
+    if ((int64_t)prefix_len + seq_lens[i] > c.max_seq) return MTE_E_CAPACITY;
+  const size_t in_b = (size_t)T * c.hidden * esize(c.dtype), out_b = (size_t)T * c.hidden * esize(c.out_dtype);
+  const size_t pin_b = (size_t)prefix_len * c.hidden * esize(c.dtype);
+  const size_t pout_b = (size_t)prefix_len * c.hidden * esize(c.out_dtype);
+  auto overlap = [](const void *a, size_t na, const void *b, size_t nb) {
+    const char *x = (const char *)a, *y = (const char *)b;
+    return x < y + nb && y < x + na;
+  };
+  if (overlap(embeds, in_b, out_hidden, out_b) || overlap(prefix_embeds, pin_b, out_hidden, out_b) ||
+      overlap(embeds, in_b, out_prefix, pout_b) || overlap(prefix_embeds, pin_b, out_prefix, pout_b) ||
+      overlap(out_prefix, pout_b, out_hidden, out_b))
+    return MTE_E_INVALID;
+  DeviceGuard g(e->device);
+  const int out_fmt = in_fmt(c.out_dtype);
+  hipError_t err = hipSuccess;
+  // 1. The prefix, once: one sequence of prefix_len tokens, recording every
+  //    layer's q/k/v rows.
+  {
+    std::vector<int32_t> cu{0, prefix_len};
+    const PrefixCtx rec{e->pkv, prefix_len, true};
+    err = launch_rope_table(prefix_pos, prefix_len, c.head_dim / 2, e->rope, e->rcos, e->rsin, stream);
+    if (err == hipSuccess)
+      err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, prefix_embeds, e->h, nullptr, 0, e->layers[0].attn_norm,
+                           e->xn, prefix_len, c.hidden, c.rms_eps, stream);
+    int np = 0;
+    if (err == hipSuccess) err = run_layers(e, e->h, cu, 1, prefix_len, 0, c.n_layers, true, &np, stream, &rec);
+    if (err == hipSuccess)
+      err = launch_rmsnorm(FMT_F32, out_fmt, e->h, nullptr, np ? e->ws : nullptr, np, e->final_norm, out_prefix,
+                           prefix_len, c.hidden, c.rms_eps, stream);
+  }
+  // 2. The sequences' own tokens, attending to the cached prefix first.
+  if (err == hipSuccess) {
+    std::vector<int32_t> cu(batch + 1, 0);
+    for (int i = 0; i < batch; ++i) cu[i + 1] = cu[i] + seq_lens[i];
+    const PrefixCtx use{e->pkv, prefix_len, false};
+    err = launch_rope_table(pos_thw, T, c.head_dim / 2, e->rope, e->rcos, e->rsin, stream);
+    if (err == hipSuccess)
+      err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, embeds, e->h, nullptr, 0, e->layers[0].attn_norm, e->xn,
+                           T, c.hidden, c.rms_eps, stream);
+    int np = 0;
+    if (err == hipSuccess) err = run_layers(e, e->h, cu, batch, T, 0, c.n_layers, true, &np, stream, &use);
+    if (err == hipSuccess)
+      err = launch_rmsnorm(FMT_F32, out_fmt, e->h, nullptr, np ? e->ws : nullptr, np, e->final_norm, out_hidden,
+                           T, c.hidden, c.rms_eps, stream);
+  }
   return err == hipSuccess ? MTE_OK : MTE_E_HIP;
 }
 

@@ -36,6 +36,8 @@ constexpr int kMaxSeqPerLaunch = 256;
 
 struct AttnArgs {
   const float *qkv;   // [T, ld_qkv] fp32
+  const float *pre;   // [P, ld_qkv] fp32: keys / values of a shared prefix every sequence sees, or null
+  int P;              // prefix length (0: none)
   char *o;
   float o_scale;   // output multiplier (MODE_F16)
   int ld_qkv;      // floats per token row of qkv
@@ -163,7 +165,14 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   float m_i = -INFINITY, l_i = 0.f;
   const int my_q = qw + lrow;
 
-  const int n_blocks = (q_last >= 0) ? (q_last / KV + 1) : 0;
+  // Keys are numbered over [0, P + L): the shared prefix's first, then the
+  // sequence's own; own query i sits at key index P + i.
+  const int P = a.P;
+  const int n_blocks = (q_last >= 0) ? ((P + q_last) / KV + 1) : 0;
+  auto key_row = [&](int kv) -> const float * {
+    kv = min(kv, P + L - 1);
+    return kv < P ? a.pre + (size_t)kv * ld : a.qkv + base + (size_t)(kv - P) * ld;
+  };
   // Staging of one key/value tile through registers, one tile ahead:
   //  K: thread chunk (row r, chunk c) of EC consecutive d -> sK[r][c] (swizzled);
   //  V: thread (column d, row group v) reads EC rows of column d (lanes
@@ -179,10 +188,11 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   auto gload = [&](int b, int kv0) {
 #pragma unroll
     for (int t = 0; t < KCH; ++t) {
-      const int idx = tid + t * 256, r = min(kv0 + idx / NCH, L - 1), c = idx % NCH;
+      const int idx = tid + t * 256, c = idx % NCH;
+      const float *kr = key_row(kv0 + idx / NCH);
 #pragma unroll
       for (int e = 0; e < EC; e += 4) {
-        const f32x4 v = *(const f32x4 *)(a.qkv + base + (size_t)r * ld + k_off + c * EC + e);
+        const f32x4 v = *(const f32x4 *)(kr + k_off + c * EC + e);
         kx[b][t][e] = v[0]; kx[b][t][e + 1] = v[1]; kx[b][t][e + 2] = v[2]; kx[b][t][e + 3] = v[3];
       }
     }
@@ -191,7 +201,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       const int idx = tid + t * 256, d = idx % HD, v = idx / HD;
 #pragma unroll
       for (int e = 0; e < EC; ++e)
-        vx[b][t][e] = a.qkv[base + (size_t)min(kv0 + v * EC + e, L - 1) * ld + v_off + d];
+        vx[b][t][e] = key_row(kv0 + v * EC + e)[v_off + d];
     }
   };
   // Register slot b -> LDS tile sKb / sVtb.
@@ -235,7 +245,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   };
   // One key/value tile for this wave: scores, online softmax, O update.
   auto compute = [&](int kv0, const u32x4 *sK, const T *sVt) {
-    if (!(qw < L && kv0 <= wave_last)) return;
+    if (!(qw < L && kv0 <= P + wave_last)) return;
     // Independent accumulators (one per split product, or per k parity
     // for fp32) so consecutive MFMAs do not wait on each other's results.
     constexpr int NS = (NP == 2) ? 3 : 2;
@@ -263,7 +273,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int kv = kv0 + acc_row(r, lane);
-      s[r] = (kv <= my_q && kv < L) ? s[r] * sc : -INFINITY;
+      s[r] = (kv <= P + my_q && kv < P + L) ? s[r] * sc : -INFINITY;
       mb = fmaxf(mb, s[r]);
     }
     mb = warp_max_xor(mb, 32);
@@ -371,11 +381,14 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   }
 }
 
-hipError_t launch_attention(int mode, const float *qkv, void *o, float out_scale, const int32_t *cu,
-                            int batch, int Hq, int Hkv, int d, hipStream_t s) {
+hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int P, void *o, float out_scale,
+                            const int32_t *cu, int batch, int Hq, int Hkv, int d, hipStream_t s) {
   const int rep = Hq / Hkv;
+  if (P < 0 || (P > 0 && !prefix)) return hipErrorInvalidValue;
   AttnArgs a;
   a.qkv = qkv;
+  a.pre = prefix;
+  a.P = P;
   a.ld_qkv = (Hq + 2 * Hkv) * d;
   a.o = (char *)o;
   a.o_scale = out_scale;
@@ -402,7 +415,7 @@ hipError_t launch_attention(int mode, const float *qkv, void *o, float out_scale
     dim3 grid(tiles, Hkv * a.head_blocks);
     // Sequences of at most 128 tokens: every workgroup stages all of its
     // (at most 4) key/value tiles at once.
-    const bool all = max_len <= 4 * 32;
+    const bool all = P + max_len <= 4 * 32;
 #define MTE_ATTN(M_, D_)                                                             \
     if (all) hipLaunchKernelGGL((k_attn<M_, D_, 4>), grid, dim3(256), 0, s, a);      \
     else hipLaunchKernelGGL((k_attn<M_, D_, 1>), grid, dim3(256), 0, s, a);

@@ -109,11 +109,13 @@ hipError_t launch_qkv_parts(float *qkv, const float *parts, int nparts, int T, i
 
 // Causal GQA attention over packed sequences. qkv: fp32 [T, (Hq+2Hkv)*d],
 // q heads first, then k, then v (q and k already normalised and rotated).
-// o: [T, Hq*d], float (MODE_F32) or fp16 (MODE_F16) times out_scale.
-// cu: host int32[batch+1] sequence offsets. Launches in chunks of <= 256
-// sequences.
-hipError_t launch_attention(int mode, const float *qkv, void *o, float out_scale, const int32_t *cu,
-                            int batch, int Hq, int Hkv, int d, hipStream_t s);
+// prefix: fp32 [P, (Hq+2Hkv)*d] rows of a shared prefix (same layout; its k
+// and v columns are read) that every sequence attends to in full before
+// its own keys, or P = 0. o: [T, Hq*d], float (MODE_F32) or fp16
+// (MODE_F16) times out_scale. cu: host int32[batch+1] sequence offsets.
+// Launches in chunks of <= 256 sequences.
+hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int P, void *o, float out_scale,
+                            const int32_t *cu, int batch, int Hq, int Hkv, int d, hipStream_t s);
 
 // Positions of packed sequences (see mte_build_positions).
 hipError_t launch_positions(const int32_t *layouts5, int batch, int32_t *pos_thw, int T,

@@ -79,6 +79,27 @@ class TextEncoder:
                             len(seq_lens), layer_begin, layer_end, h_out.data_ptr(), _stream(stream))
         return h_out
 
+    def reserve_prefix(self, max_prefix: int) -> None:
+        B.mte_encoder_reserve_prefix(self.handle, max_prefix)
+
+    def encode_prefixed(self, prefix_embeds: torch.Tensor, prefix_pos: torch.Tensor,
+                        embeds: torch.Tensor, pos_thw: torch.Tensor, seq_lens: Sequence[int],
+                        stream: Optional[torch.cuda.Stream] = None):
+        """Sequences sharing a prefix -> (prefix rows [P, D], own rows [T, D])."""
+        P, T = prefix_embeds.shape[0], int(sum(seq_lens))
+        for name, t, rows in (("prefix_embeds", prefix_embeds, P), ("embeds", embeds, T)):
+            if t.dtype != self.dtype or t.shape != (rows, self.cfg.hidden) or not t.is_contiguous():
+                raise ValueError(f"{name} must be a contiguous [rows, hidden] tensor of the encoder dtype")
+        for name, t, rows in (("prefix_pos", prefix_pos, P), ("pos_thw", pos_thw, T)):
+            if t.dtype != torch.int32 or t.shape != (3, rows) or not t.is_contiguous():
+                raise ValueError(f"{name} must be a contiguous int32 [3, rows] tensor")
+        out_p = torch.empty((P, self.cfg.hidden), dtype=self.out_dtype, device=embeds.device)
+        out = torch.empty((T, self.cfg.hidden), dtype=self.out_dtype, device=embeds.device)
+        B.mte_encode_prefixed(self.handle, prefix_embeds.data_ptr(), prefix_pos.data_ptr(), P,
+                              embeds.data_ptr(), pos_thw.data_ptr(), list(seq_lens), len(seq_lens),
+                              out_p.data_ptr(), out.data_ptr(), _stream(stream))
+        return out_p, out
+
     def close(self) -> None:
         if getattr(self, "handle", None):
             B.mte_encoder_destroy(self.handle)

@@ -25,7 +25,8 @@ def _declared_functions():
 def test_header_declares_the_boundary():
     names = _declared_functions()
     for n in ("mte_encoder_create", "mte_encode", "mte_build_positions", "mte_encoder_destroy",
-              "mte_status_string", "mte_config_validate", "mte_check_batch", "mte_encode_layers"):
+              "mte_status_string", "mte_config_validate", "mte_check_batch", "mte_encode_layers",
+              "mte_encoder_reserve_prefix", "mte_encode_prefixed"):
         assert n in names
 
 
@@ -87,6 +88,8 @@ def test_encode_rejects_null_encoder(B):
     assert B.lib.mte_encode(None, 1, 1, B._i32([4]), 1, 1, None) == -1
     assert B.lib.mte_encode_layers(None, 1, 1, B._i32([4]), 1, 0, 1, 1, None) == -1
     assert B.lib.mte_timing_enable(None, 0, 4) == -1
+    assert B.lib.mte_encoder_reserve_prefix(None, 80) == -1
+    assert B.lib.mte_encode_prefixed(None, 1, 1, 80, 1, 1, B._i32([96]), 1, 1, 1, None) == -1
     B.lib.mte_encoder_destroy(None)  # no-op
 
 
