@@ -522,7 +522,7 @@ static const double kTileRate[kNumTiles] = {959, 944, 895, 850, 850, 884, 850, 8
 
 // Measured choices (MI355X sweep of every tile and split count, weights
 // rotated through 600 MB so that they stream from HBM) for the decoder's four
-// projections (D 2048 / FFN 6144 / 16+8+8 heads of 128). A K split is only
+// projections (D 2048 / FFN 6144 / 16+8+8 heads of 128) at 96 ... 10240 rows. A K split is only
 // kept where it still wins after the consumer's extra pass over the fp32
 // partial sums (at 1536 rows two QKV partials cost 16 us to add up, more than
 // the split saves). Other row counts take the entry of the nearest row
@@ -541,6 +541,8 @@ static const TileChoice kChoices[] = {
     {12288, 2048, EPI_SWIGLU, 768, 3, 1},  {2048, 6144, EPI_RESID, 768, 14, 2},
     {4096, 2048, EPI_QKV, 1536, 23, 1},   {2048, 2048, EPI_RESID, 1536, 12, 1},
     {12288, 2048, EPI_SWIGLU, 1536, 20, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
+    {4096, 2048, EPI_QKV, 3072, 27, 1},   {2048, 2048, EPI_RESID, 3072, 23, 1},
+    {12288, 2048, EPI_SWIGLU, 3072, 20, 1}, {2048, 6144, EPI_RESID, 3072, 23, 1},
     {4096, 2048, EPI_QKV, 10240, 27, 1},  {2048, 2048, EPI_RESID, 10240, 2, 1},
     {12288, 2048, EPI_SWIGLU, 10240, 26, 1}, {2048, 6144, EPI_RESID, 10240, 12, 1},
 };

@@ -92,6 +92,27 @@ def test_tiny_fp32_ragged_edges(torch):
     assert rel_err(got, ref) <= TOL_F32
 
 
+def test_tiny_fp32_many_short_sequences(torch):
+    """300 sequences of 1..8 tokens in one packed batch: the attention launches in chunks of
+    256 sequences and the position kernel in chunks of 128, so this crosses both chunk
+    boundaries; every sequence must still see only itself."""
+    dims = W.DIMS_TINY
+    layouts = tuple(W.SeqLayout(1 + i % 3, 1 if i % 4 else 0, 1 if i % 4 else 0, 1 + i % 2 if i % 4 else 0,
+                                i % 4) for i in range(300))
+    lens = W.seq_lens(layouts)
+    assert len(lens) > 256 and min(lens) >= 1
+    emb = W.embeddings(dims, layouts)
+    _say("tiny many", len(lens), sum(lens))
+    enc = make_encoder(dims, max_tokens=4096, max_batch=512, max_seq=64)
+    got = _gpu_encode(torch, enc, dims, emb, layouts)
+    enc.close()
+    ref = oracle_encode(dims, emb, layouts)
+    assert rel_err(got, ref) <= TOL_F32
+    sl = seq_slices(layouts)
+    for i in (0, 127, 128, 255, 256, 299):
+        assert rel_err(got[sl[i]], ref[sl[i]]) <= TOL_F32, i
+
+
 def test_tiny_zero_layers_is_final_norm(torch):
     dims = W.DIMS_TINY.with_(n_layers=0)
     wl = W.workload("tiny_fp32")
