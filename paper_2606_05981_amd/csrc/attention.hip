@@ -135,8 +135,10 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 
   // Q fragments of this wave's 32 rows (B operand of S^T = K Q^T); rows
   // past the sequence read its last row (their outputs are not stored).
+  // Loaded after the first key/value tiles' loads are issued, so that the
+  // two global-load round trips overlap.
   frag_t qf[NP][NCH / 2];
-  {
+  auto load_q = [&]() {
     const int qi = min(qw + lrow, L - 1);
 #pragma unroll
     for (int kk = 0; kk < NCH / 2; ++kk) {
@@ -153,7 +155,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
         for (int e = 0; e < EC; ++e) qf[p][kk][e] = sp[p][e];
     }
-  }
+  };
   // Scores are kept in log2 units: s * log2(e) / sqrt(d).
   const float sc = 1.4426950408889634f * rsqrtf((float)HD);
 
@@ -324,6 +326,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   };
   if constexpr (NB == 1) {
     if (n_blocks > 0) gload(0, 0);
+    load_q();
     for (int kb = 0; kb < n_blocks; ++kb) {
       const int kv0 = kb * KV;
       lstore(0, sK_of(0), sVt_of(0));
@@ -338,6 +341,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     for (int b = 0; b < NB; ++b)
       if (b < n_blocks) gload(b, b * KV);
     __builtin_amdgcn_sched_barrier(0);   // every tile's loads in flight before the first LDS write
+    load_q();
 #pragma unroll
     for (int b = 0; b < NB; ++b)
       if (b < n_blocks) lstore(b, sK_of(b), sVt_of(b));
