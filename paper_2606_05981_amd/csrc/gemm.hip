@@ -205,8 +205,13 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
   constexpr int ACH = BM * CH, BCH = BN * CH;     // chunks per stage (A / W)
   constexpr int NW = WM * WN;                     // waves per workgroup
   constexpr int NT = 64 * NW;                     // threads per workgroup
-  static_assert(ACH % NT == 0 && BCH % NT == 0, "whole DMA rounds");
-  constexpr int AR = ACH / NT, BR = BCH / NT;     // DMA instructions per thread per matrix
+  // DMA rounds: each wave instruction fills one group of 64 chunks. A last,
+  // partial round repeats the matrix's final group in the waves past it
+  // (the same bytes to the same LDS slots), so every wave issues the same
+  // number of loads and the vmcnt waits stay exact.
+  static_assert(ACH % 64 == 0 && BCH % 64 == 0, "whole 64-chunk groups");
+  constexpr int AG = ACH / 64, BG = BCH / 64;     // chunk groups per stage
+  constexpr int AR = (AG + NW - 1) / NW, BR = (BG + NW - 1) / NW;   // DMA instructions per thread
   constexpr int LOADS = AR + BR;                  // per thread per stage
   constexpr int STAGE = (BM + BN) * CH;           // u32x4 slots per stage
   static_assert(NW == 4 || NW == 8, "4 or 8 waves");
@@ -229,12 +234,12 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
   const char *pb[BR];
 #pragma unroll
   for (int c = 0; c < AR; ++c) {
-    const int q = (c * NW + wave) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
+    const int q = min(c * NW + wave, AG - 1) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
     pa[c] = g.A + (size_t)min(m0 + r, M - 1) * rowb + kb0 + ch * 16;
   }
 #pragma unroll
   for (int c = 0; c < BR; ++c) {
-    const int q = (c * NW + wave) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
+    const int q = min(c * NW + wave, BG - 1) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
     pb[c] = g.W + (size_t)(n0 + r) * rowb + kb0 + ch * 16;
   }
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
@@ -244,10 +249,10 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
     const uint32_t st = lds0 + (uint32_t)(slot * STAGE) * 16u;
     const size_t ko = (size_t)ks * ROWB;
     if (x < AR) {
-      dma16(pa[x] + ko, st + (uint32_t)((x * NW + uwave) * 64) * 16u);
+      dma16(pa[x] + ko, st + (uint32_t)(min(x * NW + uwave, AG - 1) * 64) * 16u);
     } else {
       const int c = x - AR;
-      dma16(pb[c] + ko, st + (uint32_t)(ACH + (c * NW + uwave) * 64) * 16u);
+      dma16(pb[c] + ko, st + (uint32_t)(ACH + min(c * NW + uwave, BG - 1) * 64) * 16u);
     }
   };
 
@@ -447,8 +452,8 @@ static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
 // Tile table: id -> instantiation (bm, bn, wave layout wm x wn, bytes of K
 // per row per stage, LDS ring stages, workgroups per CU, built for fp32
 // operands too). The LDS ring (P * (bm + bn) * rowb bytes) must fit
-// 160 KB / occ; bm * rowb / 16 and bn * rowb / 16 must be multiples of the
-// workgroup's thread count (whole DMA rounds).
+// 160 KB / occ; bm * rowb / 16 and bn * rowb / 16 must be multiples of 64
+// (whole 64-chunk DMA groups).
 #define MTE_TILE_TABLE(X)                    \
   X(0, 256, 256, 2, 2, 64, 4, 1, 0)          \
   X(1, 256, 192, 2, 2, 64, 4, 1, 0)          \
@@ -480,7 +485,9 @@ static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
   X(27, 256, 256, 4, 2, 64, 4, 1, 0)         \
   X(28, 256, 128, 4, 2, 64, 6, 1, 0)         \
   X(29, 128, 256, 2, 4, 64, 6, 1, 0)         \
-  X(30, 128, 128, 2, 4, 128, 4, 1, 0)
+  X(30, 128, 128, 2, 4, 128, 4, 1, 0)         \
+  X(31, 384, 192, 4, 2, 64, 4, 1, 0)         \
+  X(32, 192, 384, 2, 4, 64, 4, 1, 0)
 
 static const TileCfg kTiles[] = {
 #define MTE_TILE_INFO(id, bm, bn, wm, wn, rowb, p, occ, f32) {bm, bn, wm, wn, rowb, occ, f32},
@@ -518,7 +525,7 @@ static bool tile_fits(int id, int N, int K, int esz, int epi, int splits, int co
 static const double kTileRate[kNumTiles] = {959, 944, 895, 850, 850, 884, 850, 850, 800, 819,
                                             640, 777, 860, 600, 700, 650, 550, 450, 600, 600,
                                             921, 850, 850, 714, 766, 800, 1026, 1018, 850, 728,
-                                            803};
+                                            803, 950, 950};
 
 // Measured choices (MI355X sweep of every tile and split count, weights
 // rotated through 600 MB so that they stream from HBM) for the decoder's four
@@ -540,9 +547,9 @@ static const TileChoice kChoices[] = {
     {4096, 2048, EPI_QKV, 768, 12, 1},    {2048, 2048, EPI_RESID, 768, 12, 2},
     {12288, 2048, EPI_SWIGLU, 768, 3, 1},  {2048, 6144, EPI_RESID, 768, 14, 2},
     {4096, 2048, EPI_QKV, 1536, 23, 1},   {2048, 2048, EPI_RESID, 1536, 12, 1},
-    {12288, 2048, EPI_SWIGLU, 1536, 20, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
+    {12288, 2048, EPI_SWIGLU, 1536, 32, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
     {4096, 2048, EPI_QKV, 3072, 27, 1},   {2048, 2048, EPI_RESID, 3072, 23, 1},
-    {12288, 2048, EPI_SWIGLU, 3072, 20, 1}, {2048, 6144, EPI_RESID, 3072, 23, 1},
+    {12288, 2048, EPI_SWIGLU, 3072, 32, 1}, {2048, 6144, EPI_RESID, 3072, 23, 1},
     {4096, 2048, EPI_QKV, 10240, 27, 1},  {2048, 2048, EPI_RESID, 10240, 2, 1},
     {12288, 2048, EPI_SWIGLU, 10240, 26, 1}, {2048, 6144, EPI_RESID, 10240, 12, 1},
 };
