@@ -23,8 +23,8 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_gemm_b16_traffic.json")
-KERNEL_SOURCES = ["paper_2606_05981_amd/csrc/gemm.hip", "paper_2606_05981_amd/csrc/common.h",
-                  "paper_2606_05981_amd/csrc/launch.h"]
+KERNEL_SOURCES = ["paper_2606_05981_amd/csrc/gemm_kernel.h", "paper_2606_05981_amd/csrc/gemm.hip",
+                  "paper_2606_05981_amd/csrc/common.h", "paper_2606_05981_amd/csrc/launch.h"]
 
 
 def kernel_source_hash():

@@ -59,6 +59,15 @@ typedef enum {
 
 typedef enum { MTE_MROPE_SECTIONS = 0, MTE_MROPE_INTERLEAVED = 1 } mte_mrope_layout;
 
+/* How the encoder stores its projection weights (mte_config.weight_format).
+ * MTE_WEIGHTS_DTYPE: in config.dtype. MTE_WEIGHTS_E4M3: as OCP fp8 e4m3 codes
+ * with one power-of-two scale per weight row, quantised at creation by
+ * mte_quantize_e4m3_rows: half the bytes of bf16 per forward, which is what
+ * bounds a batch of one frame. The paper leaves FP8 execution on FP8-capable
+ * hardware as an unverified direction (Sec. "Negative Results and Case
+ * Studies", TensorRT FP16 paragraph). Only with dtype MTE_BF16. */
+typedef enum { MTE_WEIGHTS_DTYPE = 0, MTE_WEIGHTS_E4M3 = 1 } mte_weight_format;
+
 /* Model shape and workspace capacity.
  *  hidden = D, n_q_heads = Hq, n_kv_heads = Hkv (Hq % Hkv == 0; query head h
  *  reads kv head h / (Hq/Hkv)), head_dim = d in {64, 128}, ffn = F.
@@ -74,7 +83,11 @@ typedef enum { MTE_MROPE_SECTIONS = 0, MTE_MROPE_INTERLEAVED = 1 } mte_mrope_lay
  *  dtype: storage type of the weights, the embeddings and the bf16/f32
  *  GEMM operands (MTE_BF16: bf16 with fp32 accumulation and an fp32 residual
  *  stream; MTE_F32: fp32 throughout). out_dtype: type of out_hidden.
- *  max_tokens / max_batch / max_seq: capacity the workspace is sized for. */
+ *  max_tokens / max_batch / max_seq: capacity the workspace is sized for.
+ *  weight_format: mte_weight_format (MTE_WEIGHTS_E4M3 needs dtype MTE_BF16,
+ *  else MTE_E_UNSUPPORTED). With e4m3 weights the encoder computes the same
+ *  forward with every linear weight replaced by its dequantised value
+ *  code * scale; activations, norms and attention are unchanged. */
 typedef struct {
   int32_t n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn;
   float rms_eps, rope_theta;
@@ -84,6 +97,7 @@ typedef struct {
   int32_t dtype;
   int32_t out_dtype;
   int32_t max_tokens, max_batch, max_seq;
+  int32_t weight_format;
 } mte_config;
 
 /* One layer's weights: device pointers of type config.dtype, linear weights
@@ -206,6 +220,24 @@ int mte_encode_prefixed(mte_encoder *enc, const void *prefix_embeds, const int32
 
 /* Frees the encoder (synchronises the device first). NULL is a no-op. */
 void mte_encoder_destroy(mte_encoder *enc);
+
+/* OCP fp8 e4m3 quantisation of the rows of a matrix, the weight format of
+ * MTE_WEIGHTS_E4M3 (e4m3: sign, 4 exponent bits of bias 7, 3 significand
+ * bits; subnormals below 2^-6 in steps of 2^-9; largest finite 448; codes
+ * 0x7F / 0xFF are NaN and never produced).
+ *  src: device [rows, cols] of src_dtype (MTE_F32 or MTE_BF16), row-major.
+ *  scales: device float[rows] out: scales[r] = 2^e_r with e_r the smallest
+ *    integer such that max_c |src[r,c]| <= 448 * 2^e_r (1.0 for an all-zero
+ *    row).
+ *  codes: device uint8[rows, cols] out: the e4m3 code nearest to
+ *    src[r,c] / 2^e_r (an exact division), ties to the even significand;
+ *    a result of zero is coded +0 (0x00) whatever the sign.
+ * The dequantised weight is decode(codes[r,c]) * scales[r]. Enqueues one
+ * kernel on `stream`; no allocation, no synchronisation.
+ * Errors: MTE_E_INVALID (null pointer, rows or cols <= 0, bad dtype),
+ * MTE_E_HIP (launch failure). */
+int mte_quantize_e4m3_rows(const void *src, int32_t src_dtype, int32_t rows, int32_t cols,
+                           uint8_t *codes, float *scales, hipStream_t stream);
 
 /* Static description of a status code. Never NULL. */
 const char *mte_status_string(int status);

@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(_HERE, "libmte.so")
 
 MTE_F32, MTE_BF16 = 0, 1
 MTE_MROPE_SECTIONS, MTE_MROPE_INTERLEAVED = 0, 1
+MTE_WEIGHTS_DTYPE, MTE_WEIGHTS_E4M3 = 0, 1
 STATUS = {0: "MTE_OK", -1: "MTE_E_INVALID", -2: "MTE_E_CAPACITY", -3: "MTE_E_HIP",
           -4: "MTE_E_OOM", -5: "MTE_E_UNSUPPORTED"}
 KERNEL_CLASSES = {"qkv_gemm": 0, "attention": 1, "o_gemm": 2, "gate_up_gemm": 3, "down_gemm": 4}
@@ -34,7 +35,8 @@ class mte_config(C.Structure):
                 ("rms_eps", C.c_float), ("rope_theta", C.c_float),
                 ("mrope_section", C.c_int32 * 3), ("mrope_layout", C.c_int32),
                 ("qk_norm", C.c_int32), ("dtype", C.c_int32), ("out_dtype", C.c_int32),
-                ("max_tokens", C.c_int32), ("max_batch", C.c_int32), ("max_seq", C.c_int32)]
+                ("max_tokens", C.c_int32), ("max_batch", C.c_int32), ("max_seq", C.c_int32),
+                ("weight_format", C.c_int32)]
 
 
 class mte_layer_weights(C.Structure):
@@ -74,6 +76,7 @@ _sig = {
     "mte_timing_enable": (C.c_int, [_P, C.c_int32, C.c_int32]),
     "mte_timing_read": (C.c_int, [_P, C.POINTER(C.c_int32), C.POINTER(C.c_double)]),
     "mte_timing_disable": (C.c_int, [_P]),
+    "mte_quantize_e4m3_rows": (C.c_int, [_P, C.c_int32, C.c_int32, C.c_int32, _P, _P, _P]),
 }
 for _name, (_res, _args) in _sig.items():
     _f = getattr(lib, _name)
@@ -93,7 +96,7 @@ def _i32(values: Sequence[int]):
 def make_config(n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, rms_eps=1e-6,
                 rope_theta=5e6, mrope_section=(24, 20, 20), mrope_layout=0, qk_norm=1,
                 dtype=MTE_BF16, out_dtype=None, max_tokens=4096, max_batch=64,
-                max_seq=4096) -> mte_config:
+                max_seq=4096, weight_format=MTE_WEIGHTS_DTYPE) -> mte_config:
     c = mte_config()
     c.n_layers, c.hidden, c.n_q_heads, c.n_kv_heads = n_layers, hidden, n_q_heads, n_kv_heads
     c.head_dim, c.ffn, c.rms_eps, c.rope_theta = head_dim, ffn, rms_eps, rope_theta
@@ -101,6 +104,7 @@ def make_config(n_layers, hidden, n_q_heads, n_kv_heads, head_dim, ffn, rms_eps=
     c.mrope_layout, c.qk_norm, c.dtype = mrope_layout, qk_norm, dtype
     c.out_dtype = dtype if out_dtype is None else out_dtype
     c.max_tokens, c.max_batch, c.max_seq = max_tokens, max_batch, max_seq
+    c.weight_format = weight_format
     return c
 
 
@@ -181,3 +185,9 @@ def mte_timing_read(enc: int):
 
 def mte_timing_disable(enc: int) -> int:
     return _check(lib.mte_timing_disable(enc), "mte_timing_disable")
+
+
+def mte_quantize_e4m3_rows(src: int, src_dtype: int, rows: int, cols: int, codes: int, scales: int,
+                           stream: int) -> int:
+    return _check(lib.mte_quantize_e4m3_rows(src, src_dtype, rows, cols, codes, scales, stream),
+                  "mte_quantize_e4m3_rows")

@@ -23,7 +23,9 @@ constexpr int64_t kMaxTokens = (1 << 24) - 1;  // positions and offsets stay exa
 constexpr int kNumClasses = 5;
 
 struct LayerW {
-  void *w_qkv, *w_o, *w_gu, *w_d;              // operand type (fp16 or fp32), repacked
+  void *w_qkv, *w_o, *w_gu, *w_d;              // operand type (fp16, fp32 or e4m3 codes), repacked
+  // e4m3 weights: the scale of every weight row (column of the product)
+  const float *cs_qkv = nullptr, *cs_o = nullptr, *cs_gu = nullptr, *cs_d = nullptr;
   float *attn_norm, *mlp_norm, *q_norm, *k_norm;
   // Products are multiplied by s_* (the inverse of the weight's and the
   // activation's power-of-two pre-scales); the attention output and the
@@ -59,6 +61,7 @@ struct mte_encoder {
   float *final_norm = nullptr;
   // Activations feeding the matrix cores are fp32 (MODE_F32) or fp16 (MODE_F16).
   int mode = MODE_F32;
+  int gmode = MODE_F32;      // of the projection GEMMs: mode, or MODE_F8W for e4m3 weights
   int act_fmt = FMT_F32;
   float *h = nullptr;        // [max_tokens, D] fp32 residual stream
   void *xn = nullptr;        // [max_tokens, D] normalised GEMM input
@@ -117,6 +120,8 @@ int mte_config_validate(const mte_config *c) {
       (c->out_dtype != MTE_F32 && c->out_dtype != MTE_BF16))
     return MTE_E_INVALID;
   if (c->max_tokens <= 0 || c->max_batch <= 0 || c->max_seq <= 0) return MTE_E_INVALID;
+  if (c->weight_format != MTE_WEIGHTS_DTYPE && c->weight_format != MTE_WEIGHTS_E4M3) return MTE_E_INVALID;
+  if (c->weight_format == MTE_WEIGHTS_E4M3 && c->dtype != MTE_BF16) return MTE_E_UNSUPPORTED;
   // Shapes the kernels are built for.
   if (c->head_dim != 64 && c->head_dim != 128) return MTE_E_UNSUPPORTED;
   const int rep = c->n_q_heads / c->n_kv_heads;
@@ -206,11 +211,15 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
   e->cfg = c;
   if (hipGetDevice(&e->device) != hipSuccess) { delete e; return MTE_E_HIP; }
 
-  const size_t es = esize(c.dtype);              // weights and activations: fp16 or fp32
+  const size_t es = esize(c.dtype);              // activations: fp16 or fp32
+  const bool w8 = c.weight_format == MTE_WEIGHTS_E4M3;
+  const size_t ws8 = w8 ? 1 : es;                // bytes per stored weight
   const size_t D = c.hidden, F = c.ffn, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads;
   const size_t nqkv = (Hq + 2 * Hkv) * d;
-  const size_t b_qkv = nqkv * D * es, b_o = D * Hq * d * es, b_gu = 2 * F * D * es, b_d = D * F * es;
-  const size_t per_layer = b_qkv + b_o + b_gu + b_d;
+  const size_t b_qkv = nqkv * D * ws8, b_o = D * Hq * d * ws8, b_gu = 2 * F * D * ws8, b_d = D * F * ws8;
+  // e4m3: the row scales of the four matrices follow their codes
+  const size_t b_cs = w8 ? (nqkv + D + 2 * F + D) * sizeof(float) : 0;
+  const size_t per_layer = b_qkv + b_o + b_gu + b_d + b_cs;
   const size_t g_per_layer = 2 * D + 2 * d;
   const size_t MT = c.max_tokens;
 
@@ -219,6 +228,7 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
   if (hipMalloc((void **)&e->gbuf, (g_per_layer * c.n_layers + D) * sizeof(float)) != hipSuccess)
     return fail(MTE_E_OOM);
   e->mode = c.dtype == MTE_BF16 ? MODE_F16 : MODE_F32;
+  e->gmode = w8 ? MODE_F8W : e->mode;
   e->act_fmt = c.dtype == MTE_BF16 ? FMT_F16 : FMT_F32;
   if (hipMalloc((void **)&e->h, MT * D * sizeof(float)) != hipSuccess ||
       hipMalloc(&e->xn, MT * D * es) != hipSuccess ||
@@ -296,10 +306,15 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
       // of v rows) and of gate / up is bounded by that times the row norm
       // of its weight; |silu(z)| <= |z|.
       const double ba = sqrtD * mx(S_AN), bm = sqrtD * mx(S_MN);
+      // e4m3 codes are within 2^-4 relative of their weight (plus a
+      // subnormal step 2^-10 of the row scale, far below 2^-4 of the row
+      // norm): the row norms of the dequantised weights grow by at most 1/8.
+      const double q8 = w8 ? 1.125 : 1.0;
       ka = act_shift(ba);
       km = act_shift(bm);
-      ko = act_shift(ba * rn(S_V));
-      ky = act_shift((bm * rn(S_G)) * (bm * rn(S_U)));
+      ko = act_shift(ba * rn(S_V) * q8);
+      ky = act_shift((bm * rn(S_G) * q8) * (bm * rn(S_U) * q8));
+      if (w8) w_qkv = w_o = w_gu = w_d = 0;    // codes are not pre-scaled; the row scales apply
     }
     o.s_qkv = std::ldexp(1.f, ka - w_qkv);
     o.s_o = std::ldexp(1.f, ko - w_o);
@@ -310,20 +325,49 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
     const int df = f16 ? FMT_F16 : FMT_F32;
     const size_t bq = Hq * d * D * es, bk = Hkv * d * D * es;
     const float sq = std::ldexp(1.f, w_qkv);
-    he = launch_convert_rows(sf, L.w_q, df, o.w_qkv, (int)(Hq * d), (int)D, sq, 0, 0, stream);
-    if (he == hipSuccess)
-      he = launch_convert_rows(sf, L.w_k, df, (char *)o.w_qkv + bq, (int)(Hkv * d), (int)D, sq, 0, 0, stream);
-    if (he == hipSuccess)
-      he = launch_convert_rows(sf, L.w_v, df, (char *)o.w_qkv + bq + bk, (int)(Hkv * d), (int)D, sq, 0, 0,
-                               stream);
-    if (he == hipSuccess)
-      he = launch_convert_rows(sf, L.w_o, df, o.w_o, (int)D, (int)(Hq * d), std::ldexp(1.f, w_o), 0, 0, stream);
-    if (he == hipSuccess)
-      he = launch_convert_rows(sf, L.w_gate, df, o.w_gu, (int)F, (int)D, std::ldexp(1.f, w_gu), 1, 0, stream);
-    if (he == hipSuccess)
-      he = launch_convert_rows(sf, L.w_up, df, o.w_gu, (int)F, (int)D, std::ldexp(1.f, w_gu), 1, 1, stream);
-    if (he == hipSuccess)
-      he = launch_convert_rows(sf, L.w_down, df, o.w_d, (int)D, (int)F, std::ldexp(1.f, w_d), 0, 0, stream);
+    if (w8) {
+      float *cs = (float *)(base + b_qkv + b_o + b_gu + b_d);
+      o.cs_qkv = cs;
+      o.cs_o = cs + nqkv;
+      o.cs_gu = cs + nqkv + D;
+      o.cs_d = cs + nqkv + D + 2 * F;
+      uint8_t *q = (uint8_t *)o.w_qkv;
+      float *qs = (float *)o.cs_qkv;
+      he = launch_quantize_e4m3_rows(sf, L.w_q, (int)(Hq * d), (int)D, q, qs, 0, 0, stream);
+      if (he == hipSuccess)
+        he = launch_quantize_e4m3_rows(sf, L.w_k, (int)(Hkv * d), (int)D, q + Hq * d * D, qs + Hq * d, 0, 0,
+                                       stream);
+      if (he == hipSuccess)
+        he = launch_quantize_e4m3_rows(sf, L.w_v, (int)(Hkv * d), (int)D, q + (Hq + Hkv) * d * D,
+                                       qs + (Hq + Hkv) * d, 0, 0, stream);
+      if (he == hipSuccess)
+        he = launch_quantize_e4m3_rows(sf, L.w_o, (int)D, (int)(Hq * d), (uint8_t *)o.w_o, (float *)o.cs_o, 0,
+                                       0, stream);
+      if (he == hipSuccess)
+        he = launch_quantize_e4m3_rows(sf, L.w_gate, (int)F, (int)D, (uint8_t *)o.w_gu, (float *)o.cs_gu, 1,
+                                       0, stream);
+      if (he == hipSuccess)
+        he = launch_quantize_e4m3_rows(sf, L.w_up, (int)F, (int)D, (uint8_t *)o.w_gu, (float *)o.cs_gu, 1, 1,
+                                       stream);
+      if (he == hipSuccess)
+        he = launch_quantize_e4m3_rows(sf, L.w_down, (int)D, (int)F, (uint8_t *)o.w_d, (float *)o.cs_d, 0, 0,
+                                       stream);
+    } else {
+      he = launch_convert_rows(sf, L.w_q, df, o.w_qkv, (int)(Hq * d), (int)D, sq, 0, 0, stream);
+      if (he == hipSuccess)
+        he = launch_convert_rows(sf, L.w_k, df, (char *)o.w_qkv + bq, (int)(Hkv * d), (int)D, sq, 0, 0, stream);
+      if (he == hipSuccess)
+        he = launch_convert_rows(sf, L.w_v, df, (char *)o.w_qkv + bq + bk, (int)(Hkv * d), (int)D, sq, 0, 0,
+                                 stream);
+      if (he == hipSuccess)
+        he = launch_convert_rows(sf, L.w_o, df, o.w_o, (int)D, (int)(Hq * d), std::ldexp(1.f, w_o), 0, 0, stream);
+      if (he == hipSuccess)
+        he = launch_convert_rows(sf, L.w_gate, df, o.w_gu, (int)F, (int)D, std::ldexp(1.f, w_gu), 1, 0, stream);
+      if (he == hipSuccess)
+        he = launch_convert_rows(sf, L.w_up, df, o.w_gu, (int)F, (int)D, std::ldexp(1.f, w_gu), 1, 1, stream);
+      if (he == hipSuccess)
+        he = launch_convert_rows(sf, L.w_down, df, o.w_d, (int)D, (int)F, std::ldexp(1.f, w_d), 0, 0, stream);
+    }
     if (he == hipSuccess) he = launch_to_f32(sf, L.attn_norm, o.attn_norm, (int)D, std::ldexp(1.f, -ka), stream);
     if (he == hipSuccess) he = launch_to_f32(sf, L.mlp_norm, o.mlp_norm, (int)D, std::ldexp(1.f, -km), stream);
     if (he == hipSuccess && c.qk_norm) he = launch_to_f32(sf, L.q_norm, o.q_norm, (int)d, 1.f, stream);
@@ -390,7 +434,7 @@ hipError_t run_layers(mte_encoder *e, float *h, const std::vector<int32_t> &cu, 
   const mte_config &c = e->cfg;
   const int D = c.hidden, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
   const int nqkv = (Hq + 2 * Hkv) * d;
-  const int mode = e->mode, af = e->act_fmt;
+  const int mode = e->mode, gm = e->gmode, af = e->act_fmt;
   float *ws = e->ws;
   const size_t wn = e->ws_elems;
   // `*pending` counts the partial sums of a K-split residual projection
@@ -408,8 +452,8 @@ hipError_t run_layers(mte_encoder *e, float *h, const std::vector<int32_t> &cu, 
                     (Hq + Hkv) * d, Hq * d, d, c.rms_eps};
     {
       Timer t(e, 0, s);
-      MTE_TRY(launch_gemm(mode, EPI_QKV, e->xn, W.w_qkv, e->qkv, T, nqkv, D, nqkv, W.s_qkv, 1.f, ws, wn,
-                          &sp, &qe, s));
+      MTE_TRY(launch_gemm(gm, EPI_QKV, e->xn, W.w_qkv, e->qkv, T, nqkv, D, nqkv, W.s_qkv, 1.f, ws, wn,
+                          &sp, &qe, s, W.cs_qkv));
     }
     if (sp) MTE_TRY(launch_qkv_parts(e->qkv, ws, sp, T, Hq, Hkv, qe, s));
     {
@@ -424,20 +468,21 @@ hipError_t run_layers(mte_encoder *e, float *h, const std::vector<int32_t> &cu, 
     }
     {
       Timer t(e, 2, s);
-      MTE_TRY(launch_gemm(mode, EPI_RESID, e->attn, W.w_o, h, T, D, Hq * d, D, W.s_o, 1.f, ws, wn, &np,
-                          nullptr, s));
+      MTE_TRY(launch_gemm(gm, EPI_RESID, e->attn, W.w_o, h, T, D, Hq * d, D, W.s_o, 1.f, ws, wn, &np,
+                          nullptr, s, W.cs_o));
     }
     MTE_TRY(launch_rmsnorm(FMT_F32, af, h, np ? h : nullptr, np ? ws : nullptr, np, W.mlp_norm, e->xn, T, D,
                            c.rms_eps, s));
     {
       Timer t(e, 3, s);
-      MTE_TRY(launch_gemm(mode, EPI_SWIGLU, e->xn, W.w_gu, e->act, T, 2 * F, D, F, W.s_gu, W.y_pre, ws, wn,
-                          &sp, nullptr, s));
+      MTE_TRY(launch_gemm(gm, EPI_SWIGLU, e->xn, W.w_gu, e->act, T, 2 * F, D, F, W.s_gu, W.y_pre, ws, wn,
+                          &sp, nullptr, s, W.cs_gu));
     }
     if (sp) MTE_TRY(launch_swiglu_parts(af, ws, sp, T, F, e->act, W.y_pre, s));
     {
       Timer t(e, 4, s);
-      MTE_TRY(launch_gemm(mode, EPI_RESID, e->act, W.w_d, h, T, D, F, D, W.s_d, 1.f, ws, wn, &np, nullptr, s));
+      MTE_TRY(launch_gemm(gm, EPI_RESID, e->act, W.w_d, h, T, D, F, D, W.s_d, 1.f, ws, wn, &np, nullptr, s,
+                          W.cs_d));
     }
   }
 #undef MTE_TRY
@@ -627,6 +672,16 @@ int mte_timing_read(mte_encoder *e, int32_t *launches, double *total_ms) {
   *total_ms = tot;
   e->ev_used = 0;
   return MTE_OK;
+}
+
+int mte_quantize_e4m3_rows(const void *src, int32_t src_dtype, int32_t rows, int32_t cols, uint8_t *codes,
+                           float *scales, hipStream_t stream) {
+  if (!src || !codes || !scales || rows <= 0 || cols <= 0) return MTE_E_INVALID;
+  if (src_dtype != MTE_F32 && src_dtype != MTE_BF16) return MTE_E_INVALID;
+  return launch_quantize_e4m3_rows(in_fmt(src_dtype), src, rows, cols, codes, scales, 0, 0, stream) ==
+                 hipSuccess
+             ? MTE_OK
+             : MTE_E_HIP;
 }
 
 int mte_timing_disable(mte_encoder *e) {

@@ -1,493 +1,10 @@
-// Projection GEMMs of the decoder layer on gfx950 matrix cores.
-//
-// C = A[M, K] * W[N, K]^T, A = activations (row-major, K contiguous),
-// W = weights in nn.Linear layout (row-major, K contiguous).
-//
-// Precision modes:
-//  MODE_F32: A and W fp32, v_mfma_f32_32x32x2_f32.
-//  MODE_F16: A and W fp16, v_mfma_f32_32x32x16_f16, fp32 accumulation. The
-//   weights are bf16 values held as fp16 times a power of two chosen per
-//   matrix so that its largest magnitude lands in [2^14, 2^15): every bf16
-//   value down to 2^-31 of that maximum converts exactly. Activations are
-//   rounded once to fp16 (an 11-bit significand, against bf16's 8) after a
-//   power-of-two pre-scale that a static bound keeps in fp16 range; the
-//   epilogue multiplies the product by the inverse of both scales (`scale`,
-//   exact). One MFMA per fragment at the same dense rate as bf16.
-//
-// Each workgroup (4 or 8 waves, WM x WN) owns a BM x BN output tile; each
-// wave a (BM/WM) x (BN/WN) block of 32x32 MFMA tiles. Eight waves, or two
-// four-wave workgroups per CU, put two waves on every SIMD, so one wave's
-// LDS reads and waits overlap the other's MFMAs. K is walked in stages of 128
-// bytes per row, staged through LDS with double buffering (one barrier per
-// stage): the next stage's global loads are in flight while the current one
-// feeds the MFMAs.
-//
-// LDS rows are 128 bytes = 8 chunks of 16 bytes; chunk c of row r is stored
-// at slot c ^ ((r ^ (r >> 3)) & 7), so the 16-byte fragment reads of 8 or 16
-// consecutive rows at one logical chunk hit distinct banks.
-//
-// Epilogues are fused: fp32 store with the per-head QK-norm and rotary
-// embedding of the q and k heads (QKV projection; a wave's columns cover
-// whole heads, so a head's sum of squares is a reduction over the wave's
-// lanes and both members of each rotary pair sit in one lane), SwiGLU over
-// gate/up rows interleaved in blocks of 16 (MLP up-projection: a 32-column
-// MFMA tile holds 16 gate and the 16 matching up columns, paired by one
-// lane exchange; written in the activation format) and accumulation into
-// the fp32 residual stream (attention output projection and MLP
-// down-projection). With K split over workgroups (small M), each
-// split stores its partial sum instead, and the kernel that consumes the
-// product adds the partials up in split order, so results do not depend on
-// the order in which workgroups finish.
-#include <cmath>
-#include <type_traits>
-
-#include "common.h"
-#include "launch.h"
+// Planning and launch of the projection GEMMs (k_gemm, gemm_kernel.h): a
+// tile configuration and K split per (M, N, K, epilogue), from a table of
+// measured choices for the decoder's projections, else from the number of
+// workgroups a tile yields and its measured steady-state rate.
+#include "gemm_kernel.h"
 
 namespace mte {
-
-struct GemmArgs {
-  const char *A;
-  const char *W;
-  void *C;            // EPI_STORE / EPI_RESID / EPI_PARTIAL: float; EPI_SWIGLU: activation format
-  size_t c_plane;     // EPI_PARTIAL: elements between the partial sums of two K splits
-  int M, N, K, ldc;
-  int k_chunk;        // K range of one split (gridDim.z splits)
-  float scale;        // product multiplier (inverse operand pre-scales)
-  float out_scale;    // EPI_SWIGLU output multiplier
-  QkvEpi qe;          // EPI_QKV
-};
-
-// Chunk swizzles for rows of 128 bytes (8 chunks) and 64 bytes (4 chunks):
-// the 16-byte fragment reads (32 consecutive rows at one logical chunk, the
-// upper half-wave at the next chunk) are free of LDS bank conflicts with
-// these two (measured with SQ_LDS_BANK_CONFLICT on gfx950; e.g. the 64-byte
-// variant c ^ ((r >> 1) & 3) is 2-way conflicted).
-template <int CH>
-__device__ __forceinline__ int swz(int r, int c) {
-  if constexpr (CH == 8) return c ^ ((r ^ (r >> 3)) & 7);
-  else return c ^ ((r >> 2) & 3);
-}
-
-// Waits until at most n vector-memory operations of this wave are pending.
-template <int n>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(n >= 0 && n < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((n & 0xF) | (0x7 << 4) | (0xF << 8) | ((n >> 4) << 14));
-}
-// Waits until at most after*LOADS vector-memory operations are pending,
-// for a wave-uniform after in [0, 3].
-template <int LOADS>
-__device__ __forceinline__ void wait_stages(int after) {
-  if (after >= 3) wait_vm<(3 * LOADS < 64 ? 3 * LOADS : 0)>();
-  else if (after == 2) wait_vm<(2 * LOADS < 64 ? 2 * LOADS : 0)>();
-  else if (after == 1) wait_vm<LOADS>();
-  else wait_vm<0>();
-}
-
-// 16-byte global -> LDS copy without a register round trip: lane i of the
-// wave writes lds_base + 16*i, lds_base wave-uniform. Written as inline asm
-// on purpose: the compiler's waitcnt pass treats the builtin form as LDS
-// traffic and then drains every outstanding LDS read (lgkmcnt(0)) before
-// the MFMAs that follow a stage's loads. The asm form is invisible to that
-// pass; the kernel orders these loads itself with explicit vmcnt waits and
-// barriers, and waits for all of them before it ends.
-// M0 is saved and restored around the load (the compiler reserves it), and
-// one wait state separates the M0 write from the load that reads it.
-__device__ __forceinline__ void dma16(const void *g, uint32_t lds_base) {
-  uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %2\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(g), "s"(lds_base)
-      : "memory");
-}
-
-// EPI_QKV epilogue of one wave: rows mw.. (TM blocks of 32), columns cw..
-// (TN blocks of 32 = whole heads of HD columns). For each row and q or k
-// head: RMS-normalise (sum of squares over the head's HD/32 column blocks
-// and the 32 lanes that hold the row) and rotate pair (c, c + HD/2), i.e.
-// column blocks (jb, jb + HD/64) of one lane. Gains are read once; the
-// rotary table values of a block of 32 rows are read before they are used.
-template <int HD, int TM, int TN>
-__device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const GemmArgs &g, int cw,
-                                             int mw, int lane) {
-  constexpr int HJB = HD / 32;                    // column blocks per head
-  constexpr int NH = TN / HJB;                    // heads of the wave
-  constexpr int NR = NH * HJB / 2;                // rotary blocks per row
-  static_assert(TN % HJB == 0, "whole heads per wave");
-  const QkvEpi &q = g.qe;
-  const int lrow = lane & 31;
-  const int M = g.M;
-  float *C = (float *)g.C;
-  bool rot[NH];
-  float gsc[TN];
-#pragma unroll
-  for (int h = 0; h < NH; ++h) {
-    const int cb = cw + h * HD;
-    rot[h] = cb < q.rot_cols;                     // wave-uniform
-    const float *gn = cb < q.nq_cols ? q.qn : q.kn;
-#pragma unroll
-    for (int jj = 0; jj < HJB; ++jj) gsc[h * HJB + jj] = (rot[h] && gn) ? gn[jj * 32 + lrow] : 1.f;
-  }
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-    float tc[16][NR], ts[16][NR];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = min(mw + i * 32 + acc_row(r, lane), M - 1);
-#pragma unroll
-      for (int x = 0; x < NR; ++x) {
-        const int h = x / (HJB / 2), jj = x % (HJB / 2);
-        tc[r][x] = 1.f;
-        ts[r][x] = 0.f;
-        if (rot[h]) {
-          const size_t o = (size_t)m * (HD / 2) + jj * 32 + lrow;
-          tc[r][x] = q.rcos[o];
-          ts[r][x] = q.rsin[o];
-        }
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = mw + i * 32 + acc_row(r, lane);
-      float v[TN];
-#pragma unroll
-      for (int j = 0; j < TN; ++j) v[j] = acc[i][j][r] * g.scale;
-#pragma unroll
-      for (int h = 0; h < NH; ++h) {
-        if (!rot[h]) continue;
-        if (q.qn) {
-          float ss = 0.f;
-#pragma unroll
-          for (int jj = 0; jj < HJB; ++jj) ss += v[h * HJB + jj] * v[h * HJB + jj];
-#pragma unroll
-          for (int o = 1; o < 32; o <<= 1) ss += __shfl_xor(ss, o, kWave);
-          const float rs = rsqrtf(ss / (float)HD + q.eps);
-#pragma unroll
-          for (int jj = 0; jj < HJB; ++jj) v[h * HJB + jj] = v[h * HJB + jj] * rs * gsc[h * HJB + jj];
-        }
-#pragma unroll
-        for (int jj = 0; jj < HJB / 2; ++jj) {
-          const int j = h * HJB + jj, jp = j + HJB / 2, x = h * (HJB / 2) + jj;
-          const float u = v[j], w = v[jp];
-          v[j] = u * tc[r][x] - w * ts[r][x];
-          v[jp] = w * tc[r][x] + u * ts[r][x];
-        }
-      }
-      if (m < M)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) C[(size_t)m * g.ldc + cw + j * 32 + lrow] = v[j];
-    }
-  }
-}
-
-// The main loop keeps P stages in an LDS ring filled by direct global->LDS
-// loads, and double-buffers the MFMA operand fragments in registers. One
-// barrier per stage, placed before the stage's last k-step: before it each
-// wave waits for its own loads of the next stage; after it (all waves' loads
-// of the next stage are in LDS, and every wave is done with the previous
-// stage) the loads of stage kt+P-1 go into the slot stage kt-1 used, and the
-// first fragments of stage kt+1 are read while the last MFMAs of stage kt
-// run. Raw s_barrier (no fence) keeps the compiler from forcing vmcnt(0) at
-// the barrier; the waits are explicit.
-template <int MODE, int BM, int BN, int WM, int WN, int ROWB, int P, int EPI, int OCC>
-__global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_eu(OCC * WM * WN / 4, OCC * WM * WN / 4))) void k_gemm(GemmArgs g) {
-  typedef typename std::conditional<MODE == MODE_F32, float, f16>::type T;
-  constexpr int KS = ROWB / (int)sizeof(T);       // k elements per stage
-  constexpr int CH = ROWB / 16;                   // 16-byte chunks per row per stage
-  constexpr int WTM = BM / WM, WTN = BN / WN;     // wave tile
-  constexpr int TM = WTM / 32, TN = WTN / 32;     // 32x32 MFMA tiles per wave
-  constexpr int ACH = BM * CH, BCH = BN * CH;     // chunks per stage (A / W)
-  constexpr int NW = WM * WN;                     // waves per workgroup
-  constexpr int NT = 64 * NW;                     // threads per workgroup
-  // DMA rounds: each wave instruction fills one group of 64 chunks. A last,
-  // partial round repeats the matrix's final group in the waves past it
-  // (the same bytes to the same LDS slots), so every wave issues the same
-  // number of loads and the vmcnt waits stay exact.
-  static_assert(ACH % 64 == 0 && BCH % 64 == 0, "whole 64-chunk groups");
-  constexpr int AG = ACH / 64, BG = BCH / 64;     // chunk groups per stage
-  constexpr int AR = (AG + NW - 1) / NW, BR = (BG + NW - 1) / NW;   // DMA instructions per thread
-  constexpr int LOADS = AR + BR;                  // per thread per stage
-  constexpr int STAGE = (BM + BN) * CH;           // u32x4 slots per stage
-  static_assert(NW == 4 || NW == 8, "4 or 8 waves");
-  static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
-  static_assert(LOADS * (P - 2) < 64 && P >= 3 && P <= 6, "vmcnt range, ring depth");
-  typedef typename Frag<T>::type frag_t;
-
-  extern __shared__ u32x4 lds[];                  // [P][STAGE]
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
-  const int M = g.M;
-  const size_t rowb = (size_t)g.K * sizeof(T);    // row pitch in bytes (A and W)
-  const size_t kb0 = (size_t)blockIdx.z * g.k_chunk * sizeof(T);
-  const int nk = g.k_chunk / KS;
-
-  // DMA sources: instruction c of this thread fills LDS slot q = (c*NW + wave)*64 + lane
-  // of its matrix (row q / CH, swizzled slot q % CH, logical chunk slot ^ f(row)).
-  const char *pa[AR];
-  const char *pb[BR];
-#pragma unroll
-  for (int c = 0; c < AR; ++c) {
-    const int q = min(c * NW + wave, AG - 1) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
-    pa[c] = g.A + (size_t)min(m0 + r, M - 1) * rowb + kb0 + ch * 16;
-  }
-#pragma unroll
-  for (int c = 0; c < BR; ++c) {
-    const int q = min(c * NW + wave, BG - 1) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
-    pb[c] = g.W + (size_t)(n0 + r) * rowb + kb0 + ch * 16;
-  }
-  const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
-  const int uwave = __builtin_amdgcn_readfirstlane(wave);   // wave-uniform in an SGPR
-  // DMA load x (0 <= x < LOADS) of K-stage `ks` into ring slot `slot`.
-  auto dma_one = [&](int ks, int slot, int x) {
-    const uint32_t st = lds0 + (uint32_t)(slot * STAGE) * 16u;
-    const size_t ko = (size_t)ks * ROWB;
-    if (x < AR) {
-      dma16(pa[x] + ko, st + (uint32_t)(min(x * NW + uwave, AG - 1) * 64) * 16u);
-    } else {
-      const int c = x - AR;
-      dma16(pb[c] + ko, st + (uint32_t)(ACH + min(c * NW + uwave, BG - 1) * 64) * 16u);
-    }
-  };
-
-  f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-  frag_t fa[2][TM], fb[2][TN];
-  const int lrow = lane & 31, lgrp = lane >> 5;
-  // Fragment read x (0 <= x < NR) of k-step kk of the stage at `st` into
-  // buffer b, in the order the MFMAs consume them: the W fragments, then the
-  // A fragments.
-  auto read_one = [&](const u32x4 *st, int kk, int b, int x) {
-    const int ch = kk * 2 + lgrp;
-    if (x < TN) {
-      const int r = wn * WTN + x * 32 + lrow;
-      fb[b][x] = __builtin_bit_cast(frag_t, st[ACH + r * CH + swz<CH>(r, ch)]);
-    } else {
-      const int i = x - TN;
-      const int r = wm * WTM + i * 32 + lrow;
-      fa[b][i] = __builtin_bit_cast(frag_t, st[r * CH + swz<CH>(r, ch)]);
-    }
-  };
-  auto mfma_one = [&](int b, int x) {
-    const int j = x % TN, i = x / TN;
-    mfma32(acc[i][j], fa[b][i], fb[b][j]);
-  };
-  constexpr int KK = CH / 2;                      // 16-k steps per stage (even)
-  static_assert(KK % 2 == 0, "fragment buffer parity");
-  constexpr int NM = TM * TN;                     // MFMAs per k-step
-  constexpr int NR = TM + TN;                     // fragment reads per k-step
-  // The loads of one stage are issued in NPART parts: part 0 right after the
-  // barrier of stage kt-P+1, parts 1.. in the k-steps before the barrier of
-  // stage kt-P+2. With P >= 4 every stage still has P-3 whole stages of loads
-  // in flight behind it at the barrier that waits for it; P = 3 issues each
-  // stage whole, after the barrier.
-  constexpr int NPART = (P >= 4) ? KK : 1;
-  constexpr int PART = (LOADS + NPART - 1) / NPART;
-
-  // One k-step: the NM MFMAs on fragment buffer `cur`, with the side work
-  // spread between them in issue order -- the NR fragment reads of the next
-  // k-step (k-step rkk of the stage at rst, into buffer cur^1), then DMA
-  // loads [d0, d1) of stage ks into slot `slot`. With `bar`, the barrier of
-  // the stage (after this wave's loads of the next stage have landed) goes
-  // after the first MFMA, ahead of all side work.
-  // Each unit of side work is pinned behind its MFMA by a scheduling
-  // barrier, so the matrix core keeps busy while it issues.
-  auto kstep = [&](int cur, const u32x4 *rst, int rkk, int ks, int slot, int d0, int d1, bool bar) {
-    const int nside = NR + (d1 - d0);
-#pragma unroll
-    for (int m = 0; m < NM; ++m) {
-      mfma_one(cur, m);
-      if (bar && m == 0) {
-        wait_vm<(P - 3) * LOADS>();        // this wave's loads of the next stage landed
-        __builtin_amdgcn_s_barrier();      // ... everyone's, and the previous stage is free
-        asm volatile("" ::: "memory");     // keep LDS reads of the next stage below it
-      }
-      const int s0 = (m * nside + NM - 1) / NM, s1 = ((m + 1) * nside + NM - 1) / NM;
-#pragma unroll
-      for (int x = s0; x < s1; ++x) {
-        if (x < NR) read_one(rst, rkk, cur ^ 1, x);
-        else dma_one(ks, slot, d0 + x - NR);
-      }
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  };
-
-  // The loop body is branch-free (a branch between LDS reads and their
-  // use makes the waitcnt pass drain all outstanding reads): every iteration
-  // issues its loads -- past the end, repeats of the last stage into slots
-  // that are never read again -- so every wait is a fixed vmcnt.
-  // Prologue: stages 0..P-3 whole and part 0 of stage P-2 (P = 3: stages
-  // 0..P-2 whole), then stage 0 must have landed.
-  constexpr int PRE_FULL = (NPART > 1) ? P - 2 : P - 1;
-  constexpr int PRE_PART = (NPART > 1) ? (PART < LOADS ? PART : LOADS) : 0;
-#pragma unroll
-  for (int s = 0; s < PRE_FULL; ++s)
-#pragma unroll
-    for (int x = 0; x < LOADS; ++x) dma_one(min(s, nk - 1), s, x);
-#pragma unroll
-  for (int x = 0; x < PRE_PART; ++x) dma_one(min(P - 2, nk - 1), P - 2, x);
-  wait_vm<(PRE_FULL - 1) * LOADS + PRE_PART>();
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-#pragma unroll
-  for (int x = 0; x < NR; ++x) read_one(lds, 0, 0, x);
-  for (int kt = 0; kt < nk; ++kt) {
-    const u32x4 *st = lds + (kt % P) * STAGE;
-    const u32x4 *nx = lds + ((kt + 1) % P) * STAGE;
-    const int ksa = min(kt + P - 2, nk - 1), sla = (kt + P - 2) % P;   // parts 1.. issued here
-    const int ksb = min(kt + P - 1, nk - 1), slb = (kt + P - 1) % P;   // part 0 issued here
-#pragma unroll
-    for (int kk = 0; kk < KK; ++kk) {
-      const int cur = kk & 1;
-      if (kk + 1 < KK) {
-        const int q = kk + 1;                       // DMA part of this k-step
-        const int d0 = (NPART > 1) ? min(q * PART, LOADS) : 0;
-        const int d1 = (NPART > 1) ? min((q + 1) * PART, LOADS) : 0;
-        kstep(cur, st, kk + 1, ksa, sla, d0, d1, false);
-      } else {
-        const int d1 = (NPART > 1) ? min(PART, LOADS) : LOADS;
-        kstep(cur, nx, 0, ksb, slb, 0, d1, true);
-      }
-    }
-  }
-  wait_vm<0>();                          // no load may land after the workgroup ends
-
-  // Epilogue.
-  if constexpr (EPI == EPI_QKV) {
-    const int cw = n0 + wn * WTN;
-    // (the host only launches tiles whose waves cover whole heads)
-    if (g.qe.hd == 128) {
-      if constexpr (TN % 4 == 0) qkv_epilogue<128, TM, TN>(acc, g, cw, m0 + wm * WTM, lane);
-    } else {
-      if constexpr (TN % 2 == 0) qkv_epilogue<64, TM, TN>(acc, g, cw, m0 + wm * WTM, lane);
-    }
-    return;
-  }
-  if constexpr (EPI == EPI_SWIGLU) {
-    // Column block j (32 columns) of the interleaved product holds gate
-    // (lanes l%32 < 16) and up (l%32 >= 16) of outputs f = 16*block + l%16.
-    // Of each pair of accumulator rows (r, r+1) the gate lane finishes row r
-    // and the up lane row r+1, each receiving the value it lacks from lane
-    // l ^ 16 (exchanged by all lanes together, outside any row test).
-    const bool upl = lrow >= 16;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int f = ((n0 + wn * WTN + j * 32) >> 1) + (lrow & 15);
-#pragma unroll
-        for (int r = 0; r < 16; r += 2) {
-          const float a0 = acc[i][j][r] * g.scale, a1 = acc[i][j][r + 1] * g.scale;
-          const float recv = __shfl_xor(upl ? a0 : a1, 16, kWave);
-          const float gt = upl ? recv : a0, up = upl ? a1 : recv;
-          const int m = m0 + wm * WTM + i * 32 + acc_row(r + (upl ? 1 : 0), lane);
-          const float y = gt / (1.f + __expf(-gt)) * up * g.out_scale;
-          if (m < M) {
-            const size_t o = (size_t)m * g.ldc + f;
-            if constexpr (MODE == MODE_F32) ((float *)g.C)[o] = y;
-            else ((f16 *)g.C)[o] = (f16)y;
-          }
-        }
-      }
-    }
-    return;
-  }
-#pragma unroll
-  for (int i = 0; i < TM; ++i) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = m0 + wm * WTM + i * 32 + acc_row(r, lane);
-      if (m >= M) continue;
-      float *C = (float *)g.C + (EPI == EPI_PARTIAL ? (size_t)blockIdx.z * g.c_plane : 0);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const size_t o = (size_t)m * g.ldc + n0 + wn * WTN + j * 32 + lrow;
-        if constexpr (EPI == EPI_RESID) C[o] += acc[i][j][r] * g.scale;
-        else C[o] = acc[i][j][r] * g.scale;
-      }
-    }
-  }
-}
-
-
-// ------------------------------------------------------------- planning
-// A tile configuration is a compile-time instantiation; the planner picks
-// one per (M, N, K, epilogue): from a table of measured choices for the
-// decoder's projections, else from the number of workgroups a tile yields
-// and its measured steady-state rate.
-struct TileCfg {
-  int bm, bn, wm, wn, rowb, occ, f32;
-};
-
-template <int MODE, int BM, int BN, int WM, int WN, int ROWB, int P, int EPI, int OCC, int F32>
-static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
-  if constexpr (EPI == EPI_QKV && (BN / WN) % 64 != 0) {
-    return hipErrorInvalidValue;  // the QK-norm epilogue needs whole heads per wave
-  } else if constexpr (MODE == MODE_F32 && !F32) {
-    return hipErrorInvalidValue;  // fp32 operands are built for a few tiles only
-  } else {
-    constexpr int lds_bytes = P * (BM + BN) * ROWB;
-    auto kern = k_gemm<MODE, BM, BN, WM, WN, ROWB, P, EPI, OCC>;
-    static const hipError_t attr = hipFuncSetAttribute(
-        (const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, lds_bytes);
-    if (attr != hipSuccess) return attr;
-    dim3 grid(a.N / BN, (a.M + BM - 1) / BM, splits);
-    hipLaunchKernelGGL(kern, grid, dim3(64 * WM * WN), lds_bytes, s, a);
-    return hipGetLastError();
-  }
-}
-
-// Tile table: id -> instantiation (bm, bn, wave layout wm x wn, bytes of K
-// per row per stage, LDS ring stages, workgroups per CU, built for fp32
-// operands too). The LDS ring (P * (bm + bn) * rowb bytes) must fit
-// 160 KB / occ; bm * rowb / 16 and bn * rowb / 16 must be multiples of 64
-// (whole 64-chunk DMA groups).
-#define MTE_TILE_TABLE(X)                    \
-  X(0, 256, 256, 2, 2, 64, 4, 1, 0)          \
-  X(1, 256, 192, 2, 2, 64, 4, 1, 0)          \
-  X(2, 192, 256, 2, 2, 64, 4, 1, 0)          \
-  X(3, 192, 192, 2, 2, 64, 5, 1, 0)          \
-  X(4, 192, 192, 2, 2, 128, 3, 1, 0)         \
-  X(5, 256, 128, 2, 2, 128, 3, 1, 0)         \
-  X(6, 256, 128, 2, 2, 64, 6, 1, 0)          \
-  X(7, 128, 256, 2, 2, 64, 6, 1, 0)          \
-  X(8, 192, 128, 2, 2, 128, 3, 1, 0)         \
-  X(9, 128, 128, 2, 2, 128, 4, 1, 1)         \
-  X(10, 128, 128, 2, 2, 64, 4, 2, 0)         \
-  X(11, 256, 128, 4, 1, 64, 6, 1, 0)         \
-  X(12, 128, 128, 4, 1, 128, 4, 1, 1)        \
-  X(13, 128, 64, 4, 1, 64, 4, 2, 1)          \
-  X(14, 96, 128, 1, 4, 128, 4, 1, 0)         \
-  X(15, 64, 256, 1, 4, 128, 3, 1, 0)         \
-  X(16, 64, 128, 2, 2, 64, 4, 2, 1)          \
-  X(17, 32, 256, 1, 4, 128, 3, 1, 1)         \
-  X(18, 192, 64, 2, 2, 128, 4, 1, 0)         \
-  X(19, 96, 256, 1, 4, 128, 3, 1, 0)         \
-  X(20, 192, 192, 2, 2, 64, 3, 2, 0)         \
-  X(21, 256, 128, 2, 2, 64, 3, 2, 0)         \
-  X(22, 128, 256, 2, 2, 64, 3, 2, 0)         \
-  X(23, 128, 128, 4, 1, 64, 4, 2, 0)         \
-  X(24, 256, 128, 4, 1, 64, 3, 2, 0)         \
-  X(25, 192, 128, 2, 2, 64, 3, 2, 0)         \
-  X(26, 256, 256, 2, 4, 64, 4, 1, 0)         \
-  X(27, 256, 256, 4, 2, 64, 4, 1, 0)         \
-  X(28, 256, 128, 4, 2, 64, 6, 1, 0)         \
-  X(29, 128, 256, 2, 4, 64, 6, 1, 0)         \
-  X(30, 128, 128, 2, 4, 128, 4, 1, 0)         \
-  X(31, 384, 192, 4, 2, 64, 4, 1, 0)         \
-  X(32, 192, 384, 2, 4, 64, 4, 1, 0)
 
 static const TileCfg kTiles[] = {
 #define MTE_TILE_INFO(id, bm, bn, wm, wn, rowb, p, occ, f32) {bm, bn, wm, wn, rowb, occ, f32},
@@ -498,22 +15,11 @@ constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
 int gemm_num_tiles() { return kNumTiles; }
 
-template <int MODE, int EPI>
-static hipError_t run_id(int id, const GemmArgs &a, int splits, hipStream_t s) {
-  switch (id) {
-#define MTE_TILE_CASE(idv, bm, bn, wm, wn, rowb, p, occ, f32) \
-  case idv: return run<MODE, bm, bn, wm, wn, rowb, p, EPI, occ, f32>(a, splits, s);
-    MTE_TILE_TABLE(MTE_TILE_CASE)
-#undef MTE_TILE_CASE
-  }
-  return hipErrorInvalidValue;
-}
-
-// col_align: columns a wave must cover in whole units (heads for the QKV
 // epilogue; gate/up pairs sit inside every 32-column block).
-static bool tile_fits(int id, int N, int K, int esz, int epi, int splits, int col_align = 32) {
+static bool tile_fits(int id, int N, int K, int esz, int epi, int splits, int col_align = 32,
+                      bool w8 = false) {
   const TileCfg &t = kTiles[id];
-  if (N % t.bn || (esz == 4 && !t.f32)) return false;
+  if (N % t.bn || (esz == 4 && !t.f32) || (w8 && t.rowb != 128)) return false;
   const int ks = t.rowb / esz;
   if (K % splits || (K / splits) % ks) return false;
   if (epi == EPI_QKV && (t.bn / t.wn) % col_align) return false;
@@ -553,13 +59,20 @@ static const TileChoice kChoices[] = {
     {4096, 2048, EPI_QKV, 10240, 27, 1},  {2048, 2048, EPI_RESID, 10240, 2, 1},
     {12288, 2048, EPI_SWIGLU, 10240, 26, 1}, {2048, 6144, EPI_RESID, 10240, 12, 1},
 };
+// The same for e4m3 weights (tiles staging 128 bytes of A per row).
+static const TileChoice kChoicesW8[] = {
+    {4096, 2048, EPI_QKV, 96, 12, 4},     {2048, 2048, EPI_RESID, 96, 30, 4},
+    {12288, 2048, EPI_SWIGLU, 96, 12, 2},  {2048, 6144, EPI_RESID, 96, 18, 8},
+    {4096, 2048, EPI_QKV, 192, 18, 4},    {2048, 2048, EPI_RESID, 192, 14, 4},
+    {12288, 2048, EPI_SWIGLU, 192, 14, 1}, {2048, 6144, EPI_RESID, 192, 14, 8},
+};
 
 // Fallback estimate: rounds of workgroups over the compute units x the time
 // one full round takes at the tile's measured rate. Split-K is only
 // considered up to 2048 rows (2 splits above 256), and only where the
 // partial sums fit `ws_elems`.
 static void plan_model(int M, int N, int K, int esz, int epi, int col_align, size_t ws_elems,
-                       int *tile, int *splits) {
+                       bool w8, int *tile, int *splits) {
   const int cus = 256;
   double best = 1e30;
   *tile = -1;
@@ -567,7 +80,7 @@ static void plan_model(int M, int N, int K, int esz, int epi, int col_align, siz
   for (int id = 0; id < kNumTiles; ++id) {
     for (int sp = 1; sp <= 8; sp *= 2) {
       if (sp > 1 && (M > 2048 || (M > 256 && sp > 2) || (size_t)sp * M * N > ws_elems)) continue;
-      if (!tile_fits(id, N, K, esz, sp > 1 ? EPI_PARTIAL : epi, sp, col_align)) continue;
+      if (!tile_fits(id, N, K, esz, sp > 1 ? EPI_PARTIAL : epi, sp, col_align, w8)) continue;
       const TileCfg &t = kTiles[id];
       const double tiles = (double)(N / t.bn) * ((M + t.bm - 1) / t.bm) * sp;
       const double slots = (double)cus * t.occ;
@@ -583,71 +96,68 @@ static void plan_model(int M, int N, int K, int esz, int epi, int col_align, siz
   }
 }
 
-static void plan(int M, int N, int K, int esz, int epi, int col_align, size_t ws_elems, int *tile,
-                 int *splits) {
+static void plan(int M, int N, int K, int esz, int epi, int col_align, size_t ws_elems, bool w8,
+                 int *tile, int *splits) {
   const TileChoice *best = nullptr;
   double bd = 1e30;
   if (esz == 2) {
-    for (const TileChoice &c : kChoices) {
+    const TileChoice *tab = w8 ? kChoicesW8 : kChoices;
+    const size_t ntab = w8 ? sizeof(kChoicesW8) / sizeof(kChoicesW8[0]) : sizeof(kChoices) / sizeof(kChoices[0]);
+    for (size_t ci = 0; ci < ntab; ++ci) {
+      const TileChoice &c = tab[ci];
       if (c.n != N || c.k != K || c.epi != epi) continue;
       const double d = std::fabs(std::log((double)M / c.m));
       if (d < bd) { bd = d; best = &c; }
     }
   }
   if (best &&
-      tile_fits(best->tile, N, K, esz, best->splits > 1 ? EPI_PARTIAL : epi, best->splits, col_align) &&
+      tile_fits(best->tile, N, K, esz, best->splits > 1 ? EPI_PARTIAL : epi, best->splits, col_align, w8) &&
       (best->splits == 1 ||
        ((M <= 256 || (M <= 2048 && best->splits == 2)) && (size_t)best->splits * M * N <= ws_elems))) {
     *tile = best->tile;
     *splits = best->splits;
     return;
   }
-  plan_model(M, N, K, esz, epi, col_align, ws_elems, tile, splits);
+  plan_model(M, N, K, esz, epi, col_align, ws_elems, w8, tile, splits);
 }
 
-template <int MODE>
-static hipError_t launch_mode(int epi, int tile, int splits, const GemmArgs &a, hipStream_t s) {
-  switch (epi) {
-    case EPI_STORE: return run_id<MODE, EPI_STORE>(tile, a, splits, s);
-    case EPI_SWIGLU: return run_id<MODE, EPI_SWIGLU>(tile, a, splits, s);
-    case EPI_RESID: return run_id<MODE, EPI_RESID>(tile, a, splits, s);
-    case EPI_QKV: return run_id<MODE, EPI_QKV>(tile, a, splits, s);
-    default: return run_id<MODE, EPI_PARTIAL>(tile, a, splits, s);
-  }
-}
+hipError_t launch_mode_f8w(int epi, int tile, int splits, const GemmArgs &a, hipStream_t s);
 
 hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void *A, const void *W,
                             void *C, size_t c_plane, int M, int N, int K, int ldc, float scale,
-                            float out_scale, const QkvEpi *qe, hipStream_t s) {
+                            float out_scale, const QkvEpi *qe, hipStream_t s, const float *col_scale) {
   if (M <= 0) return hipSuccess;
-  const int esz = mode == MODE_F16 ? 2 : 4;
+  const bool w8 = mode == MODE_F8W;
+  const int esz = mode == MODE_F32 ? 4 : 2;
   if (epi == EPI_QKV && (!qe || (qe->hd != 64 && qe->hd != 128))) return hipErrorInvalidValue;
+  if (w8 && !col_scale) return hipErrorInvalidValue;
   if (tile < 0 || tile >= kNumTiles || splits < 1 ||
-      !tile_fits(tile, N, K, esz, epi, splits, epi == EPI_QKV ? qe->hd : 32) ||
+      !tile_fits(tile, N, K, esz, epi, splits, epi == EPI_QKV ? qe->hd : 32, w8) ||
       (splits > 1 && epi != EPI_PARTIAL))
     return hipErrorInvalidValue;
   GemmArgs a{(const char *)A, (const char *)W, C, c_plane, M, N, K, ldc, K / splits, scale, out_scale,
-             epi == EPI_QKV ? *qe : QkvEpi{}};
+             epi == EPI_QKV ? *qe : QkvEpi{}, w8 ? col_scale : nullptr};
+  if (w8) return launch_mode_f8w(epi, tile, splits, a, s);
   return mode == MODE_F16 ? launch_mode<MODE_F16>(epi, tile, splits, a, s)
                           : launch_mode<MODE_F32>(epi, tile, splits, a, s);
 }
 
 hipError_t launch_gemm(int mode, int epi, const void *A, const void *W, void *C, int M, int N, int K,
                        int ldc, float scale, float out_scale, float *ws, size_t ws_elems,
-                       int *splits_out, const QkvEpi *qe, hipStream_t s) {
+                       int *splits_out, const QkvEpi *qe, hipStream_t s, const float *col_scale) {
   *splits_out = 0;
   if (M <= 0) return hipSuccess;
   if (epi == EPI_QKV && !qe) return hipErrorInvalidValue;
   int tile, splits;
-  plan(M, N, K, mode == MODE_F16 ? 2 : 4, epi, epi == EPI_QKV ? qe->hd : 32, ws ? ws_elems : 0, &tile,
-       &splits);
+  plan(M, N, K, mode == MODE_F32 ? 4 : 2, epi, epi == EPI_QKV ? qe->hd : 32, ws ? ws_elems : 0,
+       mode == MODE_F8W, &tile, &splits);
   if (tile < 0) return hipErrorInvalidValue;
   if (splits > 1) {
     *splits_out = splits;
     return launch_gemm_tile(mode, EPI_PARTIAL, tile, splits, A, W, ws, (size_t)M * N, M, N, K, N, scale,
-                            1.f, nullptr, s);
+                            1.f, nullptr, s, col_scale);
   }
-  return launch_gemm_tile(mode, epi, tile, 1, A, W, C, 0, M, N, K, ldc, scale, out_scale, qe, s);
+  return launch_gemm_tile(mode, epi, tile, 1, A, W, C, 0, M, N, K, ldc, scale, out_scale, qe, s, col_scale);
 }
 
 }  // namespace mte

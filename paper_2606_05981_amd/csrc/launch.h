@@ -14,6 +14,8 @@ enum Mode {
                  // power-of-two scaled fp16, activations rounded once to fp16), fp32
                  // accumulate; attention: fp32 q/k/v/P split into bf16 hi + lo, three
                  // bf16 MFMAs per product; attention output rounded to fp16
+  MODE_F8W = 2,  // projections only: fp16 activations as MODE_F16, weights OCP e4m3 codes
+                 // with a power-of-two scale per weight row, widened to fp16 for the MFMAs
 };
 
 // Storage formats of activation buffers.
@@ -56,9 +58,13 @@ struct QkvEpi {
 // columns). Otherwise *splits_out = 0 and C holds the result.
 // qe: the EPI_QKV parameters (else ignored, may be null). With a K split,
 // EPI_QKV's normalisation and rotation are left to the consumer as well.
+// MODE_F8W: W holds e4m3 codes [N, K] and col_scale [N] the scale of each
+// weight row (column of the product), applied before `scale` and the
+// epilogue; col_scale is ignored in the other modes.
 hipError_t launch_gemm(int mode, int epi, const void *A, const void *W, void *C, int M, int N, int K,
                        int ldc, float scale, float out_scale, float *ws, size_t ws_elems,
-                       int *splits_out, const QkvEpi *qe, hipStream_t s);
+                       int *splits_out, const QkvEpi *qe, hipStream_t s,
+                       const float *col_scale = nullptr);
 
 // The same with an explicit tile configuration (index into the GEMM tile
 // table) and number of K splits (> 1 only with EPI_PARTIAL, partial sums
@@ -66,7 +72,8 @@ hipError_t launch_gemm(int mode, int epi, const void *A, const void *W, void *C,
 // the tile does not fit the shape.
 hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void *A, const void *W,
                             void *C, size_t c_plane, int M, int N, int K, int ldc, float scale,
-                            float out_scale, const QkvEpi *qe, hipStream_t s);
+                            float out_scale, const QkvEpi *qe, hipStream_t s,
+                            const float *col_scale = nullptr);
 int gemm_num_tiles();
 
 // Per-row RMSNorm: out[r, :] = x[r, :] / sqrt(mean(x[r,:]^2) + eps) * g with
@@ -138,5 +145,15 @@ hipError_t launch_matrix_stats(int src_fmt, const void *src, int rows, int cols,
 // 32*(f/16) + f%16, up row f to 32*(f/16) + 16 + f%16, `up` selecting which).
 hipError_t launch_convert_rows(int src_fmt, const void *src, int dst_fmt, void *dst, int rows, int cols,
                                float scale, int interleave, int up, hipStream_t s);
+
+// OCP e4m3 quantisation of the rows of a [rows, cols] matrix (format src_fmt,
+// FMT_F32 or FMT_BF16): row r gets the scale 2^e_r with e_r the smallest
+// integer such that max_c |src[r, c]| <= 448 * 2^e_r (e_r = 0 for an
+// all-zero row), and code(src[r, c] / 2^e_r) per element, rounded to
+// nearest, ties to even (the division is exact), zero as +0. Source row r
+// goes to destination row map(r) of codes (cols bytes per row) and scales,
+// map as in launch_convert_rows (interleave / up).
+hipError_t launch_quantize_e4m3_rows(int src_fmt, const void *src, int rows, int cols, uint8_t *codes,
+                                     float *scales, int interleave, int up, hipStream_t s);
 
 }  // namespace mte

@@ -473,4 +473,66 @@ hipError_t launch_convert_rows(int src_fmt, const void *src, int dst_fmt, void *
   return hipGetLastError();
 }
 
+// OCP e4m3 code of x, |x| <= 448, rounded to nearest with ties to even.
+// Below 2^-6 the codes are subnormal with quantum 2^-9; binade [2^E, 2^(E+1))
+// above has quantum 2^(E-3). A significand that rounds up to 16 carries into
+// the exponent field through the code arithmetic itself, and 2^-6 (count 8
+// of the subnormal quantum) is the first normal code. Zero is +0.
+__device__ __forceinline__ uint32_t e4m3_code(float x) {
+  const float a = fabsf(x);
+  uint32_t mag;
+  if (a < 0.015625f) {
+    mag = (uint32_t)rintf(a * 512.f);                                 // exact scaling, 0..8
+  } else {
+    const int E = (int)((__float_as_uint(a) >> 23) & 0xFF) - 127;     // 2^-6 <= a <= 448: normal
+    mag = (uint32_t)((E + 7) * 8) + (uint32_t)rintf(ldexpf(a, 3 - E)) - 8u;   // count 8..16
+  }
+  return mag == 0 ? 0u : (mag | (x < 0.f ? 0x80u : 0u));
+}
+
+// One workgroup per source row: the row's max |x| fixes its scale 2^e
+// (smallest e with max <= 448 * 2^e, frexp: max = f * 2^E2, f in [0.5, 1),
+// 448 = 0.875 * 2^9), then every element is coded after the exact division.
+template <typename TS>
+__global__ __launch_bounds__(256) void k_quantize_e4m3_rows(const TS *__restrict__ src, int cols,
+                                                            uint8_t *__restrict__ codes,
+                                                            float *__restrict__ scales, int interleave,
+                                                            int up) {
+  __shared__ float rmax[4];
+  const int r = blockIdx.x;
+  const int dr = interleave ? 32 * (r >> 4) + 16 * up + (r & 15) : r;
+  const TS *s = src + (size_t)r * cols;
+  float mx = 0.f;
+  for (int c = threadIdx.x; c < cols; c += 256) mx = fmaxf(mx, fabsf(to_f32(s[c])));
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) mx = warp_max_xor(mx, m);
+  if ((threadIdx.x & 63) == 0) rmax[threadIdx.x >> 6] = mx;
+  __syncthreads();
+  const float amax = fmaxf(fmaxf(rmax[0], rmax[1]), fmaxf(rmax[2], rmax[3]));
+  int e = 0;
+  if (amax > 0.f) {
+    int E2 = 0;
+    const float f = frexpf(amax, &E2);
+    e = f <= 0.875f ? E2 - 9 : E2 - 8;
+  }
+  uint8_t *d = codes + (size_t)dr * cols;
+  for (int c = threadIdx.x; c < cols; c += 256) d[c] = (uint8_t)e4m3_code(ldexpf(to_f32(s[c]), -e));
+  if (threadIdx.x == 0) scales[dr] = ldexpf(1.f, e);
+}
+
+hipError_t launch_quantize_e4m3_rows(int src_fmt, const void *src, int rows, int cols, uint8_t *codes,
+                                     float *scales, int interleave, int up, hipStream_t s) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  if (interleave && rows % 16) return hipErrorInvalidValue;
+  if (src_fmt == FMT_BF16)
+    hipLaunchKernelGGL(k_quantize_e4m3_rows<bf16>, dim3(rows), dim3(256), 0, s, (const bf16 *)src, cols, codes,
+                       scales, interleave, up);
+  else if (src_fmt == FMT_F32)
+    hipLaunchKernelGGL(k_quantize_e4m3_rows<float>, dim3(rows), dim3(256), 0, s, (const float *)src, cols,
+                       codes, scales, interleave, up);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 }  // namespace mte

@@ -119,3 +119,16 @@ def build_positions(layouts: Sequence[Sequence[int]], device="cuda",
     pos = torch.empty((3, T), dtype=torch.int32, device=device)
     B.mte_build_positions(layouts, pos.data_ptr(), _stream(stream))
     return pos
+
+
+def quantize_e4m3_rows(w: torch.Tensor, stream: Optional[torch.cuda.Stream] = None):
+    """OCP e4m3 codes and power-of-two row scales of a [rows, cols] bf16 / fp32
+    device matrix (mte_quantize_e4m3_rows) -> (uint8 [rows, cols], float32 [rows])."""
+    if w.dim() != 2 or not w.is_cuda or not w.is_contiguous() or w.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("w must be a contiguous 2-D bf16 or fp32 tensor on the GPU")
+    rows, cols = w.shape
+    codes = torch.empty((rows, cols), dtype=torch.uint8, device=w.device)
+    scales = torch.empty((rows,), dtype=torch.float32, device=w.device)
+    B.mte_quantize_e4m3_rows(w.data_ptr(), B.MTE_BF16 if w.dtype == torch.bfloat16 else B.MTE_F32, rows, cols,
+                             codes.data_ptr(), scales.data_ptr(), _stream(stream))
+    return codes, scales

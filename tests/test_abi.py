@@ -18,7 +18,7 @@ def B():
 def _declared_functions():
     src = open(os.path.join(ROOT, "include", "mte.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\**\s*(mte_[a-z_]+)\s*\(", src, flags=re.M)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\**\s*(mte_[a-z0-9_]+)\s*\(", src, flags=re.M)
     return sorted(set(names))
 
 
@@ -26,7 +26,7 @@ def test_header_declares_the_boundary():
     names = _declared_functions()
     for n in ("mte_encoder_create", "mte_encode", "mte_build_positions", "mte_encoder_destroy",
               "mte_status_string", "mte_config_validate", "mte_check_batch", "mte_encode_layers",
-              "mte_encoder_reserve_prefix", "mte_encode_prefixed"):
+              "mte_encoder_reserve_prefix", "mte_encode_prefixed", "mte_quantize_e4m3_rows"):
         assert n in names
 
 
@@ -62,6 +62,8 @@ def test_valid_configs(B):
     (dict(hidden=2000), -5), (dict(ffn=6000), -5),
     (dict(n_q_heads=12, n_kv_heads=4), -5),          # group of 3 query heads
     (dict(max_tokens=1 << 24), -5),
+    (dict(weight_format=2), -1), (dict(weight_format=-1), -1),
+    (dict(weight_format=1, dtype=0), -5),           # e4m3 weights need bf16 storage
 ])
 def test_invalid_configs(B, kw, status):
     assert B.mte_config_validate(_full(B, **kw)) == status
@@ -125,6 +127,21 @@ def test_build_positions_rejects_null(B):
     assert B.lib.mte_build_positions(None, 1, 4096, None) == -1
     assert B.lib.mte_build_positions(arr, 1, None, None) == -1
     assert B.lib.mte_build_positions(arr, 0, 4096, None) == -1
+
+
+def test_e4m3_config_valid(B):
+    assert B.mte_config_validate(_full(B, weight_format=B.MTE_WEIGHTS_E4M3)) == 0
+    assert ctypes.sizeof(B.mte_config) == 4 * 19   # 19 four-byte fields, as in mte.h
+
+
+def test_quantize_rejects_bad_arguments(B):
+    q = B.lib.mte_quantize_e4m3_rows
+    assert q(None, 1, 4, 4, 4096, 8192, None) == -1       # null source
+    assert q(4096, 1, 4, 4, None, 8192, None) == -1       # null codes
+    assert q(4096, 1, 4, 4, 4096, None, None) == -1       # null scales
+    assert q(4096, 1, 0, 4, 4096, 8192, None) == -1       # no rows
+    assert q(4096, 1, 4, -1, 4096, 8192, None) == -1      # no columns
+    assert q(4096, 5, 4, 4, 4096, 8192, None) == -1       # bad dtype
 
 
 def test_status_strings(B):
