@@ -65,7 +65,7 @@ def step_flops(dims, lens):
     return dims.n_layers * (g + att)
 
 
-def run_workload(torch, name, steps, warmup, timing_class=None, use_graph=True):
+def run_workload(torch, name, steps, warmup, timing_class=None, use_graph=True, weight_format=0):
     from paper_2606_05981_amd import binding as B
     from paper_2606_05981_amd.encoder import TextEncoder, build_positions
     from synth import workloads as W
@@ -78,7 +78,7 @@ def run_workload(torch, name, steps, warmup, timing_class=None, use_graph=True):
                         dims.head_dim, dims.ffn, rms_eps=dims.rms_eps, rope_theta=dims.rope_theta,
                         mrope_section=dims.mrope_section, mrope_layout=dims.mrope_layout,
                         qk_norm=dims.qk_norm, dtype=B.MTE_BF16, out_dtype=B.MTE_F32, max_tokens=T,
-                        max_batch=len(lens), max_seq=max(lens))
+                        max_batch=len(lens), max_seq=max(lens), weight_format=weight_format)
     enc = TextEncoder.from_host(cfg, (W.layer_weights(dims, l) for l in range(dims.n_layers)),
                                 W.final_norm_gain(dims))
     emb = torch.from_numpy(W.embeddings(dims, wl.layouts)).to("cuda", torch.bfloat16)
@@ -333,6 +333,36 @@ def run_prefix(torch, prefix, steps, warmup, frames=16):
     return res
 
 
+def e4m3_weight_bytes(dims):
+    """Bytes the encoder reads per forward with e4m3 weights: one byte per linear
+    weight, a float scale per weight row, fp32 norm gains."""
+    D, F, d = dims.hidden, dims.ffn, dims.head_dim
+    nqkv = (dims.n_q_heads + 2 * dims.n_kv_heads) * d
+    rows = nqkv + D + 2 * F + D
+    gains = 2 * D + (2 * d if dims.qk_norm else 0)
+    return dims.n_layers * (dims.params_per_layer + 4 * rows + 4 * gains)
+
+
+def run_e4m3(torch, name, steps, warmup, dims, batch1=True):
+    """The same steps with MTE_WEIGHTS_E4M3 encoders (weights quantised at creation)."""
+    out = {"format": "OCP e4m3 codes, power-of-two scale per weight row; fp16 activations, "
+                     "fp16 MFMA after exact widening, fp32 accumulate"}
+    m = run_workload(torch, name, steps, warmup, weight_format=1)
+    out["main"] = {"workload": name, "ms_per_step": round(m["wall_s"] * 1e3 / steps, 4),
+                   "tokens_per_s": round(m["T"] * steps / m["wall_s"], 1)}
+    if batch1:
+        b1 = run_workload(torch, "stack_b1", steps, warmup, weight_format=1)
+        t1 = b1["wall_s"] / steps
+        wbytes = e4m3_weight_bytes(dims) + 2 * b1["T"] * dims.hidden * 2
+        out["batch1"] = {"workload": "stack_b1: 1 frame x 96 tokens, 28 layers",
+                         "ms_per_step": round(t1 * 1e3, 4), "tokens_per_s": round(b1["T"] / t1, 1),
+                         "hbm_roofline": {"bound": "hbm", "achieved": round(wbytes / t1 / 1e9, 1),
+                                          "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                                          "frac": round(wbytes / t1 / 1e9 / PEAK_HBM_GBS, 4),
+                                          "bytes_per_step": wbytes}}
+    return out
+
+
 def copy_calibration(torch, mib=512, reps=5):
     """A plain device-to-device copy of `mib` MiB, `reps` times: the known-size kernel
     that calibrates the FETCH_SIZE / WRITE_SIZE counters (each dispatch moves exactly
@@ -358,6 +388,8 @@ def main():
                     help="only run the known-size copy used to calibrate HBM byte counters")
     ap.add_argument("--prefix", type=int, default=0,
                     help="also measure frames sharing a prefix of this many text tokens")
+    ap.add_argument("--no-e4m3", action="store_true",
+                    help="skip the runs with e4m3 weights (batch 1 and the main workload)")
     ap.add_argument("--overlap", action="store_true",
                     help="also measure the encoder on a side stream beside a main-stream GEMM load")
     args = ap.parse_args()
@@ -429,6 +461,8 @@ def main():
                                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                           "frac": round(wbytes / t1 / 1e9 / PEAK_HBM_GBS, 4),
                                           "bytes_per_step": wbytes}}
+    if not args.no_e4m3:
+        res["e4m3_weights"] = run_e4m3(torch, args.workload, K, args.warmup, dims, not args.no_batch1)
     if args.overlap:
         res["side_stream_overlap"] = {
             "batch16": run_overlap(torch, args.workload, K, args.warmup),
