@@ -53,6 +53,31 @@ class mte_seq_layout(C.Structure):
                 ("grid_w", C.c_int32), ("n_text_after", C.c_int32)]
 
 
+class mte_vision_config(C.Structure):
+    _fields_ = [("depth", C.c_int32), ("hidden", C.c_int32), ("n_heads", C.c_int32), ("head_dim", C.c_int32),
+                ("ffn", C.c_int32), ("patch", C.c_int32), ("merge", C.c_int32), ("in_channels", C.c_int32),
+                ("out_hidden", C.c_int32), ("ln_eps", C.c_float), ("rope_theta", C.c_float),
+                ("dtype", C.c_int32), ("out_dtype", C.c_int32), ("max_images", C.c_int32),
+                ("max_side", C.c_int32)]
+
+
+VISION_LAYER_FIELDS = ("ln1_g", "ln1_b", "w_qkv", "b_qkv", "w_o", "b_o", "ln2_g", "ln2_b", "w_fc1", "b_fc1",
+                       "w_fc2", "b_fc2")
+VISION_OUTER_FIELDS = ("patch_w", "patch_b", "merge_ln_g", "merge_ln_b", "merge_w1", "merge_b1", "merge_w2",
+                       "merge_b2")
+
+
+class mte_vision_layer_weights(C.Structure):
+    _fields_ = [(n, C.c_void_p) for n in VISION_LAYER_FIELDS]
+
+
+class mte_vision_weights(C.Structure):
+    _fields_ = [("patch_w", C.c_void_p), ("patch_b", C.c_void_p),
+                ("layers", C.POINTER(mte_vision_layer_weights)),
+                ("merge_ln_g", C.c_void_p), ("merge_ln_b", C.c_void_p), ("merge_w1", C.c_void_p),
+                ("merge_b1", C.c_void_p), ("merge_w2", C.c_void_p), ("merge_b2", C.c_void_p)]
+
+
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_05981_amd.build`")
 lib = C.CDLL(LIB_PATH)
@@ -77,6 +102,11 @@ _sig = {
     "mte_timing_read": (C.c_int, [_P, C.POINTER(C.c_int32), C.POINTER(C.c_double)]),
     "mte_timing_disable": (C.c_int, [_P]),
     "mte_quantize_e4m3_rows": (C.c_int, [_P, C.c_int32, C.c_int32, C.c_int32, _P, _P, _P]),
+    "mte_vision_config_validate": (C.c_int, [C.POINTER(mte_vision_config)]),
+    "mte_vision_create": (C.c_int, [C.POINTER(mte_vision_config), C.POINTER(mte_vision_weights), _P,
+                                    C.POINTER(_P)]),
+    "mte_vision_encode": (C.c_int, [_P, _P, C.c_int32, C.c_int32, C.c_int32, _P, _P]),
+    "mte_vision_destroy": (None, [_P]),
 }
 for _name, (_res, _args) in _sig.items():
     _f = getattr(lib, _name)
@@ -191,3 +221,44 @@ def mte_quantize_e4m3_rows(src: int, src_dtype: int, rows: int, cols: int, codes
                            stream: int) -> int:
     return _check(lib.mte_quantize_e4m3_rows(src, src_dtype, rows, cols, codes, scales, stream),
                   "mte_quantize_e4m3_rows")
+
+
+def make_vision_config(depth, hidden, n_heads, head_dim, ffn, patch=16, merge=2, in_channels=3, out_hidden=2048,
+                       ln_eps=1e-6, rope_theta=10000.0, dtype=MTE_BF16, out_dtype=None, max_images=16,
+                       max_side=256) -> mte_vision_config:
+    c = mte_vision_config()
+    c.depth, c.hidden, c.n_heads, c.head_dim, c.ffn = depth, hidden, n_heads, head_dim, ffn
+    c.patch, c.merge, c.in_channels, c.out_hidden = patch, merge, in_channels, out_hidden
+    c.ln_eps, c.rope_theta, c.dtype = ln_eps, rope_theta, dtype
+    c.out_dtype = dtype if out_dtype is None else out_dtype
+    c.max_images, c.max_side = max_images, max_side
+    return c
+
+
+def mte_vision_config_validate(cfg: mte_vision_config) -> int:
+    return lib.mte_vision_config_validate(C.byref(cfg))
+
+
+def mte_vision_create(cfg: mte_vision_config, outer: dict, layers: Sequence[dict], stream: int) -> int:
+    """outer: device addresses keyed like VISION_OUTER_FIELDS; layers: per block keyed like
+    VISION_LAYER_FIELDS."""
+    arr = (mte_vision_layer_weights * max(1, len(layers)))()
+    for i, L in enumerate(layers):
+        for k, v in L.items():
+            setattr(arr[i], k, v)
+    w = mte_vision_weights()
+    for k in VISION_OUTER_FIELDS:
+        setattr(w, k, outer[k])
+    w.layers = arr if layers else None
+    h = _P()
+    _check(lib.mte_vision_create(C.byref(cfg), C.byref(w), stream, C.byref(h)), "mte_vision_create")
+    return h.value
+
+
+def mte_vision_encode(enc: int, pixels: int, n_images: int, height: int, width: int, out: int,
+                      stream: int) -> int:
+    return _check(lib.mte_vision_encode(enc, pixels, n_images, height, width, out, stream), "mte_vision_encode")
+
+
+def mte_vision_destroy(enc: int) -> None:
+    lib.mte_vision_destroy(enc)

@@ -46,6 +46,7 @@ struct AttnArgs {
   int hpb;         // query heads per workgroup
   int head_blocks;
   int n_seq;
+  int causal;      // 0: every query sees all keys of its sequence (and the prefix)
   int cu[kMaxSeqPerLaunch + 1];     // absolute token offsets
   int tile0[kMaxSeqPerLaunch + 1];  // first workgroup tile of each sequence
 };
@@ -170,7 +171,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   // Keys are numbered over [0, P + L): the shared prefix's first, then the
   // sequence's own; own query i sits at key index P + i.
   const int P = a.P;
-  const int n_blocks = (q_last >= 0) ? ((P + q_last) / KV + 1) : 0;
+  const int n_blocks = (q_last < 0) ? 0 : a.causal ? ((P + q_last) / KV + 1) : ((P + L - 1) / KV + 1);
   auto key_row = [&](int kv) -> const float * {
     kv = min(kv, P + L - 1);
     return kv < P ? a.pre + (size_t)kv * ld : a.qkv + base + (size_t)(kv - P) * ld;
@@ -247,7 +248,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   };
   // One key/value tile for this wave: scores, online softmax, O update.
   auto compute = [&](int kv0, const u32x4 *sK, const T *sVt) {
-    if (!(qw < L && kv0 <= P + wave_last)) return;
+    if (!(qw < L && kv0 <= (a.causal ? P + wave_last : P + L - 1))) return;
     // Independent accumulators (one per split product, or per k parity
     // for fp32) so consecutive MFMAs do not wait on each other's results.
     constexpr int NS = (NP == 2) ? 3 : 2;
@@ -275,7 +276,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int kv = kv0 + acc_row(r, lane);
-      s[r] = (kv <= P + my_q && kv < P + L) ? s[r] * sc : -INFINITY;
+      s[r] = ((!a.causal || kv <= P + my_q) && kv < P + L) ? s[r] * sc : -INFINITY;
       mb = fmaxf(mb, s[r]);
     }
     mb = warp_max_xor(mb, 32);
@@ -386,10 +387,11 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 }
 
 hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int P, void *o, float out_scale,
-                            const int32_t *cu, int batch, int Hq, int Hkv, int d, hipStream_t s) {
+                            const int32_t *cu, int batch, int Hq, int Hkv, int d, hipStream_t s, int causal) {
   const int rep = Hq / Hkv;
   if (P < 0 || (P > 0 && !prefix)) return hipErrorInvalidValue;
   AttnArgs a;
+  a.causal = causal ? 1 : 0;
   a.qkv = qkv;
   a.pre = prefix;
   a.P = P;

@@ -128,9 +128,11 @@ hipError_t launch_mode_f8w(int epi, int tile, int splits, const GemmArgs &a, hip
 
 hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void *A, const void *W,
                             void *C, size_t c_plane, int M, int N, int K, int ldc, float scale,
-                            float out_scale, const QkvEpi *qe, hipStream_t s, const float *col_scale) {
+                            float out_scale, const QkvEpi *qe, hipStream_t s, const float *col_scale,
+                            const float *bias) {
   if (M <= 0) return hipSuccess;
   const bool w8 = mode == MODE_F8W;
+  if (bias && splits > 1) return hipErrorInvalidValue;
   const int esz = mode == MODE_F32 ? 4 : 2;
   if (epi == EPI_QKV && (!qe || (qe->hd != 64 && qe->hd != 128))) return hipErrorInvalidValue;
   if (w8 && !col_scale) return hipErrorInvalidValue;
@@ -139,7 +141,7 @@ hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void 
       (splits > 1 && epi != EPI_PARTIAL))
     return hipErrorInvalidValue;
   GemmArgs a{(const char *)A, (const char *)W, C, c_plane, M, N, K, ldc, K / splits, scale, out_scale,
-             epi == EPI_QKV ? *qe : QkvEpi{}, w8 ? col_scale : nullptr};
+             epi == EPI_QKV ? *qe : QkvEpi{}, w8 ? col_scale : nullptr, bias};
   if (w8) return launch_mode_f8w(epi, tile, splits, a, s);
   return mode == MODE_F16 ? launch_mode<MODE_F16>(epi, tile, splits, a, s)
                           : launch_mode<MODE_F32>(epi, tile, splits, a, s);
@@ -147,12 +149,13 @@ hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void 
 
 hipError_t launch_gemm(int mode, int epi, const void *A, const void *W, void *C, int M, int N, int K,
                        int ldc, float scale, float out_scale, float *ws, size_t ws_elems,
-                       int *splits_out, const QkvEpi *qe, hipStream_t s, const float *col_scale) {
+                       int *splits_out, const QkvEpi *qe, hipStream_t s, const float *col_scale,
+                       const float *bias) {
   *splits_out = 0;
   if (M <= 0) return hipSuccess;
   if (epi == EPI_QKV && !qe) return hipErrorInvalidValue;
   int tile, splits;
-  plan(M, N, K, mode == MODE_F32 ? 4 : 2, epi, epi == EPI_QKV ? qe->hd : 32, ws ? ws_elems : 0,
+  plan(M, N, K, mode == MODE_F32 ? 4 : 2, epi, epi == EPI_QKV ? qe->hd : 32, (ws && !bias) ? ws_elems : 0,
        mode == MODE_F8W, &tile, &splits);
   if (tile < 0) return hipErrorInvalidValue;
   if (splits > 1) {
@@ -160,7 +163,8 @@ hipError_t launch_gemm(int mode, int epi, const void *A, const void *W, void *C,
     return launch_gemm_tile(mode, EPI_PARTIAL, tile, splits, A, W, ws, (size_t)M * N, M, N, K, N, scale,
                             1.f, nullptr, s, col_scale);
   }
-  return launch_gemm_tile(mode, epi, tile, 1, A, W, C, 0, M, N, K, ldc, scale, out_scale, qe, s, col_scale);
+  return launch_gemm_tile(mode, epi, tile, 1, A, W, C, 0, M, N, K, ldc, scale, out_scale, qe, s, col_scale,
+                          bias);
 }
 
 }  // namespace mte

@@ -57,15 +57,22 @@ namespace mte {
 struct GemmArgs {
   const char *A;
   const char *W;
-  void *C;            // EPI_STORE / EPI_RESID / EPI_PARTIAL: float; EPI_SWIGLU: activation format
+  void *C;            // EPI_STORE / EPI_RESID / EPI_PARTIAL: float; EPI_SWIGLU / EPI_GELU: activation format
   size_t c_plane;     // EPI_PARTIAL: elements between the partial sums of two K splits
   int M, N, K, ldc;
   int k_chunk;        // K range of one split (gridDim.z splits)
   float scale;        // product multiplier (inverse operand pre-scales)
-  float out_scale;    // EPI_SWIGLU output multiplier
+  float out_scale;    // EPI_SWIGLU / EPI_GELU output multiplier
   QkvEpi qe;          // EPI_QKV
   const float *cs;    // MODE_F8W: per-column (weight row) scales [N]
+  const float *bias;  // [N] added to the product before the epilogue (unsplit launches), or null
 };
+
+// tanh-approximated GELU: 0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3))).
+__device__ __forceinline__ float gelu_tanh(float z) {
+  const float u = 0.7978845608028654f * (z + 0.044715f * z * z * z);
+  return 0.5f * z * (1.f + tanhf(u));
+}
 
 // Chunk swizzles for rows of 128 bytes (8 chunks) and 64 bytes (4 chunks):
 // the 16-byte fragment reads (32 consecutive rows at one logical chunk, the
@@ -412,6 +419,19 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
         for (int r = 0; r < 16; ++r) acc[i][j][r] *= c;
     }
   }
+  if (g.bias) {
+    // bias / scale added to the accumulators: `scale` is a power of two, so
+    // (acc + bias / scale) * scale rounds exactly like acc * scale + bias.
+    const float ib = 1.f / g.scale;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const float b = g.bias[n0 + wn * WTN + j * 32 + lrow] * ib;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] += b;
+    }
+  }
 
   // Epilogue.
   if constexpr (EPI == EPI_QKV) {
@@ -453,6 +473,24 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
     }
     return;
   }
+  if constexpr (EPI == EPI_GELU) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + wm * WTM + i * 32 + acc_row(r, lane);
+        if (m >= M) continue;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const size_t o = (size_t)m * g.ldc + n0 + wn * WTN + j * 32 + lrow;
+          const float y = gelu_tanh(acc[i][j][r] * g.scale) * g.out_scale;
+          if constexpr (MODE == MODE_F32) ((float *)g.C)[o] = y;
+          else ((f16 *)g.C)[o] = (f16)y;
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -481,8 +519,8 @@ static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
     return hipErrorInvalidValue;  // the QK-norm epilogue needs whole heads per wave
   } else if constexpr (MODE == MODE_F32 && !F32) {
     return hipErrorInvalidValue;  // fp32 operands are built for a few tiles only
-  } else if constexpr (MODE == MODE_F8W && ROWB != 128) {
-    return hipErrorInvalidValue;  // e4m3 weights: tiles staging 128 bytes of A per row
+  } else if constexpr (MODE == MODE_F8W && (ROWB != 128 || EPI == EPI_GELU)) {
+    return hipErrorInvalidValue;  // e4m3 weights: tiles staging 128 bytes of A per row, decoder epilogues
   } else {
     constexpr int lds_bytes = P * (BM + (MODE == MODE_F8W ? BN / 2 : BN)) * ROWB;
     auto kern = k_gemm<MODE, BM, BN, WM, WN, ROWB, P, EPI, OCC>;
@@ -557,6 +595,7 @@ static hipError_t launch_mode(int epi, int tile, int splits, const GemmArgs &a, 
     case EPI_SWIGLU: return run_id<MODE, EPI_SWIGLU>(tile, a, splits, s);
     case EPI_RESID: return run_id<MODE, EPI_RESID>(tile, a, splits, s);
     case EPI_QKV: return run_id<MODE, EPI_QKV>(tile, a, splits, s);
+    case EPI_GELU: return run_id<MODE, EPI_GELU>(tile, a, splits, s);
     default: return run_id<MODE, EPI_PARTIAL>(tile, a, splits, s);
   }
 }

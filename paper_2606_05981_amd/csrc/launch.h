@@ -32,6 +32,7 @@ enum Epilogue {
   EPI_RESID = 2,   // C (float residual stream) [m, n] += scale * acc
   EPI_PARTIAL = 3, // C (float) + split * c_plane [m, n] = scale * acc: one K split's partial sum
   EPI_QKV = 4,     // C (float) [m, n] = scale * acc, q and k heads RMS-normalised per head and rotated
+  EPI_GELU = 5,    // C [m, n] = out_scale * gelu_tanh(scale * acc), float (MODE_F32) or fp16
 };
 
 // Parameters of EPI_QKV: columns [0, nq_cols) are q heads, [nq_cols,
@@ -61,10 +62,12 @@ struct QkvEpi {
 // MODE_F8W: W holds e4m3 codes [N, K] and col_scale [N] the scale of each
 // weight row (column of the product), applied before `scale` and the
 // epilogue; col_scale is ignored in the other modes.
+// bias: optional float [N] added to the product (after col_scale and `scale`, before the
+// epilogue); `scale` must then be a power of two, and the product is never K-split.
 hipError_t launch_gemm(int mode, int epi, const void *A, const void *W, void *C, int M, int N, int K,
                        int ldc, float scale, float out_scale, float *ws, size_t ws_elems,
                        int *splits_out, const QkvEpi *qe, hipStream_t s,
-                       const float *col_scale = nullptr);
+                       const float *col_scale = nullptr, const float *bias = nullptr);
 
 // The same with an explicit tile configuration (index into the GEMM tile
 // table) and number of K splits (> 1 only with EPI_PARTIAL, partial sums
@@ -73,7 +76,7 @@ hipError_t launch_gemm(int mode, int epi, const void *A, const void *W, void *C,
 hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void *A, const void *W,
                             void *C, size_t c_plane, int M, int N, int K, int ldc, float scale,
                             float out_scale, const QkvEpi *qe, hipStream_t s,
-                            const float *col_scale = nullptr);
+                            const float *col_scale = nullptr, const float *bias = nullptr);
 int gemm_num_tiles();
 
 // Per-row RMSNorm: out[r, :] = x[r, :] / sqrt(mean(x[r,:]^2) + eps) * g with
@@ -120,9 +123,11 @@ hipError_t launch_qkv_parts(float *qkv, const float *parts, int nparts, int T, i
 // and v columns are read) that every sequence attends to in full before
 // its own keys, or P = 0. o: [T, Hq*d], float (MODE_F32) or fp16
 // (MODE_F16) times out_scale. cu: host int32[batch+1] sequence offsets.
-// Launches in chunks of <= 256 sequences.
+// Launches in chunks of <= 256 sequences. causal = 0: bidirectional (every
+// query attends to all keys of its own sequence).
 hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int P, void *o, float out_scale,
-                            const int32_t *cu, int batch, int Hq, int Hkv, int d, hipStream_t s);
+                            const int32_t *cu, int batch, int Hq, int Hkv, int d, hipStream_t s,
+                            int causal = 1);
 
 // Positions of packed sequences (see mte_build_positions).
 hipError_t launch_positions(const int32_t *layouts5, int batch, int32_t *pos_thw, int T,
@@ -139,12 +144,26 @@ hipError_t launch_matrix_stats(int src_fmt, const void *src, int rows, int cols,
                                hipStream_t s);
 
 // Converts rows [0, rows) of src (format src_fmt, cols columns) into
-// dst_fmt (FMT_F32 or FMT_F16) times `scale` (a power of two), writing
+// dst_fmt (bf16 -> FMT_F16, f32 -> FMT_F32 or FMT_BF16) times `scale` (a power of two), writing
 // source row r to destination row map(r): map(r) = r, or with `interleave`
 // the gate/up packing (src = gate or up of F = rows rows: gate row f goes to
 // 32*(f/16) + f%16, up row f to 32*(f/16) + 16 + f%16, `up` selecting which).
 hipError_t launch_convert_rows(int src_fmt, const void *src, int dst_fmt, void *dst, int rows, int cols,
                                float scale, int interleave, int up, hipStream_t s);
+
+// Vision tower. Patches of n images [n, C, H, W] (in_fmt FMT_F32 / FMT_BF16)
+// -> out [n * (H/patch) * (W/patch), C*patch*patch] (out_fmt FMT_F32 / FMT_F16),
+// patches of an image in merge-group order (groups of merge x merge patches
+// row-major over the image, row-major inside a group), each patch's vector in
+// (channel, row, column) order. H and W multiples of patch * merge.
+hipError_t launch_patchify(int in_fmt, const void *pixels, int n, int C, int H, int W, int patch, int merge,
+                           int out_fmt, void *out, hipStream_t s);
+// pos [3, n * patches per image]: t = 0, h = patch row, w = patch column (same order).
+hipError_t launch_patch_positions(int32_t *pos, int n, int H, int W, int patch, int merge, hipStream_t s);
+// y[r] = (x[r] - mean) / sqrt(var + eps) * g + b per row of x (float [rows, D],
+// D <= 4096); y in out_fmt (FMT_F32 / FMT_F16).
+hipError_t launch_layernorm(const float *x, const float *g, const float *b, int out_fmt, void *y, int rows, int D,
+                            float eps, hipStream_t s);
 
 // OCP e4m3 quantisation of the rows of a [rows, cols] matrix (format src_fmt,
 // FMT_F32 or FMT_BF16): row r gets the scale 2^e_r with e_r the smallest

@@ -468,6 +468,9 @@ hipError_t launch_convert_rows(int src_fmt, const void *src, int dst_fmt, void *
   else if (src_fmt == FMT_F32 && dst_fmt == FMT_F32)
     hipLaunchKernelGGL((k_convert_rows<float, float>), grid, dim3(256), 0, s, (const float *)src,
                        (float *)dst, cols, scale, interleave, up);
+  else if (src_fmt == FMT_F32 && dst_fmt == FMT_BF16)
+    hipLaunchKernelGGL((k_convert_rows<float, bf16>), grid, dim3(256), 0, s, (const float *)src,
+                       (bf16 *)dst, cols, scale, interleave, up);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

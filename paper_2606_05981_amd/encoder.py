@@ -132,3 +132,53 @@ def quantize_e4m3_rows(w: torch.Tensor, stream: Optional[torch.cuda.Stream] = No
     B.mte_quantize_e4m3_rows(w.data_ptr(), B.MTE_BF16 if w.dtype == torch.bfloat16 else B.MTE_F32, rows, cols,
                              codes.data_ptr(), scales.data_ptr(), _stream(stream))
     return codes, scales
+
+
+class VisionEncoder:
+    """Owns one mte_vision (include/mte_vision.h): images -> image-token embeddings."""
+
+    def __init__(self, cfg: B.mte_vision_config, outer: Dict[str, torch.Tensor],
+                 layers: Sequence[Dict[str, torch.Tensor]], stream: Optional[torch.cuda.Stream] = None):
+        self.cfg = cfg
+        self.dtype = TORCH_DTYPE[cfg.dtype]
+        self.out_dtype = TORCH_DTYPE[cfg.out_dtype]
+        for t in list(outer.values()) + [t for L in layers for t in L.values()]:
+            if t.dtype != self.dtype or not t.is_cuda or not t.is_contiguous():
+                raise ValueError(f"vision weights: expected contiguous {self.dtype} tensors on the GPU")
+        self.handle = B.mte_vision_create(cfg, {k: outer[k].data_ptr() for k in B.VISION_OUTER_FIELDS},
+                                          [{k: L[k].data_ptr() for k in B.VISION_LAYER_FIELDS} for L in layers],
+                                          _stream(stream))
+        torch.cuda.synchronize()
+
+    @classmethod
+    def from_host(cls, cfg: B.mte_vision_config, outer, layer_arrays, device="cuda"):
+        dt = TORCH_DTYPE[cfg.dtype]
+        put = lambda a: torch.as_tensor(a).to(device=device, dtype=dt).contiguous()
+        return cls(cfg, {k: put(outer[k]) for k in B.VISION_OUTER_FIELDS},
+                   [{k: put(L[k]) for k in B.VISION_LAYER_FIELDS} for L in layer_arrays])
+
+    def encode(self, pixels: torch.Tensor, out: Optional[torch.Tensor] = None,
+               stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+        """pixels [n, C, H, W] of the config dtype -> [n * tokens per image, out_hidden]."""
+        c = self.cfg
+        if pixels.dim() != 4 or pixels.dtype != self.dtype or not pixels.is_contiguous() or \
+                pixels.shape[1] != c.in_channels:
+            raise ValueError("pixels must be a contiguous [n, C, H, W] tensor of the encoder dtype")
+        n, _, h, w = pixels.shape
+        s = c.patch * c.merge
+        rows = n * (h // s) * (w // s)
+        if out is None:
+            out = torch.empty((rows, c.out_hidden), dtype=self.out_dtype, device=pixels.device)
+        B.mte_vision_encode(self.handle, pixels.data_ptr(), n, h, w, out.data_ptr(), _stream(stream))
+        return out
+
+    def close(self) -> None:
+        if getattr(self, "handle", None):
+            B.mte_vision_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

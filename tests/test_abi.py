@@ -16,7 +16,7 @@ def B():
 
 
 def _declared_functions():
-    src = open(os.path.join(ROOT, "include", "mte.h")).read()
+    src = "".join(open(os.path.join(ROOT, "include", f)).read() for f in ("mte.h", "mte_vision.h"))
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][A-Za-z0-9_]*\s*\**\s*(mte_[a-z0-9_]+)\s*\(", src, flags=re.M)
     return sorted(set(names))
@@ -26,7 +26,8 @@ def test_header_declares_the_boundary():
     names = _declared_functions()
     for n in ("mte_encoder_create", "mte_encode", "mte_build_positions", "mte_encoder_destroy",
               "mte_status_string", "mte_config_validate", "mte_check_batch", "mte_encode_layers",
-              "mte_encoder_reserve_prefix", "mte_encode_prefixed", "mte_quantize_e4m3_rows"):
+              "mte_encoder_reserve_prefix", "mte_encode_prefixed", "mte_quantize_e4m3_rows",
+              "mte_vision_config_validate", "mte_vision_create", "mte_vision_encode", "mte_vision_destroy"):
         assert n in names
 
 
@@ -147,3 +148,34 @@ def test_quantize_rejects_bad_arguments(B):
 def test_status_strings(B):
     for s in (0, -1, -2, -3, -4, -5, 17):
         assert isinstance(B.mte_status_string(s), str) and B.mte_status_string(s)
+
+
+def _vision(B, **kw):
+    args = dict(depth=24, hidden=1024, n_heads=16, head_dim=64, ffn=4096)
+    args.update(kw)
+    return B.make_vision_config(**args)
+
+
+def test_vision_configs(B):
+    assert B.mte_vision_config_validate(_vision(B)) == 0
+    assert B.mte_vision_config_validate(_vision(B, depth=2, hidden=128, n_heads=2, ffn=256, out_hidden=256,
+                                                dtype=0)) == 0
+    assert B.lib.mte_vision_config_validate(None) == -1
+    for kw, st in [(dict(hidden=1000), -1),                 # hidden != heads * head_dim
+                   (dict(n_heads=10, hidden=960, head_dim=96), -5),
+                   (dict(ffn=4000), -5), (dict(out_hidden=2000), -5),
+                   (dict(patch=10), -5),                    # 3*10*10 not a multiple of 64
+                   (dict(depth=-1), -1), (dict(max_images=0), -1), (dict(max_side=16), -1),
+                   (dict(ln_eps=0.0), -1), (dict(dtype=3), -1),
+                   (dict(hidden=8192, n_heads=64, head_dim=128), -5)]:
+        assert B.mte_vision_config_validate(_vision(B, **kw)) == st, kw
+
+
+def test_vision_rejects_bad_arguments(B):
+    assert B.lib.mte_vision_encode(None, 4096, 1, 256, 256, 8192, None) == -1
+    h = ctypes.c_void_p()
+    good = _vision(B)
+    w = B.mte_vision_weights()
+    assert B.lib.mte_vision_create(ctypes.byref(good), ctypes.byref(w), None, ctypes.byref(h)) == -1
+    assert B.lib.mte_vision_create(ctypes.byref(good), None, None, ctypes.byref(h)) == -1
+    B.lib.mte_vision_destroy(None)

@@ -1,0 +1,112 @@
+"""Parity of the vision tower (mte_vision_*, through the C ABI) with the fp64
+oracle (oracle/vit_oracle.py). Error = max|gpu - oracle| / rms(oracle) over
+all image tokens. fp32 configuration <= 1e-4; bf16 weights with fp16
+matrix-core operands and fp32 accumulation <= 1e-2 for two blocks and the
+merger, <= 3e-2 for the 24-block tower (the decoder's bars)."""
+import functools
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import vit_oracle as V
+from synth import vision as SV
+from tests.gpu_common import rel_err
+
+pytestmark = pytest.mark.gpu
+
+TOL_F32 = 1e-4
+TOL_SHORT = 1e-2
+TOL_DEEP = 3e-2
+
+
+def _say(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available(), "no GPU"
+    return t
+
+
+@functools.lru_cache(maxsize=None)
+def _bw(v, l):
+    return SV.block_weights(v, l)
+
+
+@functools.lru_cache(maxsize=None)
+def _ow(v):
+    return SV.outer_weights(v)
+
+
+def _encoder(v, max_images=4, max_side=256, out_dtype=None):
+    from paper_2606_05981_amd import binding as B
+    from paper_2606_05981_amd.encoder import VisionEncoder
+    dt = B.MTE_BF16 if v.dtype == "bf16" else B.MTE_F32
+    cfg = B.make_vision_config(v.depth, v.hidden, v.n_heads, v.head_dim, v.ffn, patch=v.patch, merge=v.merge,
+                               in_channels=v.in_channels, out_hidden=v.out_hidden, ln_eps=v.ln_eps,
+                               rope_theta=v.rope_theta, dtype=dt, out_dtype=B.MTE_F32 if out_dtype is None else out_dtype,
+                               max_images=max_images, max_side=max_side)
+    return VisionEncoder.from_host(cfg, _ow(v), [_bw(v, l) for l in range(v.depth)])
+
+
+def _run(torch, enc, v, img, raw=False):
+    dt = torch.bfloat16 if v.dtype == "bf16" else torch.float32
+    out = enc.encode(torch.from_numpy(img).to("cuda", dt))
+    torch.cuda.synchronize()
+    return out.cpu() if raw else out.float().cpu().numpy()
+
+
+def _oracle(v, img):
+    return V.encode(img, v, lambda l: _bw(v, l), _ow(v))
+
+
+@pytest.mark.parametrize("n,h,w", [(2, 64, 96), (1, 64, 64), (3, 32, 32)])
+def test_vision_tiny_fp32(torch, n, h, w):
+    v = SV.VDIMS_TINY
+    img = SV.images(v, n, h, w)
+    _say("vision tiny fp32", n, h, w)
+    enc = _encoder(v, max_side=96)
+    got = _run(torch, enc, v, img)
+    enc.close()
+    ref = _oracle(v, img)
+    assert got.shape == ref.shape
+    err = rel_err(got, ref)
+    _say("  err", err)
+    assert err <= TOL_F32
+
+
+def test_vision_bf16_two_blocks(torch):
+    v = SV.VDIMS_FULL.with_(depth=2)
+    img = SV.images(v, 2, 256, 256)
+    _say("vision bf16, 2 blocks, 2 images of 256x256")
+    enc = _encoder(v)
+    got = _run(torch, enc, v, img)
+    ref = _oracle(v, img)
+    err = rel_err(got, ref)
+    _say("  err", err)
+    assert err <= TOL_SHORT
+    for i in range(2):
+        assert rel_err(got[64 * i:64 * (i + 1)], ref[64 * i:64 * (i + 1)]) <= TOL_SHORT
+    # a bf16 output is the fp32 result rounded to nearest even
+    from paper_2606_05981_amd import binding as B
+    e16 = _encoder(v, out_dtype=B.MTE_BF16)
+    y16 = _run(torch, e16, v, img, raw=True)
+    y32 = _run(torch, enc, v, img, raw=True)
+    enc.close(); e16.close()
+    assert y16.dtype == torch.bfloat16 and torch.equal(y16, y32.to(torch.bfloat16))
+
+
+def test_vision_bf16_full_depth(torch):
+    v = SV.VDIMS_FULL
+    img = SV.images(v, 1, 256, 256)
+    _say("vision bf16, 24 blocks, one 256x256 image")
+    enc = _encoder(v, max_images=16)
+    got = _run(torch, enc, v, img)
+    enc.close()
+    ref = _oracle(v, img)
+    err = rel_err(got, ref)
+    _say("  err", err)
+    assert err <= TOL_DEEP
