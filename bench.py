@@ -363,6 +363,59 @@ def run_e4m3(torch, name, steps, warmup, dims, batch1=True):
     return out
 
 
+def vision_flops(v, n, h, w):
+    """Algorithmic flops of one vision-tower pass over n images of h x w."""
+    per = (h // v.patch) * (w // v.patch)
+    T, D, F = n * per, v.hidden, v.ffn
+    mm = v.merge * v.merge
+    kp = v.in_channels * v.patch * v.patch
+    blocks = v.depth * (2 * T * (4 * D * D + 2 * F * D) + n * 4 * per * per * D)
+    merger = 2 * (T // mm) * (mm * D * mm * D + v.out_hidden * mm * D)
+    return 2 * T * D * kp + blocks + merger
+
+
+def run_vision(torch, steps, warmup, n=16, side=256):
+    """The vision tower on n images of side x side: 24 pre-norm ViT blocks of width 1024
+    and the 2x2 merger, captured once into a HIP graph and replayed."""
+    from paper_2606_05981_amd import binding as B
+    from paper_2606_05981_amd.encoder import VisionEncoder
+    from synth import vision as SV
+    v = SV.VDIMS_FULL
+    cfg = B.make_vision_config(v.depth, v.hidden, v.n_heads, v.head_dim, v.ffn, patch=v.patch, merge=v.merge,
+                               in_channels=v.in_channels, out_hidden=v.out_hidden, ln_eps=v.ln_eps,
+                               rope_theta=v.rope_theta, dtype=B.MTE_BF16, out_dtype=B.MTE_BF16,
+                               max_images=n, max_side=side)
+    enc = VisionEncoder.from_host(cfg, SV.outer_weights(v), (SV.block_weights(v, l) for l in range(v.depth)))
+    px = torch.from_numpy(SV.images(v, n, side, side)).to("cuda", torch.bfloat16)
+    out = torch.empty((n * v.tokens_per_image(side, side), v.out_hidden), dtype=torch.bfloat16, device="cuda")
+    for _ in range(warmup):
+        enc.encode(px, out)
+    torch.cuda.synchronize()
+    side_s = torch.cuda.Stream()
+    side_s.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side_s):
+        with torch.cuda.graph(graph, stream=side_s):
+            enc.encode(px, out, stream=side_s)
+    torch.cuda.current_stream().wait_stream(side_s)
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    enc.close()
+    fl = vision_flops(v, n, side, side)
+    return {"workload": f"{n} images of {side}x{side}, 24 ViT blocks (width 1024, 16 heads of 64, MLP 4096) "
+                        "+ 2x2 merger to 2048",
+            "ms_per_step": round(dt * 1e3, 4), "images_per_s": round(n / dt, 1),
+            "image_tokens_per_s": round(n * v.tokens_per_image(side, side) / dt, 1),
+            "model_tflops": round(fl / dt / 1e12, 1), "frac_of_bf16_peak": round(fl / dt / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "flops_per_step": fl}
+
+
 def copy_calibration(torch, mib=512, reps=5):
     """A plain device-to-device copy of `mib` MiB, `reps` times: the known-size kernel
     that calibrates the FETCH_SIZE / WRITE_SIZE counters (each dispatch moves exactly
@@ -390,6 +443,10 @@ def main():
                     help="also measure frames sharing a prefix of this many text tokens")
     ap.add_argument("--no-e4m3", action="store_true",
                     help="skip the runs with e4m3 weights (batch 1 and the main workload)")
+    ap.add_argument("--vision-only", action="store_true",
+                    help="only run the vision tower and print its figures (for profiling)")
+    ap.add_argument("--no-vision", action="store_true",
+                    help="skip the vision-tower run (16 images of 256x256)")
     ap.add_argument("--overlap", action="store_true",
                     help="also measure the encoder on a side stream beside a main-stream GEMM load")
     args = ap.parse_args()
@@ -402,6 +459,9 @@ def main():
     assert torch.cuda.is_available(), "no GPU"
     if args.copy_calibration:
         copy_calibration(torch)
+        return
+    if args.vision_only:
+        print(json.dumps({"vision_tower": run_vision(torch, args.steps, args.warmup)}), flush=True)
         return
 
     main_run = run_workload(torch, args.workload, args.steps, args.warmup, timing_class=3)
@@ -461,6 +521,8 @@ def main():
                                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                           "frac": round(wbytes / t1 / 1e9 / PEAK_HBM_GBS, 4),
                                           "bytes_per_step": wbytes}}
+    if not args.no_vision:
+        res["vision_tower"] = run_vision(torch, K, args.warmup)
     if not args.no_e4m3:
         res["e4m3_weights"] = run_e4m3(torch, args.workload, K, args.warmup, dims, not args.no_batch1)
     if args.overlap:

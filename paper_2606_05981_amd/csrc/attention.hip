@@ -22,9 +22,13 @@
 // operand x into bf16 hi + lo (lo = bf16(x - hi)) and forms each product
 // from three bf16 MFMAs, hi*hi + lo*hi + hi*lo (the lo*lo term is below fp32
 // accumulation noise), and writes o times a power-of-two pre-scale as fp16,
-// the operand type of the output projection. The sequence table (offsets,
-// first tile of each sequence) is passed by value in the kernel arguments,
-// so nothing is read back to the host.
+// the operand type of the output projection. With PVH (fp16 PV, MODE_F16
+// only) the scores are formed the same way but P and V enter one fp16 MFMA:
+// P in [0, 1] and V times the output pre-scale (a static bound keeps it, and
+// hence o, in fp16 range) are rounded once to fp16, as the projections'
+// activations are. The sequence table (offsets, first tile of each
+// sequence) is passed by value in the kernel arguments, so nothing is read
+// back to the host.
 #include <type_traits>
 
 #include "common.h"
@@ -83,31 +87,38 @@ __device__ __forceinline__ int vt_pos(int k) {
 // the next one in flight in registers (any length); NB > 1 loads all of a
 // workgroup's tiles up front (sequences of at most NB * 32 tokens), so the
 // whole key/value range costs one global-load latency and one barrier.
-template <int MODE, int HD, int NB>
+template <int MODE, int HD, int NB, bool PVH>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
+  static_assert(!PVH || MODE == MODE_F16, "fp16 PV with fp16 operands only");
+  // q, k: type T in NP planes; v and p: type TV in NPV planes
   typedef typename std::conditional<MODE == MODE_F32, float, bf16>::type T;
-  constexpr int NP = (MODE == MODE_F16) ? 2 : 1;   // bf16 planes per operand
+  typedef typename std::conditional<PVH, f16, T>::type TV;
+  constexpr int NP = (MODE == MODE_F16) ? 2 : 1;   // bf16 planes of q and k
+  constexpr int NPV = PVH ? 1 : NP;                // planes of v and p
   constexpr int KV = 32;
   constexpr int EC = 16 / (int)sizeof(T);        // elements per 16-byte chunk
   constexpr int NCH = HD / EC;                   // chunks per head row
-  constexpr int EPF = Frag<T>::kElems;           // values per fragment (== EC)
+  constexpr int EPF = Frag<TV>::kElems;          // values per P / V fragment
   constexpr int NFP = 16 / EPF;                  // P fragments per 32-kv tile
-  constexpr int VTP = KV + 16 / (int)sizeof(T);  // V^T row pitch: 16-byte aligned, conflict-free
+  constexpr int VTP = KV + 16 / (int)sizeof(TV); // V^T row pitch: 16-byte aligned, conflict-free
   constexpr int ND = HD / 32;                    // 32-wide d blocks
   constexpr int OTP = HD + 4;                    // padded output staging row (floats)
-  static_assert(EC == EPF, "chunk = fragment");
+  static_assert(EC == Frag<T>::kElems && (int)sizeof(T) == (int)sizeof(TV), "chunk = fragment");
   typedef typename Frag<T>::type frag_t;
+  typedef typename Frag<TV>::type vfrag_t;
+  // PVH: V is staged times the output pre-scale, so o comes out scaled
+  const float v_scale = PVH ? a.o_scale : 1.f;
 
   // The K / V^T stages and the output staging are never live together.
   constexpr int K_BYTES = NP * KV * NCH * 16;
-  constexpr int V_BYTES = NP * HD * VTP * (int)sizeof(T);
+  constexpr int V_BYTES = NPV * HD * VTP * (int)sizeof(TV);
   constexpr int O_BYTES = 4 * 32 * OTP * 4;
   constexpr int ST_BYTES = K_BYTES + V_BYTES;             // one staged tile
   constexpr int SMEM = NB * ST_BYTES > O_BYTES ? NB * ST_BYTES : O_BYTES;
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
-  // tile b: K [NP][KV * NCH] at smem + b * ST_BYTES, V^T [NP][HD * VTP] after it
+  // tile b: K [NP][KV * NCH] at smem + b * ST_BYTES, V^T [NPV][HD * VTP] after it
   auto sK_of = [&](int b) { return (u32x4 *)(smem + b * ST_BYTES); };
-  auto sVt_of = [&](int b) { return (T *)(smem + b * ST_BYTES + K_BYTES); };
+  auto sVt_of = [&](int b) { return (TV *)(smem + b * ST_BYTES + K_BYTES); };
   float *sOall = (float *)smem;                            // [4][32 * OTP]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -208,7 +219,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     }
   };
   // Register slot b -> LDS tile sKb / sVtb.
-  auto lstore = [&](int b, u32x4 *sKb, T *sVtb) {
+  auto lstore = [&](int b, u32x4 *sKb, TV *sVtb) {
 #pragma unroll
     for (int t = 0; t < KCH; ++t) {
       const int idx = tid + t * 256, r = idx / NCH, c = idx % NCH;
@@ -224,16 +235,21 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int t = 0; t < VCH; ++t) {
       const int idx = tid + t * 256, d = idx % HD, v = idx / HD;
-      T vs[NP][EC];
-      split_vals<T, NP, EC>(vx[b][t], vs);
+      TV vs[NPV][EC];
+      if constexpr (PVH) {
 #pragma unroll
-      for (int p = 0; p < NP; ++p) {
-        T *row = sVtb + p * HD * VTP + d * VTP;
+        for (int e = 0; e < EC; ++e) vs[0][e] = from_f32<TV>(vx[b][t][e] * v_scale);
+      } else {
+        split_vals<TV, NPV, EC>(vx[b][t], vs);
+      }
+#pragma unroll
+      for (int p = 0; p < NPV; ++p) {
+        TV *row = sVtb + p * HD * VTP + d * VTP;
         // keys v*EC .. v*EC+EC-1 land in runs of 4 consecutive positions
 #pragma unroll
         for (int e = 0; e < EC; e += 4) {
           const int pos = vt_pos<EPF>(v * EC + e);
-          if constexpr (sizeof(T) == 2) {
+          if constexpr (sizeof(TV) == 2) {
             u32x2 w;
             __builtin_memcpy(&w, &vs[p][e], 8);
             *(u32x2 *)(row + pos) = w;
@@ -247,7 +263,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     }
   };
   // One key/value tile for this wave: scores, online softmax, O update.
-  auto compute = [&](int kv0, const u32x4 *sK, const T *sVt) {
+  auto compute = [&](int kv0, const u32x4 *sK, const TV *sVt) {
     if (!(qw < L && kv0 <= (a.causal ? P + wave_last : P + L - 1))) return;
     // Independent accumulators (one per split product, or per k parity
     // for fp32) so consecutive MFMAs do not wait on each other's results.
@@ -273,11 +289,21 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     f32x16 s = sacc[0] + sacc[1];
     if constexpr (NS == 3) s += sacc[2];
     float mb = -INFINITY;
+    // a tile every query of the wave sees in full needs no mask
+    const bool full = kv0 + KV <= P + L && (!a.causal || kv0 + KV - 1 <= P + qw);
+    if (full) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int kv = kv0 + acc_row(r, lane);
-      s[r] = ((!a.causal || kv <= P + my_q) && kv < P + L) ? s[r] * sc : -INFINITY;
-      mb = fmaxf(mb, s[r]);
+      for (int r = 0; r < 16; ++r) {
+        s[r] *= sc;
+        mb = fmaxf(mb, s[r]);
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int kv = kv0 + acc_row(r, lane);
+        s[r] = ((!a.causal || kv <= P + my_q) && kv < P + L) ? s[r] * sc : -INFINITY;
+        mb = fmaxf(mb, s[r]);
+      }
     }
     mb = warp_max_xor(mb, 32);
     const float m_new = fmaxf(m_i, mb);
@@ -291,33 +317,41 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       ps += p[r];
     }
     l_i = l_i * alpha + ps;
+    // the running max moved for some query of the wave: rescale O
+    if (__any(alpha != 1.f)) {
 #pragma unroll
-    for (int n = 0; n < ND; ++n)
+      for (int n = 0; n < ND; ++n)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[n][r] *= alpha;
+        for (int r = 0; r < 16; ++r) oacc[n][r] *= alpha;
+    }
     // P fragments: element e of fragment f is P value i = EPF*f + e.
-    frag_t pf[NP][NFP];
+    vfrag_t pf[NPV][NFP];
 #pragma unroll
     for (int f = 0; f < NFP; ++f) {
-      T sp[NP][EPF];
-      split_vals<T, NP, EPF>(p + EPF * f, sp);
+      TV sp[NPV][EPF];
+      if constexpr (PVH) {
 #pragma unroll
-      for (int q = 0; q < NP; ++q)
+        for (int e = 0; e < EPF; ++e) sp[0][e] = from_f32<TV>(p[EPF * f + e]);
+      } else {
+        split_vals<TV, NPV, EPF>(p + EPF * f, sp);
+      }
+#pragma unroll
+      for (int q = 0; q < NPV; ++q)
 #pragma unroll
         for (int e = 0; e < EPF; ++e) pf[q][f][e] = sp[q][e];
     }
     // Consecutive MFMAs go to the ND different output blocks.
 #pragma unroll
     for (int f = 0; f < NFP; ++f) {
-      frag_t vf[ND][NP];
+      vfrag_t vf[ND][NPV];
 #pragma unroll
       for (int n = 0; n < ND; ++n)
 #pragma unroll
-        for (int q = 0; q < NP; ++q)
-          vf[n][q] = *(const frag_t *)(sVt + q * HD * VTP + (n * 32 + lrow) * VTP + (2 * f + lgrp) * EPF);
+        for (int q = 0; q < NPV; ++q)
+          vf[n][q] = *(const vfrag_t *)(sVt + q * HD * VTP + (n * 32 + lrow) * VTP + (2 * f + lgrp) * EPF);
 #pragma unroll
       for (int n = 0; n < ND; ++n) mfma32(oacc[n], vf[n][0], pf[0][f]);
-      if constexpr (NP == 2) {
+      if constexpr (NPV == 2) {
 #pragma unroll
         for (int n = 0; n < ND; ++n) mfma32(oacc[n], vf[n][1], pf[0][f]);
 #pragma unroll
@@ -357,7 +391,8 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   // along d (a lane owns a query row in the accumulator layout, which would
   // scatter 2-byte stores across rows).
   const float lt = l_i + __shfl_xor(l_i, 32, kWave);
-  const float inv = (MODE == MODE_F32 ? 1.f : a.o_scale) / lt;
+  // MODE_F16: o times its pre-scale (with PVH the pre-scale came with V)
+  const float inv = ((MODE == MODE_F32 || PVH) ? 1.f : a.o_scale) / lt;
   float *so = sOall + wave * 32 * OTP;
 #pragma unroll
   for (int n = 0; n < ND; ++n)
@@ -387,7 +422,8 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 }
 
 hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int P, void *o, float out_scale,
-                            const int32_t *cu, int batch, int Hq, int Hkv, int d, hipStream_t s, int causal) {
+                            const int32_t *cu, int batch, int Hq, int Hkv, int d, hipStream_t s, int causal,
+                            int pv_f16) {
   const int rep = Hq / Hkv;
   if (P < 0 || (P > 0 && !prefix)) return hipErrorInvalidValue;
   AttnArgs a;
@@ -422,13 +458,15 @@ hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int
     // Sequences of at most 128 tokens: every workgroup stages all of its
     // (at most 4) key/value tiles at once.
     const bool all = P + max_len <= 4 * 32;
-#define MTE_ATTN(M_, D_)                                                             \
-    if (all) hipLaunchKernelGGL((k_attn<M_, D_, 4>), grid, dim3(256), 0, s, a);      \
-    else hipLaunchKernelGGL((k_attn<M_, D_, 1>), grid, dim3(256), 0, s, a);
-    if (mode == MODE_F16) {
-      if (d == 128) { MTE_ATTN(MODE_F16, 128) } else { MTE_ATTN(MODE_F16, 64) }
+#define MTE_ATTN(M_, D_, H_)                                                             \
+    if (all) hipLaunchKernelGGL((k_attn<M_, D_, 4, H_>), grid, dim3(256), 0, s, a);      \
+    else hipLaunchKernelGGL((k_attn<M_, D_, 1, H_>), grid, dim3(256), 0, s, a);
+    if (mode == MODE_F16 && pv_f16) {
+      if (d == 128) { MTE_ATTN(MODE_F16, 128, true) } else { MTE_ATTN(MODE_F16, 64, true) }
+    } else if (mode == MODE_F16) {
+      if (d == 128) { MTE_ATTN(MODE_F16, 128, false) } else { MTE_ATTN(MODE_F16, 64, false) }
     } else {
-      if (d == 128) { MTE_ATTN(MODE_F32, 128) } else { MTE_ATTN(MODE_F32, 64) }
+      if (d == 128) { MTE_ATTN(MODE_F32, 128, false) } else { MTE_ATTN(MODE_F32, 64, false) }
     }
 #undef MTE_ATTN
     hipError_t e = hipGetLastError();

@@ -124,10 +124,12 @@ hipError_t launch_qkv_parts(float *qkv, const float *parts, int nparts, int T, i
 // its own keys, or P = 0. o: [T, Hq*d], float (MODE_F32) or fp16
 // (MODE_F16) times out_scale. cu: host int32[batch+1] sequence offsets.
 // Launches in chunks of <= 256 sequences. causal = 0: bidirectional (every
-// query attends to all keys of its own sequence).
+// query attends to all keys of its own sequence). pv_f16 (MODE_F16): P and V
+// rounded once to fp16 for one fp16 MFMA instead of the three-product bf16
+// split (scores keep the split either way).
 hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int P, void *o, float out_scale,
                             const int32_t *cu, int batch, int Hq, int Hkv, int d, hipStream_t s,
-                            int causal = 1);
+                            int causal = 1, int pv_f16 = 0);
 
 // Positions of packed sequences (see mte_build_positions).
 hipError_t launch_positions(const int32_t *layouts5, int batch, int32_t *pos_thw, int T,

@@ -315,7 +315,7 @@ int mte_vision_encode(mte_vision *e, const void *pixels, int32_t n, int32_t H, i
     MTE_TRY(launch_layernorm(e->h, L.ln1_g, L.ln1_b, af, e->xn, T, D, c.ln_eps, s));
     MTE_TRY(launch_gemm(mode, EPI_QKV, e->xn, L.w_qkv, e->qkv, T, 3 * D, D, 3 * D, L.s_qkv, 1.f, nullptr, 0, &sp,
                         &qe, s, nullptr, L.b_qkv));
-    MTE_TRY(launch_attention(mode, e->qkv, nullptr, 0, e->attn, L.o_pre, cu.data(), n, nh, nh, hd, s, 0));
+    MTE_TRY(launch_attention(mode, e->qkv, nullptr, 0, e->attn, L.o_pre, cu.data(), n, nh, nh, hd, s, 0, 1));
     MTE_TRY(launch_gemm(mode, EPI_RESID, e->attn, L.w_o, e->h, T, D, D, D, L.s_o, 1.f, nullptr, 0, &sp, nullptr, s,
                         nullptr, L.b_o));
     MTE_TRY(launch_layernorm(e->h, L.ln2_g, L.ln2_b, af, e->xn, T, D, c.ln_eps, s));

@@ -119,10 +119,70 @@ __global__ __launch_bounds__(256) void k_layernorm(const float *__restrict__ x, 
   }
 }
 
+// The same with one wave per row (four rows per block) for D a multiple of
+// 256: each lane holds NV 16-byte groups of the row (coalesced loads), and
+// both reductions stay inside the wave.
+template <typename TO, int NV>
+__global__ __launch_bounds__(256) void k_layernorm_wave(const float *__restrict__ x, const float *__restrict__ g,
+                                                        const float *__restrict__ b, TO *__restrict__ y, int rows,
+                                                        int D, float eps) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const float *xr = x + (size_t)row * D;
+  f32x4 v[NV];
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    v[k] = *(const f32x4 *)(xr + 4 * (lane + 64 * k));
+    s += (v[k][0] + v[k][1]) + (v[k][2] + v[k][3]);
+  }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) s = warp_sum_xor(s, m);
+  const float mean = s / (float)D;
+  float q = 0.f;
+#pragma unroll
+  for (int k = 0; k < NV; ++k)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float d = v[k][e] - mean;
+      q += d * d;
+    }
+#pragma unroll
+  for (int m = 32; m >= 1; m >>= 1) q = warp_sum_xor(q, m);
+  const float rs = rsqrtf(q / (float)D + eps);
+  TO *yr = y + (size_t)row * D;
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int c = 4 * (lane + 64 * k);
+    const f32x4 gg = *(const f32x4 *)(g + c), bb = *(const f32x4 *)(b + c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) yr[c + e] = from_f32<TO>((v[k][e] - mean) * rs * gg[e] + bb[e]);
+  }
+}
+
+template <typename TO>
+static bool layernorm_wave(const float *x, const float *g, const float *b, TO *y, int rows, int D, float eps,
+                           hipStream_t s) {
+  const dim3 grid((rows + 3) / 4);
+  switch (D / 256) {
+#define MTE_LN(nv) case nv: hipLaunchKernelGGL((k_layernorm_wave<TO, nv>), grid, dim3(256), 0, s, x, g, b, y, rows, D, eps); return true;
+    MTE_LN(1) MTE_LN(2) MTE_LN(3) MTE_LN(4) MTE_LN(6) MTE_LN(8) MTE_LN(12) MTE_LN(16)
+#undef MTE_LN
+  }
+  return false;
+}
+
 hipError_t launch_layernorm(const float *x, const float *g, const float *b, int out_fmt, void *y, int rows, int D,
                             float eps, hipStream_t s) {
   if (rows <= 0) return hipSuccess;
   if (D > 256 * kLnPer) return hipErrorInvalidValue;
+  if (D % 256 == 0 && ((uintptr_t)x | (uintptr_t)g | (uintptr_t)b) % 16 == 0) {
+    const bool ok = out_fmt == FMT_F16 ? layernorm_wave(x, g, b, (f16 *)y, rows, D, eps, s)
+                    : out_fmt == FMT_F32 ? layernorm_wave(x, g, b, (float *)y, rows, D, eps, s)
+                                         : false;
+    if (ok) return hipGetLastError();
+  }
   if (out_fmt == FMT_F16)
     hipLaunchKernelGGL(k_layernorm<f16>, dim3(rows), dim3(256), 0, s, x, g, b, (f16 *)y, D, eps);
   else if (out_fmt == FMT_F32)
