@@ -416,6 +416,74 @@ def run_vision(torch, steps, warmup, n=16, side=256):
             "flops_per_step": fl}
 
 
+def run_pipeline(torch, steps, warmup, n=16, side=256):
+    """Source frames to conditioning hidden states: n 256x256 frames through the vision
+    tower, whose image tokens land (strided) in the packed decoder input next to each
+    frame's 32 instruction embeddings, then positions and the 28-layer decoder; one
+    captured graph per step."""
+    from paper_2606_05981_amd import binding as B
+    from paper_2606_05981_amd.encoder import TextEncoder, VisionEncoder
+    from synth import vision as SV
+    from synth import workloads as W
+    v = SV.VDIMS_FULL
+    wl = W.workload("stack_b16")
+    dims = wl.dims
+    lens = W.seq_lens(wl.layouts)
+    L, T = lens[0], sum(lens)
+    tpi = v.tokens_per_image(side, side)
+    assert len(lens) == n and all(x == L for x in lens) and all(s.n_text_before == 0 and s.n_image == tpi
+                                                                 for s in wl.layouts)
+    vcfg = B.make_vision_config(v.depth, v.hidden, v.n_heads, v.head_dim, v.ffn, patch=v.patch, merge=v.merge,
+                                in_channels=v.in_channels, out_hidden=dims.hidden, ln_eps=v.ln_eps,
+                                rope_theta=v.rope_theta, dtype=B.MTE_BF16, out_dtype=B.MTE_BF16,
+                                max_images=n, max_side=side)
+    venc = VisionEncoder.from_host(vcfg, SV.outer_weights(v.with_(out_hidden=dims.hidden)),
+                                   (SV.block_weights(v, l) for l in range(v.depth)))
+    cfg = B.make_config(dims.n_layers, dims.hidden, dims.n_q_heads, dims.n_kv_heads, dims.head_dim, dims.ffn,
+                        rms_eps=dims.rms_eps, rope_theta=dims.rope_theta, mrope_section=dims.mrope_section,
+                        mrope_layout=dims.mrope_layout, qk_norm=dims.qk_norm, dtype=B.MTE_BF16,
+                        out_dtype=B.MTE_F32, max_tokens=T, max_batch=n, max_seq=L)
+    tenc = TextEncoder.from_host(cfg, (W.layer_weights(dims, l) for l in range(dims.n_layers)),
+                                 W.final_norm_gain(dims))
+    px = torch.from_numpy(SV.images(v, n, side, side)).to("cuda", torch.bfloat16)
+    # the packed decoder input: the instruction rows are filled once; the image rows by every step
+    emb = torch.from_numpy(W.embeddings(dims, wl.layouts)).to("cuda", torch.bfloat16)
+    out = torch.empty((T, dims.hidden), dtype=torch.float32, device="cuda")
+    pos = torch.empty((3, T), dtype=torch.int32, device="cuda")
+    layouts = [(s.n_text_before, s.grid_t, s.grid_h, s.grid_w, s.n_text_after) for s in wl.layouts]
+
+    def step(st):
+        venc.encode(px, out=emb, image_stride=L, stream=st)
+        B.mte_build_positions(layouts, pos.data_ptr(), st.cuda_stream)
+        B.mte_encode(tenc.handle, emb.data_ptr(), pos.data_ptr(), lens, n, out.data_ptr(), st.cuda_stream)
+
+    cur = torch.cuda.current_stream()
+    for _ in range(warmup):
+        step(cur)
+    torch.cuda.synchronize()
+    side_s = torch.cuda.Stream()
+    side_s.wait_stream(cur)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side_s):
+        with torch.cuda.graph(graph, stream=side_s):
+            step(side_s)
+    cur.wait_stream(side_s)
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    venc.close()
+    tenc.close()
+    return {"workload": f"{n} frames: {side}x{side} source through the vision tower ({tpi} image tokens each, "
+                        f"written into the packed decoder input) + {L - tpi} instruction tokens, 28-layer decoder",
+            "ms_per_step": round(dt * 1e3, 4), "frames_per_s": round(n / dt, 1),
+            "ms_per_frame": round(dt * 1e3 / n, 4)}
+
+
 def copy_calibration(torch, mib=512, reps=5):
     """A plain device-to-device copy of `mib` MiB, `reps` times: the known-size kernel
     that calibrates the FETCH_SIZE / WRITE_SIZE counters (each dispatch moves exactly
@@ -443,6 +511,8 @@ def main():
                     help="also measure frames sharing a prefix of this many text tokens")
     ap.add_argument("--no-e4m3", action="store_true",
                     help="skip the runs with e4m3 weights (batch 1 and the main workload)")
+    ap.add_argument("--no-pipeline", action="store_true",
+                    help="skip the frames -> vision tower -> decoder run")
     ap.add_argument("--vision-only", action="store_true",
                     help="only run the vision tower and print its figures (for profiling)")
     ap.add_argument("--no-vision", action="store_true",
@@ -523,6 +593,8 @@ def main():
                                           "bytes_per_step": wbytes}}
     if not args.no_vision:
         res["vision_tower"] = run_vision(torch, K, args.warmup)
+        if not args.no_pipeline:
+            res["frames_to_hidden"] = run_pipeline(torch, K, args.warmup)
     if not args.no_e4m3:
         res["e4m3_weights"] = run_e4m3(torch, args.workload, K, args.warmup, dims, not args.no_batch1)
     if args.overlap:

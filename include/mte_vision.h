@@ -105,6 +105,15 @@ int mte_vision_create(const mte_vision_config *cfg, const mte_vision_weights *w,
 int mte_vision_encode(mte_vision *enc, const void *pixels, int32_t n_images, int32_t height, int32_t width,
                       void *out, hipStream_t stream);
 
+/* The same with image i's tokens written to rows [i*image_stride,
+ * i*image_stride + tokens per image) of out (image_stride >= tokens per
+ * image; the rows in between are left untouched), so that the image tokens
+ * land directly in a packed text-encoder input (mte_encode's embeds) whose
+ * sequences each start with their image grid. Errors as mte_vision_encode,
+ * and MTE_E_INVALID for a stride below the tokens per image. */
+int mte_vision_encode_strided(mte_vision *enc, const void *pixels, int32_t n_images, int32_t height,
+                              int32_t width, void *out, int32_t image_stride, hipStream_t stream);
+
 /* Frees the encoder (synchronises its device); NULL is a no-op. */
 void mte_vision_destroy(mte_vision *enc);
 

@@ -106,6 +106,7 @@ _sig = {
     "mte_vision_create": (C.c_int, [C.POINTER(mte_vision_config), C.POINTER(mte_vision_weights), _P,
                                     C.POINTER(_P)]),
     "mte_vision_encode": (C.c_int, [_P, _P, C.c_int32, C.c_int32, C.c_int32, _P, _P]),
+    "mte_vision_encode_strided": (C.c_int, [_P, _P, C.c_int32, C.c_int32, C.c_int32, _P, C.c_int32, _P]),
     "mte_vision_destroy": (None, [_P]),
 }
 for _name, (_res, _args) in _sig.items():
@@ -262,3 +263,9 @@ def mte_vision_encode(enc: int, pixels: int, n_images: int, height: int, width: 
 
 def mte_vision_destroy(enc: int) -> None:
     lib.mte_vision_destroy(enc)
+
+
+def mte_vision_encode_strided(enc: int, pixels: int, n_images: int, height: int, width: int, out: int,
+                              image_stride: int, stream: int) -> int:
+    return _check(lib.mte_vision_encode_strided(enc, pixels, n_images, height, width, out, image_stride, stream),
+                  "mte_vision_encode_strided")

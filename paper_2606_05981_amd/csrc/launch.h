@@ -167,6 +167,11 @@ hipError_t launch_patch_positions(int32_t *pos, int n, int H, int W, int patch, 
 hipError_t launch_layernorm(const float *x, const float *g, const float *b, int out_fmt, void *y, int rows, int D,
                             float eps, hipStream_t s);
 
+// dst row (r / group) * group_stride + r % group = src row r of a float
+// [rows, cols] matrix (dst FMT_F32 or FMT_BF16); the other dst rows are untouched.
+hipError_t launch_scatter_rows(const float *src, int dst_fmt, void *dst, int rows, int cols, int group,
+                               int group_stride, hipStream_t s);
+
 // OCP e4m3 quantisation of the rows of a [rows, cols] matrix (format src_fmt,
 // FMT_F32 or FMT_BF16): row r gets the scale 2^e_r with e_r the smallest
 // integer such that max_c |src[r, c]| <= 448 * 2^e_r (e_r = 0 for an

@@ -286,10 +286,19 @@ int mte_vision_create(const mte_vision_config *cfg, const mte_vision_weights *w,
 
 int mte_vision_encode(mte_vision *e, const void *pixels, int32_t n, int32_t H, int32_t W, void *out,
                       hipStream_t s) {
+  if (!e || H <= 0 || W <= 0) return MTE_E_INVALID;
+  const int side = e->cfg.patch * e->cfg.merge;
+  return mte_vision_encode_strided(e, pixels, n, H, W, out, (H / side) * (W / side), s);
+}
+
+int mte_vision_encode_strided(mte_vision *e, const void *pixels, int32_t n, int32_t H, int32_t W, void *out,
+                              int32_t image_stride, hipStream_t s) {
   if (!e || !pixels || !out || n <= 0 || H <= 0 || W <= 0) return MTE_E_INVALID;
   const mte_vision_config &c = e->cfg;
   const int side = c.patch * c.merge;
   if (H % side || W % side) return MTE_E_INVALID;
+  const int tpi = (H / side) * (W / side);
+  if (image_stride < tpi || (int64_t)image_stride * n > (1 << 24)) return MTE_E_INVALID;
   if (n > c.max_images || H > c.max_side || W > c.max_side) return MTE_E_CAPACITY;
   int cur = -1;
   if (hipGetDevice(&cur) != hipSuccess) return MTE_E_HIP;
@@ -329,13 +338,14 @@ int mte_vision_encode(mte_vision *e, const void *pixels, int32_t n, int32_t H, i
   MTE_TRY(launch_layernorm(e->h, e->mln_g, e->mln_b, af, e->xn, T, D, c.ln_eps, s));
   MTE_TRY(launch_gemm(mode, EPI_GELU, e->xn, e->w_m1, e->mact, Tm, MD, MD, MD, e->s_m1, e->m_pre, nullptr, 0, &sp,
                       nullptr, s, nullptr, e->b_m1));
-  if (c.out_dtype == MTE_F32) {
+  if (c.out_dtype == MTE_F32 && image_stride == tpi) {
     MTE_TRY(launch_gemm(mode, EPI_STORE, e->mact, e->w_m2, out, Tm, DO, MD, DO, e->s_m2, 1.f, nullptr, 0, &sp,
                         nullptr, s, nullptr, e->b_m2));
   } else {
     MTE_TRY(launch_gemm(mode, EPI_STORE, e->mact, e->w_m2, e->mout, Tm, DO, MD, DO, e->s_m2, 1.f, nullptr, 0, &sp,
                         nullptr, s, nullptr, e->b_m2));
-    MTE_TRY(launch_convert_rows(FMT_F32, e->mout, FMT_BF16, out, Tm, DO, 1.f, 0, 0, s));
+    MTE_TRY(launch_scatter_rows(e->mout, c.out_dtype == MTE_F32 ? FMT_F32 : FMT_BF16, out, Tm, DO, tpi,
+                                image_stride, s));
   }
 #undef MTE_TRY
 done:

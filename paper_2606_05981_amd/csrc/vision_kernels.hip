@@ -192,4 +192,31 @@ hipError_t launch_layernorm(const float *x, const float *g, const float *b, int 
   return hipGetLastError();
 }
 
+// dst row (r / group) * group_stride + r % group = src row r (float src,
+// dst FMT_F32 or FMT_BF16 rounded to nearest even); other dst rows untouched.
+template <typename TD>
+__global__ __launch_bounds__(256) void k_scatter_rows(const float *__restrict__ src, TD *__restrict__ dst, int cols,
+                                                      int group, int group_stride) {
+  const int r = blockIdx.x;
+  const size_t dr = (size_t)(r / group) * group_stride + r % group;
+  const float *sr = src + (size_t)r * cols;
+  TD *d = dst + dr * cols;
+  for (int c = threadIdx.x; c < cols; c += 256) d[c] = from_f32<TD>(sr[c]);
+}
+
+hipError_t launch_scatter_rows(const float *src, int dst_fmt, void *dst, int rows, int cols, int group,
+                               int group_stride, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  if (group <= 0 || group_stride < group) return hipErrorInvalidValue;
+  if (dst_fmt == FMT_F32)
+    hipLaunchKernelGGL(k_scatter_rows<float>, dim3(rows), dim3(256), 0, s, src, (float *)dst, cols, group,
+                       group_stride);
+  else if (dst_fmt == FMT_BF16)
+    hipLaunchKernelGGL(k_scatter_rows<bf16>, dim3(rows), dim3(256), 0, s, src, (bf16 *)dst, cols, group,
+                       group_stride);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
 }  // namespace mte

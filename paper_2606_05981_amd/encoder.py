@@ -158,18 +158,25 @@ class VisionEncoder:
                    [{k: put(L[k]) for k in B.VISION_LAYER_FIELDS} for L in layer_arrays])
 
     def encode(self, pixels: torch.Tensor, out: Optional[torch.Tensor] = None,
-               stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
-        """pixels [n, C, H, W] of the config dtype -> [n * tokens per image, out_hidden]."""
+               stream: Optional[torch.cuda.Stream] = None, image_stride: Optional[int] = None) -> torch.Tensor:
+        """pixels [n, C, H, W] of the config dtype -> [n * tokens per image, out_hidden], or with
+        image_stride image i's tokens at rows i*image_stride.. of `out` (mte_vision_encode_strided)."""
         c = self.cfg
         if pixels.dim() != 4 or pixels.dtype != self.dtype or not pixels.is_contiguous() or \
                 pixels.shape[1] != c.in_channels:
             raise ValueError("pixels must be a contiguous [n, C, H, W] tensor of the encoder dtype")
         n, _, h, w = pixels.shape
         s = c.patch * c.merge
-        rows = n * (h // s) * (w // s)
+        tpi = (h // s) * (w // s)
+        stride = tpi if image_stride is None else int(image_stride)
+        rows = (n - 1) * stride + tpi
         if out is None:
             out = torch.empty((rows, c.out_hidden), dtype=self.out_dtype, device=pixels.device)
-        B.mte_vision_encode(self.handle, pixels.data_ptr(), n, h, w, out.data_ptr(), _stream(stream))
+        if out.dtype != self.out_dtype or not out.is_contiguous() or out.dim() != 2 or \
+                out.shape[1] != c.out_hidden or out.shape[0] < rows:
+            raise ValueError("out must be a contiguous [rows, out_hidden] tensor of the output dtype")
+        B.mte_vision_encode_strided(self.handle, pixels.data_ptr(), n, h, w, out.data_ptr(), stride,
+                                    _stream(stream))
         return out
 
     def close(self) -> None:

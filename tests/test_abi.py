@@ -27,7 +27,8 @@ def test_header_declares_the_boundary():
     for n in ("mte_encoder_create", "mte_encode", "mte_build_positions", "mte_encoder_destroy",
               "mte_status_string", "mte_config_validate", "mte_check_batch", "mte_encode_layers",
               "mte_encoder_reserve_prefix", "mte_encode_prefixed", "mte_quantize_e4m3_rows",
-              "mte_vision_config_validate", "mte_vision_create", "mte_vision_encode", "mte_vision_destroy"):
+              "mte_vision_config_validate", "mte_vision_create", "mte_vision_encode", "mte_vision_destroy",
+              "mte_vision_encode_strided"):
         assert n in names
 
 
@@ -173,6 +174,7 @@ def test_vision_configs(B):
 
 def test_vision_rejects_bad_arguments(B):
     assert B.lib.mte_vision_encode(None, 4096, 1, 256, 256, 8192, None) == -1
+    assert B.lib.mte_vision_encode_strided(None, 4096, 1, 256, 256, 8192, 96, None) == -1
     h = ctypes.c_void_p()
     good = _vision(B)
     w = B.mte_vision_weights()

@@ -110,3 +110,23 @@ def test_vision_bf16_full_depth(torch):
     err = rel_err(got, ref)
     _say("  err", err)
     assert err <= TOL_DEEP
+
+
+def test_vision_strided_output_lands_in_place(torch):
+    """Image tokens written at a row stride into a prefilled buffer (the layout of a packed
+    text-encoder input): the token rows equal the dense output bit for bit, the rows between
+    images keep their contents."""
+    v = SV.VDIMS_TINY
+    img = SV.images(v, 3, 64, 96)
+    enc = _encoder(v, max_side=96)
+    dense = enc.encode(torch.from_numpy(img).cuda())
+    tpi, stride = 6, 11
+    buf = torch.full(((3 - 1) * stride + tpi + 2, v.out_hidden), 7.0, device="cuda")
+    enc.encode(torch.from_numpy(img).cuda(), out=buf, image_stride=stride)
+    torch.cuda.synchronize()
+    enc.close()
+    for i in range(3):
+        assert torch.equal(buf[i * stride:i * stride + tpi], dense[i * tpi:(i + 1) * tpi])
+        if i < 2:
+            assert bool((buf[i * stride + tpi:(i + 1) * stride] == 7.0).all())
+    assert bool((buf[2 * stride + tpi:] == 7.0).all())
