@@ -130,3 +130,26 @@ def test_vision_strided_output_lands_in_place(torch):
         if i < 2:
             assert bool((buf[i * stride + tpi:(i + 1) * stride] == 7.0).all())
     assert bool((buf[2 * stride + tpi:] == 7.0).all())
+
+
+def test_vision_rejects_bad_shapes_and_capacity(torch):
+    """Host-side checks of mte_vision_encode with a live encoder: nothing is enqueued."""
+    from paper_2606_05981_amd import binding as B
+    v = SV.VDIMS_TINY
+    enc = _encoder(v, max_images=2, max_side=64)
+    px = torch.zeros((3, 3, 64, 64), dtype=torch.float32, device="cuda")
+    out = torch.empty((64, v.out_hidden), dtype=torch.float32, device="cuda")
+    h, p, o = enc.handle, px.data_ptr(), out.data_ptr()
+    assert B.lib.mte_vision_encode(h, p, 3, 64, 64, o, None) == -2        # more images than max_images
+    assert B.lib.mte_vision_encode(h, p, 1, 96, 64, o, None) == -2        # taller than max_side
+    assert B.lib.mte_vision_encode(h, p, 1, 48, 64, o, None) == -1        # not a multiple of patch * merge
+    assert B.lib.mte_vision_encode(h, p, 0, 64, 64, o, None) == -1        # no images
+    assert B.lib.mte_vision_encode(h, None, 1, 64, 64, o, None) == -1
+    assert B.lib.mte_vision_encode_strided(h, p, 2, 64, 64, o, 3, None) == -1   # stride below 4 tokens
+    # one 32x32 image: a single image token, a single merge group
+    img = SV.images(v, 1, 32, 32)
+    got = enc.encode(torch.from_numpy(img).cuda())
+    torch.cuda.synchronize()
+    enc.close()
+    ref = _oracle(v, img)
+    assert got.shape == (1, v.out_hidden) and rel_err(got.cpu().numpy(), ref) <= TOL_F32
