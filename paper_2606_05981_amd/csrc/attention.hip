@@ -198,8 +198,44 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   constexpr int VCH = HD * (KV / EC) / 256;       // V column groups per thread
   static_assert(KCH * 256 == KV * NCH && VCH * 256 == HD * (KV / EC), "staging split");
   float kx[NB][KCH][EC], vx[NB][VCH][EC];
-  // Global loads of the tile at kv0 into register slot b.
+  // This thread's element offsets inside a tile of KV consecutive rows of
+  // pitch ld: K chunk t (row idx / NCH, chunk idx % NCH), V column group t
+  // (rows v*EC.., column d). 32-bit: a tile spans at most KV * ld elements.
+  const int ldi = a.ld_qkv;
+  int koff[KCH], voff[VCH];
+#pragma unroll
+  for (int t = 0; t < KCH; ++t) {
+    const int idx = tid + t * 256;
+    koff[t] = (idx / NCH) * ldi + k_off + (idx % NCH) * EC;
+  }
+#pragma unroll
+  for (int t = 0; t < VCH; ++t) {
+    const int idx = tid + t * 256;
+    voff[t] = (idx / HD) * EC * ldi + v_off + idx % HD;
+  }
+  // Global loads of the tile at kv0 into register slot b. A tile wholly
+  // inside the sequence's own keys or wholly inside the prefix is one block
+  // of rows at a workgroup-uniform base; the tile that straddles the prefix
+  // boundary or the end of the sequence goes row by row (clamped rows read
+  // the sequence's last key, whose scores are masked).
   auto gload = [&](int b, int kv0) {
+    const bool own = kv0 >= P && kv0 + KV <= P + L;
+    const bool pre = kv0 + KV <= P;
+    if (own || pre) {
+      const float *tb = own ? a.qkv + base + (size_t)(kv0 - P) * ld : a.pre + (size_t)kv0 * ld;
+#pragma unroll
+      for (int t = 0; t < KCH; ++t)
+#pragma unroll
+        for (int e = 0; e < EC; e += 4) {
+          const f32x4 v = *(const f32x4 *)(tb + koff[t] + e);
+          kx[b][t][e] = v[0]; kx[b][t][e + 1] = v[1]; kx[b][t][e + 2] = v[2]; kx[b][t][e + 3] = v[3];
+        }
+#pragma unroll
+      for (int t = 0; t < VCH; ++t)
+#pragma unroll
+        for (int e = 0; e < EC; ++e) vx[b][t][e] = tb[voff[t] + e * ldi];
+      return;
+    }
 #pragma unroll
     for (int t = 0; t < KCH; ++t) {
       const int idx = tid + t * 256, c = idx % NCH;
