@@ -133,9 +133,21 @@ def run_workload(torch, name, steps, warmup, timing_class=None, use_graph=True, 
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     gpu_ms = wall * 1e3
+    # per-step spread: HIP events around each of `steps` further replays
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for e0, e1 in evs:
+        e0.record()
+        run_step()
+        e1.record()
+    torch.cuda.synchronize()
+    per = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+    mean = sum(per) / len(per)
+    sd = (sum((x - mean) ** 2 for x in per) / max(len(per) - 1, 1)) ** 0.5
+    stats = {"median_ms": round(per[len(per) // 2], 4), "mean_ms": round(mean, 4), "sd_ms": round(sd, 4),
+             "steps": len(per)}
     enc.close()
     return dict(name=name, dims=dims, lens=lens, T=T, wall_s=wall, gpu_ms=gpu_ms, kern=kern,
-                eager_s=eager_s, graph=graph is not None)
+                eager_s=eager_s, graph=graph is not None, stats=stats)
 
 
 def cpu_baseline(min_seconds=10.0):
@@ -168,8 +180,14 @@ def cpu_baseline(min_seconds=10.0):
         dt = time.perf_counter() - t0
         if dt >= min_seconds:
             break
+    cpu = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
     return {"value": round(toks / dt, 2), "unit": "tokens/s", "cores": int(cores),
-            "kind": "oracle",
+            "kind": "oracle", "cpu_model": cpu, "host_cpus": os.cpu_count(),
             "sample": f"{frames} frame(s) of the 16 x 96-token batch, each a whole 28-layer "
                       f"forward ({toks} tokens in {dt:.1f} s, fp64 numpy oracle)"}
 
@@ -484,6 +502,26 @@ def run_pipeline(torch, steps, warmup, n=16, side=256):
             "ms_per_frame": round(dt * 1e3 / n, 4)}
 
 
+def copy_bandwidth(torch, mib=1024, reps=10):
+    """Achieved HBM bandwidth of a plain device copy (read + write bytes / time): the
+    measured counterpart of the published 8 TB/s, for context."""
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    dt = e0.elapsed_time(e1) / 1e3 / reps
+    del src, dst
+    return round(2 * mib * (1 << 20) / dt / 1e9, 1)
+
+
 def copy_calibration(torch, mib=512, reps=5):
     """A plain device-to-device copy of `mib` MiB, `reps` times: the known-size kernel
     that calibrates the FETCH_SIZE / WRITE_SIZE counters (each dispatch moves exactly
@@ -570,6 +608,8 @@ def main():
                    "batch": len(main_run["lens"]), "tokens_per_step": T},
         "frames_per_s": round(frames_s, 1),
         "step_launch": "HIP graph replay" if main_run["graph"] else "eager",
+        "step_ms_stats": main_run["stats"],
+        "hbm_copy_gbs_measured": copy_bandwidth(torch),
         "eager_ms_per_step": round(main_run["eager_s"] * 1e3 / K, 4),
         "model_tflops": round(total_tflops, 1),
         "roofline": {"kernel": "gate/up GEMM + SwiGLU", "bound": "mfma",
@@ -586,6 +626,7 @@ def main():
         res["batch1"] = {"workload": "stack_b1: 1 frame x 96 tokens, 28 layers",
                          "tokens_per_s": round(b1["T"] / t1, 1), "frames_per_s": round(1 / t1, 1),
                          "ms_per_step": round(t1 * 1e3, 4),
+                         "step_ms_stats": b1["stats"],
                          "eager_ms_per_step": round(b1["eager_s"] * 1e3 / K, 4),
                          "hbm_roofline": {"bound": "hbm", "achieved": round(wbytes / t1 / 1e9, 1),
                                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
