@@ -68,11 +68,16 @@ struct GemmArgs {
   const float *bias;  // [N] added to the product before the epilogue (unsplit launches), or null
 };
 
-// tanh-approximated GELU: 0.5 z (1 + tanh(sqrt(2/pi) (z + 0.044715 z^3))).
+// tanh-approximated GELU, 0.5 z (1 + tanh(u)) with u = sqrt(2/pi) (z + 0.044715 z^3),
+// evaluated as z * sigmoid(2u) = z / (1 + exp(-2u)) (the same function): one
+// exp and one hardware reciprocal (1 ulp) instead of a library tanh. Large
+// negative z: exp overflows to inf and the result is 0.
 __device__ __forceinline__ float gelu_tanh(float z) {
-  const float u = 0.7978845608028654f * (z + 0.044715f * z * z * z);
-  return 0.5f * z * (1.f + tanhf(u));
+  const float m2u = -1.5957691216057308f * z * (1.f + 0.044715f * z * z);
+  return z * __builtin_amdgcn_rcpf(1.f + __expf(m2u));
 }
+// silu(z) = z / (1 + exp(-z)), with the hardware reciprocal.
+__device__ __forceinline__ float silu_f(float z) { return z * __builtin_amdgcn_rcpf(1.f + __expf(-z)); }
 
 // Chunk swizzles for rows of 128 bytes (8 chunks) and 64 bytes (4 chunks):
 // the 16-byte fragment reads (32 consecutive rows at one logical chunk, the
@@ -462,7 +467,7 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
           const float recv = __shfl_xor(upl ? a0 : a1, 16, kWave);
           const float gt = upl ? recv : a0, up = upl ? a1 : recv;
           const int m = m0 + wm * WTM + i * 32 + acc_row(r + (upl ? 1 : 0), lane);
-          const float y = gt / (1.f + __expf(-gt)) * up * g.out_scale;
+          const float y = silu_f(gt) * up * g.out_scale;
           if (m < M) {
             const size_t o = (size_t)m * g.ldc + f;
             if constexpr (MODE == MODE_F32) ((float *)g.C)[o] = y;

@@ -276,7 +276,7 @@ __global__ __launch_bounds__(256) void k_swiglu_parts(Parts pt, int F, void *__r
       gt += qg[k];
       up += qu[k];
     }
-  const float y = gt / (1.f + __expf(-gt)) * up * out_scale;
+  const float y = gt * __builtin_amdgcn_rcpf(1.f + __expf(-gt)) * up * out_scale;   // silu(gate) * up
   if constexpr (OUT_FMT == FMT_F32) ((float *)out)[i] = y;
   else ((f16 *)out)[i] = (f16)y;
 }
