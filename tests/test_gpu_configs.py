@@ -50,3 +50,29 @@ def test_shape_variants(case):
     print(f"  {case}: one layer {e1:.3e}, two layers {e2:.3e}", file=sys.stderr, flush=True)
     assert e1 <= TOL_LAYER
     assert e2 <= TOL_STACK
+
+
+def test_long_sequences_one_layer():
+    """Long sequences at full width, one layer from the oracle's input: a 2048-token sequence
+    (a 32x32 image grid and 1024 text tokens; 64 causal query tiles, keys staged tile by tile)
+    packed with a 1003-token one whose last key tile is partial."""
+    import torch
+    from paper_2606_05981_amd.encoder import build_positions
+    assert torch.cuda.is_available(), "no GPU"
+    dims = W.DIMS_FULL.with_(n_layers=1)
+    layouts = (W.SeqLayout(0, 1, 32, 32, 1024), W.SeqLayout(11, 1, 28, 30, 152))
+    emb = W.embeddings(dims, layouts)
+    lens = W.seq_lens(layouts)
+    print("long sequences", lens, file=sys.stderr, flush=True)
+    enc = make_encoder(dims, max_tokens=sum(lens), max_batch=2, max_seq=max(lens))
+    h_in = torch.from_numpy(emb.astype(np.float32)).cuda()
+    h = enc.encode_layers(h_in, build_positions(layout_tuples(layouts)), lens, 0, 1)
+    torch.cuda.synchronize()
+    enc.close()
+    ref = O.layer_forward(emb, O.positions(layouts), lens, W.layer_weights(dims, 0), dims)
+    got = h.cpu().numpy()
+    err = rel_err(got, ref)
+    print("  err", err, file=sys.stderr, flush=True)
+    assert err <= TOL_LAYER
+    s = lens[0]
+    assert rel_err(got[:s], ref[:s]) <= TOL_LAYER and rel_err(got[s:], ref[s:]) <= TOL_LAYER

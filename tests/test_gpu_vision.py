@@ -99,6 +99,22 @@ def test_vision_bf16_two_blocks(torch):
     assert y16.dtype == torch.bfloat16 and torch.equal(y16, y32.to(torch.bfloat16))
 
 
+def test_vision_bf16_512_source(torch):
+    """A 512x512 source (1024 patches, 256 image tokens: the 16x16 grid of the long-sequence
+    decoder configuration), two full-width blocks: attention over 1024 keys."""
+    v = SV.VDIMS_FULL.with_(depth=2)
+    img = SV.images(v, 1, 512, 512)
+    _say("vision bf16, 2 blocks, one 512x512 image")
+    enc = _encoder(v, max_images=1, max_side=512)
+    got = _run(torch, enc, v, img)
+    enc.close()
+    ref = _oracle(v, img)
+    assert got.shape == (256, v.out_hidden)
+    err = rel_err(got, ref)
+    _say("  err", err)
+    assert err <= TOL_SHORT
+
+
 def test_vision_bf16_full_depth(torch):
     v = SV.VDIMS_FULL
     img = SV.images(v, 1, 256, 256)
