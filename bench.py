@@ -522,6 +522,24 @@ def copy_bandwidth(torch, mib=1024, reps=10):
     return round(2 * mib * (1 << 20) / dt / 1e9, 1)
 
 
+def mfma_rate(torch, blocks=512, iters=20000):
+    """Dense fp16 matrix-core rate the device sustains under load (mte_probe_mfma: independent
+    32x32x16 MFMA chains, no memory traffic), TFLOP/s: the measured counterpart of the
+    published 2.5 PFLOP/s, which assumes the 2.4 GHz peak clock."""
+    from paper_2606_05981_amd import binding as B
+    sink = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    st = torch.cuda.current_stream().cuda_stream
+    B.mte_probe_mfma(blocks, iters // 10, sink.data_ptr(), st)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    B.mte_probe_mfma(blocks, iters, sink.data_ptr(), st)
+    e1.record()
+    torch.cuda.synchronize()
+    flops = blocks * 4 * iters * 8 * 32768
+    return round(flops / (e0.elapsed_time(e1) / 1e3) / 1e12, 1)
+
+
 def copy_calibration(torch, mib=512, reps=5):
     """A plain device-to-device copy of `mib` MiB, `reps` times: the known-size kernel
     that calibrates the FETCH_SIZE / WRITE_SIZE counters (each dispatch moves exactly
@@ -610,6 +628,7 @@ def main():
         "step_launch": "HIP graph replay" if main_run["graph"] else "eager",
         "step_ms_stats": main_run["stats"],
         "hbm_copy_gbs_measured": copy_bandwidth(torch),
+        "mfma_f16_tflops_measured": None,
         "eager_ms_per_step": round(main_run["eager_s"] * 1e3 / K, 4),
         "model_tflops": round(total_tflops, 1),
         "roofline": {"kernel": "gate/up GEMM + SwiGLU", "bound": "mfma",
@@ -619,6 +638,9 @@ def main():
                      "avg_launch_us": round(avg_us, 2), "launches": n_launch,
                      "flops_per_launch": gu_flops},
     }
+    measured = mfma_rate(torch)
+    res["mfma_f16_tflops_measured"] = measured
+    res["roofline"]["frac_of_measured_peak"] = round(achieved / measured, 4)
     if not args.no_batch1:
         b1 = run_workload(torch, "stack_b1", K, args.warmup)
         t1 = b1["wall_s"] / K

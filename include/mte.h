@@ -221,6 +221,16 @@ int mte_encode_prefixed(mte_encoder *enc, const void *prefix_embeds, const int32
 /* Frees the encoder (synchronises the device first). NULL is a no-op. */
 void mte_encoder_destroy(mte_encoder *enc);
 
+/* Measurement helper (no part of the encoder): enqueues a kernel of `blocks`
+ * workgroups of 4 waves in which every wave runs `iters` rounds of eight
+ * independent fp16 32x32x16 matrix-core operations (v_mfma_f32_32x32x16_f16,
+ * 32768 flops each) with no memory traffic, so that flops / duration is the
+ * dense fp16 rate the device sustains under matrix-core load (its clock
+ * drops below the 2.4 GHz the published peak assumes). sink: device float
+ * [blocks * 256], overwritten. Errors: MTE_E_INVALID (null sink, blocks or
+ * iters <= 0), MTE_E_HIP. */
+int mte_probe_mfma(int32_t blocks, int32_t iters, float *sink, hipStream_t stream);
+
 /* OCP fp8 e4m3 quantisation of the rows of a matrix, the weight format of
  * MTE_WEIGHTS_E4M3 (e4m3: sign, 4 exponent bits of bias 7, 3 significand
  * bits; subnormals below 2^-6 in steps of 2^-9; largest finite 448; codes

@@ -16,8 +16,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libmte.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["gemm.hip", "gemm_f8.hip", "attention.hip", "norm_rope.hip", "vision_kernels.hip", "api.cpp",
-           "vision.cpp"]
+SOURCES = ["gemm.hip", "gemm_f8.hip", "attention.hip", "norm_rope.hip", "vision_kernels.hip", "probe.hip",
+           "api.cpp", "vision.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -40,7 +40,7 @@ def _compile(src: str) -> str:
 
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD_DIR, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(7, len(SOURCES))) as ex:
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
         objs = list(ex.map(_compile, SOURCES))
     tmp = OUT + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]

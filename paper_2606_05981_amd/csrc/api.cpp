@@ -684,6 +684,11 @@ int mte_quantize_e4m3_rows(const void *src, int32_t src_dtype, int32_t rows, int
              : MTE_E_HIP;
 }
 
+int mte_probe_mfma(int32_t blocks, int32_t iters, float *sink, hipStream_t stream) {
+  if (!sink || blocks <= 0 || iters <= 0) return MTE_E_INVALID;
+  return launch_mfma_probe(blocks, iters, sink, stream) == hipSuccess ? MTE_OK : MTE_E_HIP;
+}
+
 int mte_timing_disable(mte_encoder *e) {
   if (!e) return MTE_E_INVALID;
   e->timing_class = -1;

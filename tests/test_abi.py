@@ -136,6 +136,12 @@ def test_e4m3_config_valid(B):
     assert ctypes.sizeof(B.mte_config) == 4 * 19   # 19 four-byte fields, as in mte.h
 
 
+def test_probe_rejects_bad_arguments(B):
+    assert B.lib.mte_probe_mfma(0, 10, 4096, None) == -1
+    assert B.lib.mte_probe_mfma(4, 0, 4096, None) == -1
+    assert B.lib.mte_probe_mfma(4, 10, None, None) == -1
+
+
 def test_quantize_rejects_bad_arguments(B):
     q = B.lib.mte_quantize_e4m3_rows
     assert q(None, 1, 4, 4, 4096, 8192, None) == -1       # null source
