@@ -604,7 +604,9 @@ def main():
     achieved = gu_flops / (avg_us * 1e-6) / 1e12
     total_tflops = step_flops(dims, main_run["lens"]) * K / main_run["wall_s"] / 1e12
     res = {
-        "metric": "encoder prefill tokens/s (96 tok/frame, bs16; bs1 in batch1)",
+        # value: tokens/s at batch 16 (frames_per_s beside it); batch 1 in "batch1"; the
+        # roofline fractions in "roofline" (MFMA, batch 16) and "batch1.hbm_roofline"
+        "metric": "encoder prefill tokens/s & frames/s (96 tok/frame, bs 1/16); % MFMA/HBM roofline",
         "value": round(tok_s, 1),
         "unit": "tokens/s",
         "n_gpus": 1,
