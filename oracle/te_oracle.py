@@ -23,7 +23,7 @@ writes out the standard pre-norm decoder stack such a model is defined by:
         x = x + (silu(m Wg^T) * (m Wu^T)) Wd^T
     out = RMSNorm(x) * g_final
 
-Readings where the paper is silent (all of them listed in the design doc):
+Readings where the paper is silent (each a choice the paper leaves open):
 rotate-half pairing (element j with j + d/2); inverse frequencies
 theta^(-2j/d); rotary pairs split into contiguous t/h/w sections, or the
 interleaved assignment; positions of image tokens (t, h, w) on the merged

@@ -9,7 +9,7 @@ through Qwen3-VL's vision tower, whose output fills the prompt's image
 placeholder with the image tokens the decoder attends to (Sec. I; Sec. III-A
 "Notation and Setup"). The paper gives no architecture, so this writes out
 the plain pre-norm ViT with a patch merger that such a tower is defined by,
-with these readings (all listed in the design doc):
+with these readings (each a choice the paper leaves open):
 
     patch vectors: C x patch x patch pixels in (channel, row, column) order,
         patches enumerated in merge-group order (groups of merge x merge
