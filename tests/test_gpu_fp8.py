@@ -124,3 +124,31 @@ def test_e4m3_two_layer_stack(torch):
         for sl in seq_slices(layouts):
             assert rel_err(got[sl], ref[sl]) <= TOL_STACK
     enc.close()
+
+
+def test_e4m3_graph_replays_match_eager(torch):
+    """The e4m3 encoder (quantised at creation) captures into a graph like the bf16 one."""
+    from paper_2606_05981_amd.encoder import build_positions
+    dims = W.DIMS_FULL.with_(n_layers=2)
+    layouts = [W.workload("stack_b1").layouts[0]] * 2
+    x = torch.from_numpy(W.embeddings(dims, layouts)).to("cuda", torch.bfloat16)
+    pos = build_positions(layout_tuples(layouts))
+    lens = W.seq_lens(layouts)
+    enc = make_encoder(dims, weight_format=E4M3)
+    eager = enc.encode(x, pos, lens).clone()
+    out = torch.empty_like(eager)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            enc.encode(x, pos, lens, out=out)
+    torch.cuda.current_stream().wait_stream(s)
+    for r in range(3):
+        out.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(out, eager), r
+        enc.encode(x, pos, lens)
+        torch.cuda.synchronize()
+    enc.close()

@@ -169,3 +169,30 @@ def test_vision_rejects_bad_shapes_and_capacity(torch):
     enc.close()
     ref = _oracle(v, img)
     assert got.shape == (1, v.out_hidden) and rel_err(got.cpu().numpy(), ref) <= TOL_F32
+
+
+def test_vision_graph_replays_match_eager(torch):
+    """mte_vision_encode only enqueues work: captured once, every replay (with eager work in
+    between) reproduces the eager result bit for bit, also when written strided."""
+    v = SV.VDIMS_FULL.with_(depth=2)
+    img = torch.from_numpy(SV.images(v, 2, 256, 256)).to("cuda", torch.bfloat16)
+    enc = _encoder(v)
+    eager = enc.encode(img).clone()
+    out = torch.empty((2 * 96, v.out_hidden), dtype=torch.float32, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            enc.encode(img, out=out, image_stride=96, stream=s)
+    torch.cuda.current_stream().wait_stream(s)
+    for r in range(3):
+        out.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        for i in range(2):
+            assert torch.equal(out[96 * i:96 * i + 64], eager[64 * i:64 * (i + 1)]), (r, i)
+        assert bool(torch.isnan(out[64:96]).all())          # rows between images untouched
+        enc.encode(img)                                      # eager work between replays
+        torch.cuda.synchronize()
+    enc.close()
