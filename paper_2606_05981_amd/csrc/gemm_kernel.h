@@ -140,12 +140,49 @@ __device__ __forceinline__ f16x8 widen_e4m3(u32x2 w) {
   return f16x8{a[0], a[1], b[0], b[1], c[0], c[1], d[0], d[1]};
 }
 
+// Cross-lane steps without the LDS unit (gfx950):
+// swap16(a, b): v_permlane16_swap -- in each 32-lane half, the upper 16 lanes'
+// a and the lower 16 lanes' b trade places, so that afterwards a lower lane
+// holds (its a, its partner's a) and an upper lane (its partner's b, its b).
+__device__ __forceinline__ void swap16(float &a, float &b) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false);
+  a = __uint_as_float(r[0]);
+  b = __uint_as_float(r[1]);
+}
+// x + the same value of lane (l + n) mod 16 in its 16-lane row (DPP row_ror:n).
+template <int n>
+__device__ __forceinline__ float add_row_ror(float x) {
+  return x + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x120 + n, 0xf, 0xf, false));
+}
+// Sum of x over the 32 lanes of each half-wave, in every lane of it.
+__device__ __forceinline__ float sum_half_wave(float x) {
+  x = add_row_ror<8>(x);
+  x = add_row_ror<4>(x);
+  x = add_row_ror<2>(x);
+  x = add_row_ror<1>(x);            // every lane: its 16-lane row's sum
+  float y = x;
+  swap16(x, y);                     // (own, partner) or (partner, own)
+  return x + y;
+}
+
+// Element at byte offset `off` of `base`: with a wave-uniform base and a 32-bit
+// lane offset this is one global access with a scalar base address (no
+// 64-bit address arithmetic per lane).
+template <typename T>
+__device__ __forceinline__ T &at(T *base, uint32_t off) { return *(T *)((char *)base + off); }
+
+// Row of accumulator register r of a 32x32 MFMA tile, less the lane's
+// 4 * (lane >> 5): acc_row(r, lane) = acc_row0(r) + 4 * (lane >> 5).
+__host__ __device__ constexpr int acc_row0(int r) { return 8 * (r >> 2) + (r & 3); }
+
 // EPI_QKV epilogue of one wave: rows mw.. (TM blocks of 32), columns cw..
-// (TN blocks of 32 = whole heads of HD columns). For each row and q or k
-// head: RMS-normalise (sum of squares over the head's HD/32 column blocks
-// and the 32 lanes that hold the row) and rotate pair (c, c + HD/2), i.e.
-// column blocks (jb, jb + HD/64) of one lane. Gains are read once; the
-// rotary table values of a block of 32 rows are read before they are used.
+// (TN blocks of 32 = whole heads of HD columns), mw and cw wave-uniform. For
+// each row and q or k head: RMS-normalise (sum of squares over the head's
+// HD/32 column blocks and the 32 lanes that hold the row) and rotate pair
+// (c, c + HD/2), i.e. column blocks (jb, jb + HD/64) of one lane. Gains are
+// read once; the rotary table values of a block of 32 rows are read before
+// they are used. A block wholly inside M is stored at a wave-uniform row
+// address plus a 32-bit lane offset, without per-row tests.
 template <int HD, int TM, int TN>
 __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const GemmArgs &g, int cw,
                                              int mw, int lane) {
@@ -154,9 +191,10 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const 
   constexpr int NR = NH * HJB / 2;                // rotary blocks per row
   static_assert(TN % HJB == 0, "whole heads per wave");
   const QkvEpi &q = g.qe;
-  const int lrow = lane & 31;
+  const int lrow = lane & 31, lgrp = lane >> 5;
   const int M = g.M;
   float *C = (float *)g.C;
+  const uint32_t lofs = (uint32_t)(4 * lgrp * g.ldc + lrow) * 4u;   // bytes
   bool rot[NH];
   float gsc[TN];
 #pragma unroll
@@ -169,25 +207,47 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const 
   }
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
+    const int mb = mw + i * 32;
+    const bool full = mb + 32 <= M;               // wave-uniform
     float tc[16][NR], ts[16][NR];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = min(mw + i * 32 + acc_row(r, lane), M - 1);
+    for (int r = 0; r < 16; ++r)
 #pragma unroll
       for (int x = 0; x < NR; ++x) {
-        const int h = x / (HJB / 2), jj = x % (HJB / 2);
         tc[r][x] = 1.f;
         ts[r][x] = 0.f;
-        if (rot[h]) {
-          const size_t o = (size_t)m * (HD / 2) + jj * 32 + lrow;
-          tc[r][x] = q.rcos[o];
-          ts[r][x] = q.rsin[o];
+      }
+    // table row mb + acc_row(r, lane), clamped to M - 1 in a partial block
+    if (full) {
+      const uint32_t to = (uint32_t)(4 * lgrp * (HD / 2) + lrow) * 4u;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const size_t rb = (size_t)(mb + acc_row0(r)) * (HD / 2);
+#pragma unroll
+        for (int x = 0; x < NR; ++x) {
+          const int h = x / (HJB / 2), jj = x % (HJB / 2);
+          if (rot[h]) {
+            tc[r][x] = at(q.rcos + rb, to + jj * 128u);
+            ts[r][x] = at(q.rsin + rb, to + jj * 128u);
+          }
+        }
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const size_t rb = (size_t)min(mb + acc_row(r, lane), M - 1) * (HD / 2);
+#pragma unroll
+        for (int x = 0; x < NR; ++x) {
+          const int h = x / (HJB / 2), jj = x % (HJB / 2);
+          if (rot[h]) {
+            tc[r][x] = q.rcos[rb + jj * 32 + lrow];
+            ts[r][x] = q.rsin[rb + jj * 32 + lrow];
+          }
         }
       }
     }
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int m = mw + i * 32 + acc_row(r, lane);
       float v[TN];
 #pragma unroll
       for (int j = 0; j < TN; ++j) v[j] = acc[i][j][r] * g.scale;
@@ -198,8 +258,7 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const 
           float ss = 0.f;
 #pragma unroll
           for (int jj = 0; jj < HJB; ++jj) ss += v[h * HJB + jj] * v[h * HJB + jj];
-#pragma unroll
-          for (int o = 1; o < 32; o <<= 1) ss += __shfl_xor(ss, o, kWave);
+          ss = sum_half_wave(ss);
           const float rs = rsqrtf(ss / (float)HD + q.eps);
 #pragma unroll
           for (int jj = 0; jj < HJB; ++jj) v[h * HJB + jj] = v[h * HJB + jj] * rs * gsc[h * HJB + jj];
@@ -212,9 +271,16 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const 
           v[jp] = w * tc[r][x] + u * ts[r][x];
         }
       }
-      if (m < M)
+      if (full) {
+        float *p = C + (size_t)(mb + acc_row0(r)) * g.ldc + cw;
 #pragma unroll
-        for (int j = 0; j < TN; ++j) C[(size_t)m * g.ldc + cw + j * 32 + lrow] = v[j];
+        for (int j = 0; j < TN; ++j) at(p, lofs + j * 128u) = v[j];
+      } else {
+        const int m = mb + acc_row(r, lane);
+        if (m < M)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) C[(size_t)m * g.ldc + cw + j * 32 + lrow] = v[j];
+      }
     }
   }
 }
@@ -438,76 +504,140 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
     }
   }
 
-  // Epilogue.
+  // Epilogue. The wave's rows are mw + 32 i + acc_row(r, lane), its columns
+  // cw + 32 j + lrow (mw, cw wave-uniform). A 32-row block wholly inside M
+  // (a wave-uniform test) is written without per-row tests, each row at a
+  // wave-uniform address plus a 32-bit lane offset; only the last, partial
+  // block tests rows.
+  const int uwm = uwave / WN, uwn = uwave % WN;
+  const int mw = m0 + uwm * WTM, cw = n0 + uwn * WTN;
   if constexpr (EPI == EPI_QKV) {
-    const int cw = n0 + wn * WTN;
     // (the host only launches tiles whose waves cover whole heads)
     if (g.qe.hd == 128) {
-      if constexpr (TN % 4 == 0) qkv_epilogue<128, TM, TN>(acc, g, cw, m0 + wm * WTM, lane);
+      if constexpr (TN % 4 == 0) qkv_epilogue<128, TM, TN>(acc, g, cw, mw, lane);
     } else {
-      if constexpr (TN % 2 == 0) qkv_epilogue<64, TM, TN>(acc, g, cw, m0 + wm * WTM, lane);
+      if constexpr (TN % 2 == 0) qkv_epilogue<64, TM, TN>(acc, g, cw, mw, lane);
     }
     return;
   }
+  typedef typename std::conditional<MODE == MODE_F32, float, f16>::type TO;   // activation outputs
   if constexpr (EPI == EPI_SWIGLU) {
     // Column block j (32 columns) of the interleaved product holds gate
     // (lanes l%32 < 16) and up (l%32 >= 16) of outputs f = 16*block + l%16.
     // Of each pair of accumulator rows (r, r+1) the gate lane finishes row r
-    // and the up lane row r+1, each receiving the value it lacks from lane
-    // l ^ 16 (exchanged by all lanes together, outside any row test).
+    // and the up lane row r+1: one swap16 hands each the (gate, up) pair it
+    // needs. With z = scale*g and u = scale*up,
+    //   silu(z) * u * out_scale = (g * up) / (1 + 2^(g * (-scale*log2 e))) * (scale^2 * out_scale).
     const bool upl = lrow >= 16;
+    const float c1 = -g.scale * 1.4426950408889634f;
+    const float s2 = g.scale * g.scale * g.out_scale;
+    TO *C = (TO *)g.C;
+    const int fc = cw >> 1;                       // first output column of the wave
+    const uint32_t lofs = (uint32_t)((4 * lgrp + (upl ? 1 : 0)) * g.ldc + (lrow & 15)) * (uint32_t)sizeof(TO);
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
+      const int mb = mw + i * 32;
+      const bool full = mb + 32 <= M;
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int f = ((n0 + wn * WTN + j * 32) >> 1) + (lrow & 15);
-#pragma unroll
-        for (int r = 0; r < 16; r += 2) {
-          const float a0 = acc[i][j][r] * g.scale, a1 = acc[i][j][r + 1] * g.scale;
-          const float recv = __shfl_xor(upl ? a0 : a1, 16, kWave);
-          const float gt = upl ? recv : a0, up = upl ? a1 : recv;
-          const int m = m0 + wm * WTM + i * 32 + acc_row(r + (upl ? 1 : 0), lane);
-          const float y = silu_f(gt) * up * g.out_scale;
-          if (m < M) {
-            const size_t o = (size_t)m * g.ldc + f;
-            if constexpr (MODE == MODE_F32) ((float *)g.C)[o] = y;
-            else ((f16 *)g.C)[o] = (f16)y;
-          }
-        }
-      }
-    }
-    return;
-  }
-  if constexpr (EPI == EPI_GELU) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = m0 + wm * WTM + i * 32 + acc_row(r, lane);
-        if (m >= M) continue;
+      for (int r = 0; r < 16; r += 2) {
+        float y[TN];
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-          const size_t o = (size_t)m * g.ldc + n0 + wn * WTN + j * 32 + lrow;
-          const float y = gelu_tanh(acc[i][j][r] * g.scale) * g.out_scale;
-          if constexpr (MODE == MODE_F32) ((float *)g.C)[o] = y;
-          else ((f16 *)g.C)[o] = (f16)y;
+          float ga = acc[i][j][r], up = acc[i][j][r + 1];
+          swap16(ga, up);
+          const float e = __builtin_amdgcn_exp2f(ga * c1);
+          y[j] = (ga * up) * __builtin_amdgcn_rcpf(1.f + e) * s2;
+        }
+        if (full) {
+          TO *p = C + (size_t)(mb + acc_row0(r)) * g.ldc + fc;
+#pragma unroll
+          for (int j = 0; j < TN; ++j) at(p, lofs + j * 16u * (uint32_t)sizeof(TO)) = (TO)y[j];
+        } else {
+          const int m = mb + acc_row(r + (upl ? 1 : 0), lane);
+          if (m < M)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) C[(size_t)m * g.ldc + fc + j * 16 + (lrow & 15)] = (TO)y[j];
         }
       }
     }
     return;
   }
+  const uint32_t lofs = (uint32_t)(4 * lgrp * g.ldc + lrow);   // elements
+  if constexpr (EPI == EPI_GELU) {
+    // gelu_tanh(scale*a) * out_scale = a / (1 + 2^(c0 a (1 + k2 a^2))) * (scale * out_scale),
+    // c0 = -2 sqrt(2/pi) log2(e) scale, k2 = 0.044715 scale^2.
+    const float k2 = 0.044715f * g.scale * g.scale;
+    const float c0 = -1.5957691216057308f * 1.4426950408889634f * g.scale;
+    const float so = g.scale * g.out_scale;
+    TO *C = (TO *)g.C;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+      const int mb = mw + i * 32;
+      const bool full = mb + 32 <= M;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float y[TN];
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const float a = acc[i][j][r];
+          const float e = __builtin_amdgcn_exp2f(a * fmaf(a * a, k2, 1.f) * c0);
+          y[j] = a * __builtin_amdgcn_rcpf(1.f + e) * so;
+        }
+        if (full) {
+          TO *p = C + (size_t)(mb + acc_row0(r)) * g.ldc + cw;
+#pragma unroll
+          for (int j = 0; j < TN; ++j) at(p, (lofs + j * 32u) * (uint32_t)sizeof(TO)) = (TO)y[j];
+        } else {
+          const int m = mb + acc_row(r, lane);
+          if (m < M)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) C[(size_t)m * g.ldc + cw + j * 32 + lrow] = (TO)y[j];
+        }
+      }
+    }
+    return;
+  }
+  // EPI_STORE / EPI_PARTIAL: C = scale * acc; EPI_RESID: C += scale * acc (one
+  // rounding: scale is a power of two), the block's old values all read
+  // before the first store so that their latencies overlap.
+  float *C = (float *)g.C + (EPI == EPI_PARTIAL ? (size_t)blockIdx.z * g.c_plane : 0);
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
+    const int mb = mw + i * 32;
+    const bool full = mb + 32 <= M;
+    float old[16][TN];
+    if constexpr (EPI == EPI_RESID) {
+      if (full) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float *p = C + (size_t)(mb + acc_row0(r)) * g.ldc + cw;
+#pragma unroll
+          for (int j = 0; j < TN; ++j) old[r][j] = at(p, (lofs + j * 32u) * 4u);
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = min(mb + acc_row(r, lane), M - 1);
+#pragma unroll
+          for (int j = 0; j < TN; ++j) old[r][j] = C[(size_t)m * g.ldc + cw + j * 32 + lrow];
+        }
+      }
+    }
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int m = m0 + wm * WTM + i * 32 + acc_row(r, lane);
-      if (m >= M) continue;
-      float *C = (float *)g.C + (EPI == EPI_PARTIAL ? (size_t)blockIdx.z * g.c_plane : 0);
+      float y[TN];
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const size_t o = (size_t)m * g.ldc + n0 + wn * WTN + j * 32 + lrow;
-        if constexpr (EPI == EPI_RESID) C[o] += acc[i][j][r] * g.scale;
-        else C[o] = acc[i][j][r] * g.scale;
+      for (int j = 0; j < TN; ++j)
+        y[j] = EPI == EPI_RESID ? fmaf(acc[i][j][r], g.scale, old[r][j]) : acc[i][j][r] * g.scale;
+      if (full) {
+        float *p = C + (size_t)(mb + acc_row0(r)) * g.ldc + cw;
+#pragma unroll
+        for (int j = 0; j < TN; ++j) at(p, (lofs + j * 32u) * 4u) = y[j];
+      } else {
+        const int m = mb + acc_row(r, lane);
+        if (m < M)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) C[(size_t)m * g.ldc + cw + j * 32 + lrow] = y[j];
       }
     }
   }
