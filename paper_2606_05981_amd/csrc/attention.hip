@@ -102,24 +102,20 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   constexpr int NFP = 16 / EPF;                  // P fragments per 32-kv tile
   constexpr int VTP = KV + 16 / (int)sizeof(TV); // V^T row pitch: 16-byte aligned, conflict-free
   constexpr int ND = HD / 32;                    // 32-wide d blocks
-  constexpr int OTP = HD + 4;                    // padded output staging row (floats)
   static_assert(EC == Frag<T>::kElems && (int)sizeof(T) == (int)sizeof(TV), "chunk = fragment");
   typedef typename Frag<T>::type frag_t;
   typedef typename Frag<TV>::type vfrag_t;
   // PVH: V is staged times the output pre-scale, so o comes out scaled
   const float v_scale = PVH ? a.o_scale : 1.f;
 
-  // The K / V^T stages and the output staging are never live together.
   constexpr int K_BYTES = NP * KV * NCH * 16;
   constexpr int V_BYTES = NPV * HD * VTP * (int)sizeof(TV);
-  constexpr int O_BYTES = 4 * 32 * OTP * 4;
   constexpr int ST_BYTES = K_BYTES + V_BYTES;             // one staged tile
-  constexpr int SMEM = NB * ST_BYTES > O_BYTES ? NB * ST_BYTES : O_BYTES;
+  constexpr int SMEM = NB * ST_BYTES;
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
   // tile b: K [NP][KV * NCH] at smem + b * ST_BYTES, V^T [NPV][HD * VTP] after it
   auto sK_of = [&](int b) { return (u32x4 *)(smem + b * ST_BYTES); };
   auto sVt_of = [&](int b) { return (TV *)(smem + b * ST_BYTES + K_BYTES); };
-  float *sOall = (float *)smem;                            // [4][32 * OTP]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lrow = lane & 31, lgrp = lane >> 5;
@@ -418,42 +414,34 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       if (b < n_blocks) lstore(b, sK_of(b), sVt_of(b));
     __syncthreads();
     for (int kb = 0; kb < n_blocks; ++kb) compute(kb * KV, sK_of(kb), sVt_of(kb));
-    __syncthreads();
   }
 
-  // Output: each wave writes its normalised 32 x HD tile into LDS (row-major
-  // by query, over the stage buffers, free after the loop's last barrier),
-  // then copies it out row by row so that the global stores are contiguous
-  // along d (a lane owns a query row in the accumulator layout, which would
-  // scatter 2-byte stores across rows).
+  // Output. oacc[n] holds rows d = 32 n + acc_row(r, lane) of O^T for the
+  // lane's query: accumulator registers 4c..4c+3 are four consecutive d, so
+  // each lane writes them as one 8-byte (fp16) or 16-byte (fp32) store into
+  // its query's row, and the two lane groups fill 16 (32) contiguous bytes.
   const float lt = l_i + __shfl_xor(l_i, 32, kWave);
   // MODE_F16: o times its pre-scale (with PVH the pre-scale came with V)
   const float inv = ((MODE == MODE_F32 || PVH) ? 1.f : a.o_scale) / lt;
-  float *so = sOall + wave * 32 * OTP;
+  if (my_q < L) {
+    const size_t orow = ((size_t)(s0 + my_q) * a.Hq + head) * HD + 4 * lgrp;
 #pragma unroll
-  for (int n = 0; n < ND; ++n)
+    for (int n = 0; n < ND; ++n)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) so[lrow * OTP + n * 32 + acc_row(r, lane)] = oacc[n][r] * inv;
-  __builtin_amdgcn_s_waitcnt(0xc07f);   // this wave's LDS writes done (lgkmcnt 0)
-  __builtin_amdgcn_wave_barrier();
-  if (qw < L) {
-    constexpr int LPR = HD / 4;          // lanes per row (4 values each)
-    constexpr int RPI = 64 / LPR;        // rows per instruction
+      for (int c = 0; c < 4; ++c) {
+        const int d = n * 32 + 8 * c;
+        if constexpr (MODE == MODE_F32) {
+          f32x4 y;
 #pragma unroll
-    for (int it = 0; it < 32 / RPI; ++it) {
-      const int q = it * RPI + lane / LPR, d = (lane % LPR) * 4;
-      if (qw + q >= L) continue;
-      const f32x4 y = *(const f32x4 *)(so + q * OTP + d);
-      const size_t o = ((size_t)(s0 + qw + q) * a.Hq + head) * HD + d;
-      if constexpr (MODE == MODE_F32) {
-        *(f32x4 *)((float *)a.o + o) = y;
-      } else {
-        f16x4 h;
+          for (int e = 0; e < 4; ++e) y[e] = oacc[n][4 * c + e] * inv;
+          *(f32x4 *)((float *)a.o + orow + d) = y;
+        } else {
+          f16x4 h;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) h[e] = (f16)y[e];
-        *(f16x4 *)((f16 *)a.o + o) = h;
+          for (int e = 0; e < 4; ++e) h[e] = (f16)(oacc[n][4 * c + e] * inv);
+          *(f16x4 *)((f16 *)a.o + orow + d) = h;
+        }
       }
-    }
   }
 }
 
