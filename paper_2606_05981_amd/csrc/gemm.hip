@@ -55,8 +55,8 @@ static const TileChoice kChoices[] = {
     {12288, 2048, EPI_SWIGLU, 768, 3, 1},  {2048, 6144, EPI_RESID, 768, 14, 2},
     {4096, 2048, EPI_QKV, 1536, 23, 1},   {2048, 2048, EPI_RESID, 1536, 12, 1},
     {12288, 2048, EPI_SWIGLU, 1536, 32, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
-    {4096, 2048, EPI_QKV, 3072, 27, 1},   {2048, 2048, EPI_RESID, 3072, 23, 1},
-    {12288, 2048, EPI_SWIGLU, 3072, 32, 1}, {2048, 6144, EPI_RESID, 3072, 23, 1},
+    {4096, 2048, EPI_QKV, 3072, 27, 1},   {2048, 2048, EPI_RESID, 3072, 8, 1},
+    {12288, 2048, EPI_SWIGLU, 3072, 32, 1}, {2048, 6144, EPI_RESID, 3072, 12, 1},
     {4096, 2048, EPI_QKV, 10240, 27, 1},  {2048, 2048, EPI_RESID, 10240, 2, 1},
     {12288, 2048, EPI_SWIGLU, 10240, 26, 1}, {2048, 6144, EPI_RESID, 10240, 12, 1},
     // vision tower (width 1024, MLP 4096, 768-value patches, 2x2 merger to 2048):
