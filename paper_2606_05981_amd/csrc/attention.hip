@@ -133,8 +133,18 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const int q0 = (tile - a.tile0[seq]) * QT;
   const int g = blockIdx.y / a.head_blocks, hb = blockIdx.y % a.head_blocks;
   const int head = g * a.rep + hb * a.hpb + wave / a.wph;
-  const int qw = q0 + (wave % a.wph) * 32;         // first query row of this wave
+  const int P = a.P;                               // keys of the shared prefix
   const int q_last = min(q0 + QT, L) - 1;          // last valid query row of the workgroup
+  // With every key tile staged at once and two waves per head, a head's
+  // second 32-row block past the end of the sequence would leave its wave
+  // idle: that wave instead takes the upper part of the first block's key
+  // tiles, and the two partial softmax states are merged through LDS before
+  // the output (a causal 96-token frame: 2 + 1 tiles instead of 3 on one wave).
+  const int n_first = a.causal ? ((P + min(q0 + 31, L - 1)) / KV + 1) : ((P + L - 1) / KV + 1);
+  const bool pair_split = NB > 1 && a.wph == 2 && q0 < L && q0 + 32 >= L && n_first >= 2;   // workgroup-uniform
+  const bool helper = pair_split && (wave & 1);
+  const int kb_split = n_first - n_first / 2;      // the helper's first key tile
+  const int qw = q0 + (wave % a.wph) * 32 - (helper ? 32 : 0);   // first query row of this wave
   const int wave_last = min(qw + 31, L - 1);       // last valid query row of this wave
   const size_t ld = (size_t)a.ld_qkv;
   const size_t base = (size_t)s0 * ld;             // element offset of the sequence's first row
@@ -177,7 +187,6 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 
   // Keys are numbered over [0, P + L): the shared prefix's first, then the
   // sequence's own; own query i sits at key index P + i.
-  const int P = a.P;
   const int n_blocks = (q_last < 0) ? 0 : a.causal ? ((P + q_last) / KV + 1) : ((P + L - 1) / KV + 1);
   auto key_row = [&](int kv) -> const float * {
     kv = min(kv, P + L - 1);
@@ -339,13 +348,16 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     }
     mb = warp_max_xor(mb, 32);
     const float m_new = fmaxf(m_i, mb);
-    const float alpha = exp2f(m_i - m_new);
+    // no key of the query seen yet (a helper's range can start past it):
+    // exponentiate against 0 so that every term is an exact 0, not NaN
+    const float m_ref = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = exp2f(m_i - m_ref);
     m_i = m_new;
     float p[16];
     float ps = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      p[r] = exp2f(s[r] - m_new);
+      p[r] = exp2f(s[r] - m_ref);
       ps += p[r];
     }
     l_i = l_i * alpha + ps;
@@ -413,7 +425,38 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     for (int b = 0; b < NB; ++b)
       if (b < n_blocks) lstore(b, sK_of(b), sVt_of(b));
     __syncthreads();
-    for (int kb = 0; kb < n_blocks; ++kb) compute(kb * KV, sK_of(kb), sVt_of(kb));
+    const int kb_lo = helper ? kb_split : 0;
+    const int kb_hi = (pair_split && !helper) ? kb_split : n_blocks;
+    for (int kb = kb_lo; kb < kb_hi; ++kb) compute(kb * KV, sK_of(kb), sVt_of(kb));
+    if (pair_split) {
+      // Every wave is done with the staged tiles; the helper's state (m, l,
+      // the O^T accumulators) goes over them in lane order, one slab per
+      // head, and its partner rescales both parts to the common max.
+      constexpr int MS = 2 + ND * 16;
+      static_assert(2 * MS * 64 * 4 <= SMEM, "merge slabs fit the stage buffers");
+      __syncthreads();
+      float *mx = (float *)smem + (size_t)(wave >> 1) * MS * 64 + lane;
+      if (helper) {
+        mx[0] = m_i;
+        mx[64] = l_i;
+#pragma unroll
+        for (int n = 0; n < ND; ++n)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) mx[(2 + n * 16 + r) * 64] = oacc[n][r];
+      }
+      __syncthreads();
+      if (!helper) {
+        const float mb = mx[0], lb = mx[64];
+        const float m = fmaxf(m_i, mb);           // finite: the partner saw key 0
+        const float fa = exp2f(m_i - m), fb = exp2f(mb - m);
+        l_i = l_i * fa + lb * fb;
+        m_i = m;
+#pragma unroll
+        for (int n = 0; n < ND; ++n)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[n][r] = oacc[n][r] * fa + mx[(2 + n * 16 + r) * 64] * fb;
+      }
+    }
   }
 
   // Output. oacc[n] holds rows d = 32 n + acc_row(r, lane) of O^T for the
@@ -423,7 +466,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   const float lt = l_i + __shfl_xor(l_i, 32, kWave);
   // MODE_F16: o times its pre-scale (with PVH the pre-scale came with V)
   const float inv = ((MODE == MODE_F32 || PVH) ? 1.f : a.o_scale) / lt;
-  if (my_q < L) {
+  if (my_q < L && !helper) {
     const size_t orow = ((size_t)(s0 + my_q) * a.Hq + head) * HD + 4 * lgrp;
 #pragma unroll
     for (int n = 0; n < ND; ++n)

@@ -20,12 +20,16 @@ pytestmark = pytest.mark.gpu
 TOL_STACK = 3e-2
 
 
-@pytest.mark.parametrize("prefix,frames,n_layers", [(80, 3, 4), (16, 2, 4), (80, 1, 28)])
-def test_prefixed_equals_full_sequences(prefix, frames, n_layers):
+# (24, 4, 4): 20 own tokens after 24 prefix keys, so that in the all-tiles-staged attention the
+# second key tile (keys 32..43) goes to the otherwise idle wave, and own queries 0..7 see none
+# of its keys (their partial softmax state is empty and must merge as zero).
+@pytest.mark.parametrize("prefix,hw,after,frames,n_layers",
+                         [(80, 8, 32, 3, 4), (16, 8, 32, 2, 4), (80, 8, 32, 1, 28), (24, 4, 4, 2, 2)])
+def test_prefixed_equals_full_sequences(prefix, hw, after, frames, n_layers):
     import torch
     assert torch.cuda.is_available(), "no GPU"
     dims = W.DIMS_FULL.with_(n_layers=n_layers)
-    full = tuple(W.SeqLayout(prefix, 1, 8, 8, 32) for _ in range(frames))
+    full = tuple(W.SeqLayout(prefix, 1, hw, hw, after) for _ in range(frames))
     L = full[0].length
     emb = W.embeddings(dims, full)            # text rows come first and are shared by all frames
     pos = O.positions(full)
