@@ -31,7 +31,7 @@ static bool tile_fits(int id, int N, int K, int esz, int epi, int splits, int co
 static const double kTileRate[kNumTiles] = {959, 944, 895, 850, 850, 884, 850, 850, 800, 819,
                                             640, 777, 860, 600, 700, 650, 550, 450, 600, 600,
                                             921, 850, 850, 714, 766, 800, 1026, 1018, 850, 728,
-                                            803, 950, 950};
+                                            803, 950, 950, 950, 950, 950, 850, 850, 950};
 
 // Measured choices (MI355X sweep of every tile and split count, weights
 // rotated through 600 MB so that they stream from HBM; at 96 and 192 rows
@@ -48,17 +48,17 @@ struct TileChoice {
 };
 static const TileChoice kChoices[] = {
     {4096, 2048, EPI_QKV, 96, 12, 4},     {2048, 2048, EPI_RESID, 96, 16, 4},
-    {12288, 2048, EPI_SWIGLU, 96, 12, 2},  {2048, 6144, EPI_RESID, 96, 18, 8},
-    {4096, 2048, EPI_QKV, 192, 18, 4},    {2048, 2048, EPI_RESID, 192, 16, 4},
-    {12288, 2048, EPI_SWIGLU, 192, 14, 1}, {2048, 6144, EPI_RESID, 192, 14, 8},
+    {12288, 2048, EPI_SWIGLU, 96, 12, 2},  {2048, 6144, EPI_RESID, 96, 13, 8},
+    {4096, 2048, EPI_QKV, 192, 12, 2},    {2048, 2048, EPI_RESID, 192, 16, 4},
+    {12288, 2048, EPI_SWIGLU, 192, 14, 1}, {2048, 6144, EPI_RESID, 192, 23, 8},
     {4096, 2048, EPI_QKV, 768, 12, 1},    {2048, 2048, EPI_RESID, 768, 12, 2},
     {12288, 2048, EPI_SWIGLU, 768, 3, 1},  {2048, 6144, EPI_RESID, 768, 14, 2},
     {4096, 2048, EPI_QKV, 1536, 23, 1},   {2048, 2048, EPI_RESID, 1536, 12, 1},
-    {12288, 2048, EPI_SWIGLU, 1536, 32, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
+    {12288, 2048, EPI_SWIGLU, 1536, 32, 1}, {2048, 6144, EPI_RESID, 1536, 5, 2},
     {4096, 2048, EPI_QKV, 3072, 27, 1},   {2048, 2048, EPI_RESID, 3072, 8, 1},
-    {12288, 2048, EPI_SWIGLU, 3072, 32, 1}, {2048, 6144, EPI_RESID, 3072, 12, 1},
-    {4096, 2048, EPI_QKV, 10240, 27, 1},  {2048, 2048, EPI_RESID, 10240, 2, 1},
-    {12288, 2048, EPI_SWIGLU, 10240, 26, 1}, {2048, 6144, EPI_RESID, 10240, 12, 1},
+    {12288, 2048, EPI_SWIGLU, 3072, 32, 1}, {2048, 6144, EPI_RESID, 3072, 8, 1},
+    {4096, 2048, EPI_QKV, 10240, 27, 1},  {2048, 2048, EPI_RESID, 10240, 36, 1},
+    {12288, 2048, EPI_SWIGLU, 10240, 38, 1}, {2048, 6144, EPI_RESID, 10240, 12, 1},
     // vision tower (width 1024, MLP 4096, 768-value patches, 2x2 merger to 2048):
     // 16 images of 256 patches, merger at 1024 rows
     {3072, 1024, EPI_QKV, 4096, 27, 1},   {1024, 1024, EPI_RESID, 4096, 12, 1},
@@ -69,11 +69,11 @@ static const TileChoice kChoices[] = {
 // The same for e4m3 weights (tiles staging 128 bytes of A per row).
 static const TileChoice kChoicesW8[] = {
     {4096, 2048, EPI_QKV, 96, 17, 4},     {2048, 2048, EPI_RESID, 96, 17, 4},
-    {12288, 2048, EPI_SWIGLU, 96, 14, 1},  {2048, 6144, EPI_RESID, 96, 12, 8},
+    {12288, 2048, EPI_SWIGLU, 96, 14, 1},  {2048, 6144, EPI_RESID, 96, 17, 8},
     {4096, 2048, EPI_QKV, 192, 17, 2},    {2048, 2048, EPI_RESID, 192, 17, 4},
     {12288, 2048, EPI_SWIGLU, 192, 14, 1}, {2048, 6144, EPI_RESID, 192, 12, 8},
-    {4096, 2048, EPI_QKV, 1536, 12, 1},   {2048, 2048, EPI_RESID, 1536, 12, 1},
-    {12288, 2048, EPI_SWIGLU, 1536, 4, 1}, {2048, 6144, EPI_RESID, 1536, 14, 2},
+    {4096, 2048, EPI_QKV, 1536, 36, 1},   {2048, 2048, EPI_RESID, 1536, 14, 1},
+    {12288, 2048, EPI_SWIGLU, 1536, 33, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
 };
 
 // Fallback estimate: rounds of workgroups over the compute units x the time

@@ -23,10 +23,10 @@
 // Each workgroup (4 or 8 waves, WM x WN) owns a BM x BN output tile; each
 // wave a (BM/WM) x (BN/WN) block of 32x32 MFMA tiles. Eight waves, or two
 // four-wave workgroups per CU, put two waves on every SIMD, so one wave's
-// LDS reads and waits overlap the other's MFMAs. K is walked in stages of 128
-// bytes per row, staged through LDS with double buffering (one barrier per
-// stage): the next stage's global loads are in flight while the current one
-// feeds the MFMAs.
+// LDS reads and waits overlap the other's MFMAs. K is walked in stages of 64
+// or 128 bytes per row, staged through a ring of 2-6 LDS slots (one barrier
+// per stage): the loads of the next P stages are in flight while the current
+// one feeds the MFMAs.
 //
 // LDS rows are 128 bytes = 8 chunks of 16 bytes; chunk c of row r is stored
 // at slot c ^ ((r ^ (r >> 3)) & 7), so the 16-byte fragment reads of 8 or 16
@@ -95,6 +95,12 @@ template <int n>
 __device__ __forceinline__ void wait_vm() {
   static_assert(n >= 0 && n < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((n & 0xF) | (0x7 << 4) | (0xF << 8) | ((n >> 4) << 14));
+}
+// The same, and until every LDS access of this wave has completed.
+template <int n>
+__device__ __forceinline__ void wait_vm_lds0() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((n & 0xF) | (0x7 << 4) | (0x0 << 8) | ((n >> 4) << 14));
 }
 // Waits until at most after*LOADS vector-memory operations are pending,
 // for a wave-uniform after in [0, 3].
@@ -287,13 +293,14 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const 
 
 // The main loop keeps P stages in an LDS ring filled by direct global->LDS
 // loads, and double-buffers the MFMA operand fragments in registers. One
-// barrier per stage, placed before the stage's last k-step: before it each
-// wave waits for its own loads of the next stage; after it (all waves' loads
-// of the next stage are in LDS, and every wave is done with the previous
-// stage) the loads of stage kt+P-1 go into the slot stage kt-1 used, and the
-// first fragments of stage kt+1 are read while the last MFMAs of stage kt
-// run. Raw s_barrier (no fence) keeps the compiler from forcing vmcnt(0) at
-// the barrier; the waits are explicit.
+// barrier per stage, placed after the first MFMA of the stage's last k-step:
+// before it each wave waits for its own loads of the next stage and for its
+// own LDS reads (the last k-step's fragments are already in registers).
+// After it, all waves' loads of stage kt+1 are in LDS and no wave reads slot
+// kt % P again, so the loads of stage kt+P go into that slot, and the first
+// fragments of stage kt+1 are read while the last MFMAs of stage kt run.
+// Raw s_barrier (no fence) keeps the compiler from forcing vmcnt(0) at the
+// barrier; the waits are explicit.
 template <int MODE, int BM, int BN, int WM, int WN, int ROWB, int P, int EPI, int OCC>
 __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_eu(OCC * WM * WN / 4, OCC * WM * WN / 4))) void k_gemm(GemmArgs g) {
   typedef typename std::conditional<MODE == MODE_F32, float, f16>::type T;
@@ -318,7 +325,7 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
   constexpr int STAGE = ACH + BCH;                // u32x4 slots per stage
   static_assert(NW == 4 || NW == 8, "4 or 8 waves");
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
-  static_assert(LOADS * (P - 2) < 64 && P >= 3 && P <= 6, "vmcnt range, ring depth");
+  static_assert(LOADS * (P - 1) < 64 && P >= 2 && P <= 6, "vmcnt range, ring depth");
   typedef typename Frag<T>::type frag_t;
 
   extern __shared__ u32x4 lds[];                  // [P][STAGE]
@@ -405,12 +412,12 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
   static_assert(KK % 2 == 0, "fragment buffer parity");
   constexpr int NM = TM * TN;                     // MFMAs per k-step
   constexpr int NR = TM + TN;                     // fragment reads per k-step
-  // The loads of one stage are issued in NPART parts: part 0 right after the
-  // barrier of stage kt-P+1, parts 1.. in the k-steps before the barrier of
-  // stage kt-P+2. With P >= 4 every stage still has P-3 whole stages of loads
-  // in flight behind it at the barrier that waits for it; P = 3 issues each
+  // The loads of stage kt+P are issued in NPART parts: part 0 right after the
+  // barrier of stage kt, parts 1.. in the k-steps of stage kt+1 before its
+  // barrier. With P >= 3 every stage still has P-2 whole stages of loads in
+  // flight behind it at the barrier that waits for it; P = 2 issues each
   // stage whole, after the barrier.
-  constexpr int NPART = (P >= 4) ? KK : 1;
+  constexpr int NPART = (P >= 3) ? KK : 1;
   constexpr int PART = (LOADS + NPART - 1) / NPART;
 
   // One k-step: the NM MFMAs on fragment buffer `cur`, with the side work
@@ -427,8 +434,8 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
     for (int m = 0; m < NM; ++m) {
       mfma_one(cur, m);
       if (bar && m == 0) {
-        wait_vm<(P - 3) * LOADS>();        // this wave's loads of the next stage landed
-        __builtin_amdgcn_s_barrier();      // ... everyone's, and the previous stage is free
+        wait_vm_lds0<(P - 2) * LOADS>();   // this wave's loads of the next stage landed, its reads done
+        __builtin_amdgcn_s_barrier();      // ... everyone's: slot kt % P is free
         asm volatile("" ::: "memory");     // keep LDS reads of the next stage below it
       }
       const int s0 = (m * nside + NM - 1) / NM, s1 = ((m + 1) * nside + NM - 1) / NM;
@@ -445,16 +452,16 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
   // use makes the waitcnt pass drain all outstanding reads): every iteration
   // issues its loads -- past the end, repeats of the last stage into slots
   // that are never read again -- so every wait is a fixed vmcnt.
-  // Prologue: stages 0..P-3 whole and part 0 of stage P-2 (P = 3: stages
-  // 0..P-2 whole), then stage 0 must have landed.
-  constexpr int PRE_FULL = (NPART > 1) ? P - 2 : P - 1;
+  // Prologue: stages 0..P-2 whole and part 0 of stage P-1 (P = 2: stages
+  // 0..P-1 whole), then stage 0 must have landed.
+  constexpr int PRE_FULL = (NPART > 1) ? P - 1 : P;
   constexpr int PRE_PART = (NPART > 1) ? (PART < LOADS ? PART : LOADS) : 0;
 #pragma unroll
   for (int s = 0; s < PRE_FULL; ++s)
 #pragma unroll
     for (int x = 0; x < LOADS; ++x) dma_one(min(s, nk - 1), s, x);
 #pragma unroll
-  for (int x = 0; x < PRE_PART; ++x) dma_one(min(P - 2, nk - 1), P - 2, x);
+  for (int x = 0; x < PRE_PART; ++x) dma_one(min(P - 1, nk - 1), P - 1, x);
   wait_vm<(PRE_FULL - 1) * LOADS + PRE_PART>();
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
@@ -463,8 +470,8 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
   for (int kt = 0; kt < nk; ++kt) {
     const u32x4 *st = lds + (kt % P) * STAGE;
     const u32x4 *nx = lds + ((kt + 1) % P) * STAGE;
-    const int ksa = min(kt + P - 2, nk - 1), sla = (kt + P - 2) % P;   // parts 1.. issued here
-    const int ksb = min(kt + P - 1, nk - 1), slb = (kt + P - 1) % P;   // part 0 issued here
+    const int ksa = min(kt + P - 1, nk - 1), sla = (kt + P - 1) % P;   // parts 1.. issued here
+    const int ksb = min(kt + P, nk - 1), slb = kt % P;                  // part 0 issued here
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
       const int cur = kk & 1;
@@ -707,7 +714,13 @@ static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
   X(29, 128, 256, 2, 4, 64, 6, 1, 0)         \
   X(30, 128, 128, 2, 4, 128, 4, 1, 0)         \
   X(31, 384, 192, 4, 2, 64, 4, 1, 0)         \
-  X(32, 192, 384, 2, 4, 64, 4, 1, 0)
+  X(32, 192, 384, 2, 4, 64, 4, 1, 0)         \
+  X(33, 192, 384, 2, 4, 128, 2, 1, 0)        \
+  X(34, 256, 256, 2, 4, 128, 2, 1, 0)        \
+  X(35, 192, 384, 2, 4, 64, 3, 1, 0)         \
+  X(36, 128, 128, 4, 1, 128, 2, 2, 0)        \
+  X(37, 192, 128, 2, 2, 128, 2, 1, 0)        \
+  X(38, 256, 256, 4, 2, 128, 2, 1, 0)
 
 
 template <int MODE, int EPI>
