@@ -53,8 +53,8 @@ static const TileChoice kChoices[] = {
     {12288, 2048, EPI_SWIGLU, 192, 14, 1}, {2048, 6144, EPI_RESID, 192, 23, 8},
     {4096, 2048, EPI_QKV, 768, 12, 1},    {2048, 2048, EPI_RESID, 768, 12, 2},
     {12288, 2048, EPI_SWIGLU, 768, 3, 1},  {2048, 6144, EPI_RESID, 768, 14, 2},
-    {4096, 2048, EPI_QKV, 1536, 23, 1},   {2048, 2048, EPI_RESID, 1536, 12, 1},
-    {12288, 2048, EPI_SWIGLU, 1536, 32, 1}, {2048, 6144, EPI_RESID, 1536, 5, 2},
+    {4096, 2048, EPI_QKV, 1536, 36, 1},   {2048, 2048, EPI_RESID, 1536, 14, 1},
+    {12288, 2048, EPI_SWIGLU, 1536, 32, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
     {4096, 2048, EPI_QKV, 3072, 27, 1},   {2048, 2048, EPI_RESID, 3072, 8, 1},
     {12288, 2048, EPI_SWIGLU, 3072, 32, 1}, {2048, 6144, EPI_RESID, 3072, 8, 1},
     {4096, 2048, EPI_QKV, 10240, 27, 1},  {2048, 2048, EPI_RESID, 10240, 36, 1},

@@ -342,14 +342,22 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
   // DMA sources: instruction c of this thread fills LDS slot q = (c*NW + wave)*64 + lane
   // of its matrix (row q / CH, swizzled slot q % CH, logical chunk slot ^ f(row)).
   const char *pa[AR];
-  const char *pb[BR];
+  // The W rows of DMA instruction c are instruction 0's plus c * BROWS when
+  // every round is whole and the step keeps the chunk swizzle (a multiple of
+  // 64 rows for 8-chunk rows, 16 for 4-chunk rows): one pointer and a uniform
+  // stride then replace BR pointers (registers the two-stage 128-byte tiles
+  // need for their fragments).
+  constexpr int BROWS = NW * 64 / CHW;
+  constexpr bool BSTRIDE = BG % NW == 0 && BROWS % (CHW == 8 ? 64 : 16) == 0;
+  const char *pb[BSTRIDE ? 1 : BR];
+  const size_t bstep = (size_t)BROWS * rowbw;
 #pragma unroll
   for (int c = 0; c < AR; ++c) {
     const int q = min(c * NW + wave, AG - 1) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
     pa[c] = g.A + (size_t)min(m0 + r, M - 1) * rowb + kb0 + ch * 16;
   }
 #pragma unroll
-  for (int c = 0; c < BR; ++c) {
+  for (int c = 0; c < (BSTRIDE ? 1 : BR); ++c) {
     const int q = min(c * NW + wave, BG - 1) * 64 + lane, r = q / CHW, ch = swz<CHW>(r, q % CHW);
     pb[c] = g.W + (size_t)(n0 + r) * rowbw + kb0w + ch * 16;
   }
@@ -363,7 +371,10 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
       dma16(pa[x] + ko, st + (uint32_t)(min(x * NW + uwave, AG - 1) * 64) * 16u);
     } else {
       const int c = x - AR;
-      dma16(pb[c] + (W8 ? ko / 2 : ko), st + (uint32_t)(ACH + min(c * NW + uwave, BG - 1) * 64) * 16u);
+      const char *src;
+      if constexpr (BSTRIDE) src = pb[0] + c * bstep;
+      else src = pb[c];
+      dma16(src + (W8 ? ko / 2 : ko), st + (uint32_t)(ACH + min(c * NW + uwave, BG - 1) * 64) * 16u);
     }
   };
 
