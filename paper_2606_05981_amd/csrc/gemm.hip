@@ -54,11 +54,11 @@ static const TileChoice kChoices[] = {
     {4096, 2048, EPI_QKV, 768, 12, 1},    {2048, 2048, EPI_RESID, 768, 12, 2},
     {12288, 2048, EPI_SWIGLU, 768, 3, 1},  {2048, 6144, EPI_RESID, 768, 14, 2},
     {4096, 2048, EPI_QKV, 1536, 36, 1},   {2048, 2048, EPI_RESID, 1536, 14, 1},
-    {12288, 2048, EPI_SWIGLU, 1536, 32, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
-    {4096, 2048, EPI_QKV, 3072, 27, 1},   {2048, 2048, EPI_RESID, 3072, 8, 1},
-    {12288, 2048, EPI_SWIGLU, 3072, 32, 1}, {2048, 6144, EPI_RESID, 3072, 8, 1},
-    {4096, 2048, EPI_QKV, 10240, 27, 1},  {2048, 2048, EPI_RESID, 10240, 36, 1},
-    {12288, 2048, EPI_SWIGLU, 10240, 38, 1}, {2048, 6144, EPI_RESID, 10240, 12, 1},
+    {12288, 2048, EPI_SWIGLU, 1536, 33, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
+    {4096, 2048, EPI_QKV, 3072, 38, 1},   {2048, 2048, EPI_RESID, 3072, 8, 1},
+    {12288, 2048, EPI_SWIGLU, 3072, 33, 1}, {2048, 6144, EPI_RESID, 3072, 8, 1},
+    {4096, 2048, EPI_QKV, 10240, 38, 1},  {2048, 2048, EPI_RESID, 10240, 36, 1},
+    {12288, 2048, EPI_SWIGLU, 10240, 33, 1}, {2048, 6144, EPI_RESID, 10240, 12, 1},
     // vision tower (width 1024, MLP 4096, 768-value patches, 2x2 merger to 2048):
     // 16 images of 256 patches, merger at 1024 rows
     {3072, 1024, EPI_QKV, 4096, 27, 1},   {1024, 1024, EPI_RESID, 4096, 12, 1},
@@ -142,6 +142,9 @@ hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void 
   const int esz = mode == MODE_F32 ? 4 : 2;
   if (epi == EPI_QKV && (!qe || (qe->hd != 64 && qe->hd != 128))) return hipErrorInvalidValue;
   if (w8 && !col_scale) return hipErrorInvalidValue;
+  // the kernel addresses both operands with 32-bit byte offsets
+  if ((size_t)M * K * esz > 0xFFFFFFFFull || (size_t)N * K * (w8 ? 1 : esz) > 0xFFFFFFFFull)
+    return hipErrorInvalidValue;
   if (tile < 0 || tile >= kNumTiles || splits < 1 ||
       !tile_fits(tile, N, K, esz, epi, splits, epi == EPI_QKV ? qe->hd : 32, w8) ||
       (splits > 1 && epi != EPI_PARTIAL))

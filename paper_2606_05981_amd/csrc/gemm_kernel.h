@@ -119,18 +119,20 @@ __device__ __forceinline__ void wait_stages(int after) {
 // the MFMAs that follow a stage's loads. The asm form is invisible to that
 // pass; the kernel orders these loads itself with explicit vmcnt waits and
 // barriers, and waits for all of them before it ends.
+// The source is a wave-uniform base (SGPRs) plus a 32-bit lane offset, so
+// each load needs one VGPR instead of a 64-bit address.
 // M0 is saved and restored around the load (the compiler reserves it), and
 // one wait state separates the M0 write from the load that reads it.
-__device__ __forceinline__ void dma16(const void *g, uint32_t lds_base) {
+__device__ __forceinline__ void dma16(const void *base, uint32_t off, uint32_t lds_base) {
   uint32_t saved;
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %2\n\t"
+      "s_mov_b32 m0, %3\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)
-      : "v"(g), "s"(lds_base)
+      : "v"(off), "s"(base), "s"(lds_base)
       : "memory");
 }
 
@@ -341,25 +343,25 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
 
   // DMA sources: instruction c of this thread fills LDS slot q = (c*NW + wave)*64 + lane
   // of its matrix (row q / CH, swizzled slot q % CH, logical chunk slot ^ f(row)).
-  const char *pa[AR];
-  // The W rows of DMA instruction c are instruction 0's plus c * BROWS when
-  // every round is whole and the step keeps the chunk swizzle (a multiple of
-  // 64 rows for 8-chunk rows, 16 for 4-chunk rows): one pointer and a uniform
-  // stride then replace BR pointers (registers the two-stage 128-byte tiles
-  // need for their fragments).
+  // As 32-bit byte offsets from g.A and g.W (the host keeps both matrices
+  // under 4 GiB). The W rows of DMA instruction c are instruction 0's plus
+  // c * BROWS when every round is whole and the step keeps the chunk swizzle
+  // (a multiple of 64 rows for 8-chunk rows, 16 for 4-chunk rows): one offset
+  // and a uniform stride then replace BR of them (registers the two-stage
+  // 128-byte tiles need for their fragments).
   constexpr int BROWS = NW * 64 / CHW;
   constexpr bool BSTRIDE = BG % NW == 0 && BROWS % (CHW == 8 ? 64 : 16) == 0;
-  const char *pb[BSTRIDE ? 1 : BR];
+  uint32_t pa[AR], pb[BSTRIDE ? 1 : BR];
   const size_t bstep = (size_t)BROWS * rowbw;
 #pragma unroll
   for (int c = 0; c < AR; ++c) {
     const int q = min(c * NW + wave, AG - 1) * 64 + lane, r = q / CH, ch = swz<CH>(r, q % CH);
-    pa[c] = g.A + (size_t)min(m0 + r, M - 1) * rowb + kb0 + ch * 16;
+    pa[c] = (uint32_t)((size_t)min(m0 + r, M - 1) * rowb + ch * 16);
   }
 #pragma unroll
   for (int c = 0; c < (BSTRIDE ? 1 : BR); ++c) {
     const int q = min(c * NW + wave, BG - 1) * 64 + lane, r = q / CHW, ch = swz<CHW>(r, q % CHW);
-    pb[c] = g.W + (size_t)(n0 + r) * rowbw + kb0w + ch * 16;
+    pb[c] = (uint32_t)((size_t)(n0 + r) * rowbw + ch * 16);
   }
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
   const int uwave = __builtin_amdgcn_readfirstlane(wave);   // wave-uniform in an SGPR
@@ -368,13 +370,12 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
     const uint32_t st = lds0 + (uint32_t)(slot * STAGE) * 16u;
     const size_t ko = (size_t)ks * ROWB;
     if (x < AR) {
-      dma16(pa[x] + ko, st + (uint32_t)(min(x * NW + uwave, AG - 1) * 64) * 16u);
+      dma16(g.A + kb0 + ko, pa[x], st + (uint32_t)(min(x * NW + uwave, AG - 1) * 64) * 16u);
     } else {
       const int c = x - AR;
-      const char *src;
-      if constexpr (BSTRIDE) src = pb[0] + c * bstep;
-      else src = pb[c];
-      dma16(src + (W8 ? ko / 2 : ko), st + (uint32_t)(ACH + min(c * NW + uwave, BG - 1) * 64) * 16u);
+      const char *wb = g.W + kb0w + (W8 ? ko / 2 : ko);
+      if constexpr (BSTRIDE) dma16(wb + c * bstep, pb[0], st + (uint32_t)(ACH + min(c * NW + uwave, BG - 1) * 64) * 16u);
+      else dma16(wb, pb[c], st + (uint32_t)(ACH + min(c * NW + uwave, BG - 1) * 64) * 16u);
     }
   };
 
