@@ -35,7 +35,9 @@ static const double kTileRate[kNumTiles] = {959, 944, 895, 850, 850, 884, 850, 8
 
 // Measured choices (MI355X sweep of every tile and split count, weights
 // rotated through 600 MB so that they stream from HBM; at 96 and 192 rows
-// timed together with the kernel that consumes the product) for the decoder's four
+// timed together with the kernel that consumes the product; the leading
+// candidates then timed again round robin, three times each, since a sweep
+// in fixed order drifts with the clock as the card warms) for the decoder's four
 // projections (D 2048 / FFN 6144 / 16+8+8 heads of 128) at 96 ... 10240 rows. A K split is only
 // kept where it still wins after the consumer's extra pass over the fp32
 // partial sums (at 1536 rows two QKV partials cost 16 us to add up, more than
@@ -47,10 +49,10 @@ struct TileChoice {
   int n, k, epi, m, tile, splits;
 };
 static const TileChoice kChoices[] = {
-    {4096, 2048, EPI_QKV, 96, 12, 4},     {2048, 2048, EPI_RESID, 96, 16, 4},
+    {4096, 2048, EPI_QKV, 96, 13, 4},     {2048, 2048, EPI_RESID, 96, 13, 4},
     {12288, 2048, EPI_SWIGLU, 96, 12, 2},  {2048, 6144, EPI_RESID, 96, 13, 8},
-    {4096, 2048, EPI_QKV, 192, 12, 2},    {2048, 2048, EPI_RESID, 192, 16, 4},
-    {12288, 2048, EPI_SWIGLU, 192, 14, 1}, {2048, 6144, EPI_RESID, 192, 23, 8},
+    {4096, 2048, EPI_QKV, 192, 12, 2},    {2048, 2048, EPI_RESID, 192, 13, 4},
+    {12288, 2048, EPI_SWIGLU, 192, 12, 1}, {2048, 6144, EPI_RESID, 192, 14, 8},
     {4096, 2048, EPI_QKV, 768, 12, 1},    {2048, 2048, EPI_RESID, 768, 12, 2},
     {12288, 2048, EPI_SWIGLU, 768, 3, 1},  {2048, 6144, EPI_RESID, 768, 14, 2},
     {4096, 2048, EPI_QKV, 1536, 36, 1},   {2048, 2048, EPI_RESID, 1536, 14, 1},
