@@ -128,7 +128,9 @@ typedef struct {
 /* Host-only check of a configuration. Returns MTE_OK, MTE_E_INVALID (null,
  * non-positive sizes, Hq % Hkv != 0, sections not summing to d/2, bad enum)
  * or MTE_E_UNSUPPORTED (head_dim not 64/128, D or F not multiples of 256,
- * capacities beyond the built limits). Makes no HIP call. */
+ * capacities beyond the built limits: at most 2^24 - 1 tokens, and every
+ * projection operand -- max_tokens x its K, or a weight matrix -- under 4 GiB).
+ * Makes no HIP call. */
 int mte_config_validate(const mte_config *cfg);
 
 /* Host-only check of one batch against a configuration (the checks

@@ -86,7 +86,9 @@ typedef struct mte_vision mte_vision;
 
 /* Host-only check: MTE_OK, MTE_E_INVALID (null, non-positive sizes,
  * hidden != n_heads*head_dim, bad enum) or MTE_E_UNSUPPORTED (head_dim not
- * 64/128, widths not multiples of 64, hidden > 4096). */
+ * 64/128, widths not multiples of 64, hidden > 4096, more than 2^24 patches,
+ * or a projection operand -- patches x its K, or a weight matrix -- of 4 GiB
+ * or more). */
 int mte_vision_config_validate(const mte_vision_config *cfg);
 
 /* Copies and repacks the weights (the caller may free its copies after

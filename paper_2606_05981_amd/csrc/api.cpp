@@ -130,6 +130,12 @@ int mte_config_validate(const mte_config *c) {
       (c->n_kv_heads * c->head_dim) % 128)
     return MTE_E_UNSUPPORTED;
   if (c->max_tokens > kMaxTokens) return MTE_E_UNSUPPORTED;
+  // the projection kernels address each operand with 32-bit byte offsets
+  const int64_t es = c->dtype == MTE_F32 ? 4 : 2;
+  const int64_t qd = (int64_t)c->n_q_heads * c->head_dim, qkv = qd + 2LL * c->n_kv_heads * c->head_dim;
+  const int64_t kmax = std::max<int64_t>(std::max<int64_t>(c->hidden, c->ffn), qd);
+  const int64_t nmax = std::max<int64_t>(std::max<int64_t>(2LL * c->ffn, qkv), c->hidden);
+  if ((int64_t)c->max_tokens * kmax * es > 0xFFFFFFFFLL || nmax * kmax * es > 0xFFFFFFFFLL) return MTE_E_UNSUPPORTED;
   return MTE_OK;
 }
 

@@ -83,6 +83,12 @@ int mte_vision_config_validate(const mte_vision_config *c) {
   if (c->max_side < side) return MTE_E_INVALID;
   const int64_t per = ((int64_t)c->max_side / c->patch) * ((int64_t)c->max_side / c->patch);
   if ((int64_t)c->max_images * per > (1 << 24)) return MTE_E_UNSUPPORTED;
+  // the projection kernels address each operand with 32-bit byte offsets
+  const int64_t es = c->dtype == MTE_F32 ? 4 : 2, mm = (int64_t)c->merge * c->merge;
+  const int64_t kmax = std::max<int64_t>(std::max<int64_t>(kp, c->hidden), std::max<int64_t>(c->ffn, mm * c->hidden));
+  const int64_t nmax = std::max<int64_t>(std::max<int64_t>(3LL * c->hidden, c->ffn), std::max<int64_t>(mm * c->hidden, c->out_hidden));
+  if ((int64_t)c->max_images * per * kmax * es > 0xFFFFFFFFLL || nmax * kmax * es > 0xFFFFFFFFLL)
+    return MTE_E_UNSUPPORTED;
   return MTE_OK;
 }
 

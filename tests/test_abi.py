@@ -64,6 +64,9 @@ def test_valid_configs(B):
     (dict(hidden=2000), -5), (dict(ffn=6000), -5),
     (dict(n_q_heads=12, n_kv_heads=4), -5),          # group of 3 query heads
     (dict(max_tokens=1 << 24), -5),
+    (dict(max_tokens=400_000), -5),                  # 400k x 6144 fp16 activations exceed 4 GiB
+    (dict(max_tokens=200_000, dtype=0), -5),         # ... in fp32 already at 200k
+    (dict(max_tokens=300_000), 0),
     (dict(weight_format=2), -1), (dict(weight_format=-1), -1),
     (dict(weight_format=1, dtype=0), -5),           # e4m3 weights need bf16 storage
 ])
@@ -174,7 +177,9 @@ def test_vision_configs(B):
                    (dict(patch=10), -5),                    # 3*10*10 not a multiple of 64
                    (dict(depth=-1), -1), (dict(max_images=0), -1), (dict(max_side=16), -1),
                    (dict(ln_eps=0.0), -1), (dict(dtype=3), -1),
-                   (dict(hidden=8192, n_heads=64, head_dim=128), -5)]:
+                   (dict(hidden=8192, n_heads=64, head_dim=128), -5),
+                   (dict(max_images=2100), -5),             # 2100 x 256 patches x 4096 fp16 exceed 4 GiB
+                   (dict(max_images=2000), 0)]:
         assert B.mte_vision_config_validate(_vision(B, **kw)) == st, kw
 
 
