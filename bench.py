@@ -278,6 +278,68 @@ def run_overlap(torch, name, steps, warmup):
             "te_ms_per_step_alone": round(te_s * 1e3 / steps, 4)}
 
 
+def run_regimes(torch, steps, warmup, names=("stack_b8", "stack_b32_l320", "stack_mixed32")):
+    """The other measured regimes of the same 28-layer encoder: 8 frames of 96 tokens,
+    32 sequences of 320 tokens, and 32 sequences of mixed lengths (96..320). One encoder
+    sized for the largest serves all three; each step is captured as a HIP graph and
+    replayed, timed with HIP events (median, and the model's TFLOP/s against the
+    published bf16 peak)."""
+    from paper_2606_05981_amd import binding as B
+    from paper_2606_05981_amd.encoder import TextEncoder
+    from synth import workloads as W
+    wls = [W.workload(n) for n in names]
+    dims = wls[0].dims
+    lens_all = [W.seq_lens(w.layouts) for w in wls]
+    cfg = B.make_config(dims.n_layers, dims.hidden, dims.n_q_heads, dims.n_kv_heads,
+                        dims.head_dim, dims.ffn, rms_eps=dims.rms_eps, rope_theta=dims.rope_theta,
+                        mrope_section=dims.mrope_section, mrope_layout=dims.mrope_layout,
+                        qk_norm=dims.qk_norm, dtype=B.MTE_BF16, out_dtype=B.MTE_F32,
+                        max_tokens=max(sum(l) for l in lens_all),
+                        max_batch=max(len(l) for l in lens_all), max_seq=max(max(l) for l in lens_all))
+    enc = TextEncoder.from_host(cfg, (W.layer_weights(dims, l) for l in range(dims.n_layers)),
+                                W.final_norm_gain(dims))
+    out = {}
+    for wl, lens in zip(wls, lens_all):
+        T = sum(lens)
+        emb = torch.from_numpy(W.embeddings(dims, wl.layouts)).to("cuda", torch.bfloat16)
+        layouts = [(q.n_text_before, q.grid_t, q.grid_h, q.grid_w, q.n_text_after) for q in wl.layouts]
+        o = torch.empty((T, dims.hidden), dtype=torch.float32, device="cuda")
+        pos = torch.empty((3, T), dtype=torch.int32, device="cuda")
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+
+        def step(st):
+            B.mte_build_positions(layouts, pos.data_ptr(), st.cuda_stream)
+            B.mte_encode(enc.handle, emb.data_ptr(), pos.data_ptr(), lens, len(lens), o.data_ptr(), st.cuda_stream)
+
+        with torch.cuda.stream(side):
+            for _ in range(warmup):
+                step(side)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph, stream=side):
+                step(side)
+        torch.cuda.current_stream().wait_stream(side)
+        for _ in range(warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        for e0, e1 in evs:
+            e0.record()
+            graph.replay()
+            e1.record()
+        torch.cuda.synchronize()
+        per = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+        ms = per[len(per) // 2]
+        tflops = step_flops(dims, lens) / (ms * 1e-3) / 1e12
+        out[wl.name] = {"sequences": len(lens), "tokens_per_step": T, "min_len": min(lens), "max_len": max(lens),
+                        "ms_per_step_median": round(ms, 4), "tokens_per_s": round(T / ms * 1e3, 1),
+                        "frames_per_s": round(len(lens) / ms * 1e3, 1), "model_tflops": round(tflops, 1),
+                        "frac_of_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4), "steps": len(per)}
+        del graph
+    enc.close()
+    return out
+
+
 def run_prefix(torch, prefix, steps, warmup, frames=16):
     """Shared prefix (the paper's system prompt, Sec. V): `frames` frames whose sequences all
     start with the same `prefix` text tokens, then an 8x8 image grid and 32 instruction tokens.
@@ -561,6 +623,8 @@ def main():
     ap.add_argument("--workload", default="stack_b16")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-batch1", action="store_true")
+    ap.add_argument("--no-regimes", action="store_true",
+                    help="skip the 8 x 96, 32 x 320 and mixed 32-sequence regimes")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the known-size copy used to calibrate HBM byte counters")
     ap.add_argument("--prefix", type=int, default=0,
@@ -656,6 +720,8 @@ def main():
                                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                           "frac": round(wbytes / t1 / 1e9 / PEAK_HBM_GBS, 4),
                                           "bytes_per_step": wbytes}}
+    if not args.no_regimes:
+        res["other_regimes"] = run_regimes(torch, min(K, 10), args.warmup)
     if not args.no_vision:
         res["vision_tower"] = run_vision(torch, K, args.warmup)
         if not args.no_pipeline:
