@@ -15,7 +15,11 @@ constexpr int kNumTiles = sizeof(kTiles) / sizeof(kTiles[0]);
 
 int gemm_num_tiles() { return kNumTiles; }
 
-// epilogue; gate/up pairs sit inside every 32-column block).
+// Whether tile `id` can run an (N, K, epilogue, splits) product: N a multiple of
+// its width, each K split a whole number of stages, fp32 operands only on the
+// tiles built for them, e4m3 weights only on 128-byte stages. col_align: columns
+// a wave must cover in whole units (heads for the QKV epilogue; gate/up pairs
+// sit inside every 32-column block).
 static bool tile_fits(int id, int N, int K, int esz, int epi, int splits, int col_align = 32,
                       bool w8 = false) {
   const TileCfg &t = kTiles[id];

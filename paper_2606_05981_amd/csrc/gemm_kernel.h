@@ -746,8 +746,6 @@ static hipError_t run_id(int id, const GemmArgs &a, int splits, hipStream_t s) {
   return hipErrorInvalidValue;
 }
 
-// col_align: columns a wave must cover in whole units (heads for the QKV
-
 template <int MODE>
 static hipError_t launch_mode(int epi, int tile, int splits, const GemmArgs &a, hipStream_t s) {
   switch (epi) {
