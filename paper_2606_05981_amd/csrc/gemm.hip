@@ -35,7 +35,7 @@ static bool tile_fits(int id, int N, int K, int esz, int epi, int splits, int co
 static const double kTileRate[kNumTiles] = {959, 944, 895, 850, 850, 884, 850, 850, 800, 819,
                                             640, 777, 860, 600, 700, 650, 550, 450, 600, 600,
                                             921, 850, 850, 714, 766, 800, 1026, 1018, 850, 728,
-                                            803, 950, 950, 950, 950, 950, 850, 850, 950};
+                                            803, 950, 950, 1150, 1106, 1084, 940, 1044, 1117};
 
 // Measured choices (MI355X sweep of every tile and split count, weights
 // rotated through 600 MB so that they stream from HBM; at 96 and 192 rows
