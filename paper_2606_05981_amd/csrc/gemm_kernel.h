@@ -102,15 +102,6 @@ __device__ __forceinline__ void wait_vm_lds0() {
   static_assert(n >= 0 && n < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((n & 0xF) | (0x7 << 4) | (0x0 << 8) | ((n >> 4) << 14));
 }
-// Waits until at most after*LOADS vector-memory operations are pending,
-// for a wave-uniform after in [0, 3].
-template <int LOADS>
-__device__ __forceinline__ void wait_stages(int after) {
-  if (after >= 3) wait_vm<(3 * LOADS < 64 ? 3 * LOADS : 0)>();
-  else if (after == 2) wait_vm<(2 * LOADS < 64 ? 2 * LOADS : 0)>();
-  else if (after == 1) wait_vm<LOADS>();
-  else wait_vm<0>();
-}
 
 // 16-byte global -> LDS copy without a register round trip: lane i of the
 // wave writes lds_base + 16*i, lds_base wave-uniform. Written as inline asm
