@@ -7,7 +7,7 @@
 namespace mte {
 
 static const TileCfg kTiles[] = {
-#define MTE_TILE_INFO(id, bm, bn, wm, wn, rowb, p, occ, f32) {bm, bn, wm, wn, rowb, occ, f32},
+#define MTE_TILE_INFO(id, bm, bn, wm, wn, rowb, p, occ, f32) {bm, bn, wm, wn, rowb, p, occ, f32},
     MTE_TILE_TABLE(MTE_TILE_INFO)
 #undef MTE_TILE_INFO
 };
@@ -24,6 +24,7 @@ static bool tile_fits(int id, int N, int K, int esz, int epi, int splits, int co
                       bool w8 = false) {
   const TileCfg &t = kTiles[id];
   if (N % t.bn || (esz == 4 && !t.f32) || (w8 && t.rowb != 128)) return false;
+  if (t.p * (t.bm + (w8 ? t.bn / 2 : t.bn)) * t.rowb * t.occ > 160 * 1024) return false;   // LDS ring
   const int ks = t.rowb / esz;
   if (K % splits || (K / splits) % ks) return false;
   if (epi == EPI_QKV && (t.bn / t.wn) % col_align) return false;

@@ -655,7 +655,7 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
 
 // A tile configuration is a compile-time instantiation of k_gemm.
 struct TileCfg {
-  int bm, bn, wm, wn, rowb, occ, f32;
+  int bm, bn, wm, wn, rowb, p, occ, f32;
 };
 
 template <int MODE, int BM, int BN, int WM, int WN, int ROWB, int P, int EPI, int OCC, int F32>
@@ -681,9 +681,10 @@ static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
 
 // Tile table: id -> instantiation (bm, bn, wave layout wm x wn, bytes of K
 // per row per stage, LDS ring stages, workgroups per CU, built for fp32
-// operands too). The LDS ring (P * (bm + bn) * rowb bytes) must fit
-// 160 KB / occ; bm * rowb / 16 and bn * rowb / 16 must be multiples of 64
-// (whole 64-chunk DMA groups).
+// operands too). The LDS ring (P * (bm + bn) * rowb bytes, bn / 2 for e4m3
+// weights) must fit 160 KB / occ; the planner skips a tile whose ring does
+// not fit the operand format. bm * rowb / 16 and bn * rowb / 16 must be
+// multiples of 64 (whole 64-chunk DMA groups).
 #define MTE_TILE_TABLE(X)                    \
   X(0, 256, 256, 2, 2, 64, 4, 1, 0)          \
   X(1, 256, 192, 2, 2, 64, 4, 1, 0)          \
