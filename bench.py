@@ -59,13 +59,55 @@ def gemm_flops(dims, T):
             "gate_up": 2 * T * 2 * F * D, "down": 2 * T * D * F}
 
 
+KERNEL_CLASSES = {0: "qkv_gemm", 1: "attention", 2: "o_gemm", 3: "gate_up_gemm", 4: "down_gemm"}
+
+
+def kernel_work(dims, lens):
+    """Algorithmic flops and bytes of one launch of each timed kernel class at these
+    sequence lengths (one layer): the projections read their fp16 weights and fp16 input
+    once and write their output (QKV fp32; SwiGLU fp16; the residual projections read
+    and write the fp32 residual stream); attention reads fp32 q/k/v and writes fp16 o.
+    With a K split the timed launch is the split GEMM alone (its partial sums are added
+    by the next kernel); its bytes are still counted as the finished product's."""
+    T = sum(lens)
+    D, F, d, hq, hkv = dims.hidden, dims.ffn, dims.head_dim, dims.n_q_heads, dims.n_kv_heads
+    nqkv = (hq + 2 * hkv) * d
+    g = gemm_flops(dims, T)
+    att = sum(4 * hq * d * L * (L + 1) // 2 for L in lens)
+    return {
+        0: (g["qkv"], 2 * nqkv * D + 2 * T * D + 4 * T * nqkv),
+        1: (att, 4 * T * nqkv + 2 * T * hq * d),
+        2: (g["o"], 2 * D * hq * d + 2 * T * hq * d + 8 * T * D),
+        3: (g["gate_up"], 2 * 2 * F * D + 2 * T * D + 2 * T * F),
+        4: (g["down"], 2 * D * F + 2 * T * F + 8 * T * D),
+    }
+
+
+def kernel_table(dims, lens, kern):
+    """Per-kernel average launch time (HIP events on the launch stream) and its rates
+    against both published peaks."""
+    work = kernel_work(dims, lens)
+    out = {}
+    for cls, (n, ms) in kern.items():
+        us = ms * 1e3 / max(n, 1)
+        fl, by = work[cls]
+        out[KERNEL_CLASSES[cls]] = {
+            "avg_launch_us": round(us, 2), "launches": n,
+            "tflops": round(fl / (us * 1e-6) / 1e12, 1),
+            "frac_bf16_peak": round(fl / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "gbs": round(by / (us * 1e-6) / 1e9, 1),
+            "frac_hbm_peak": round(by / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+            "flops_per_launch": fl, "algorithmic_bytes_per_launch": by}
+    return out
+
+
 def step_flops(dims, lens):
     g = sum(gemm_flops(dims, sum(lens)).values())
     att = sum(4 * dims.n_q_heads * dims.head_dim * L * (L + 1) // 2 for L in lens)
     return dims.n_layers * (g + att)
 
 
-def run_workload(torch, name, steps, warmup, timing_class=None, use_graph=True, weight_format=0):
+def run_workload(torch, name, steps, warmup, timing_classes=(), use_graph=True, weight_format=0):
     from paper_2606_05981_amd import binding as B
     from paper_2606_05981_amd.encoder import TextEncoder, build_positions
     from synth import workloads as W
@@ -112,19 +154,20 @@ def run_workload(torch, name, steps, warmup, timing_class=None, use_graph=True, 
             graph.replay()
         torch.cuda.synchronize()
     run_step = graph.replay if graph is not None else step
-    # Eager pass over the same steps: the library records HIP events around
-    # every launch of the timed kernel class on the launch stream.
-    kern = None
-    if timing_class is not None:
-        B.mte_timing_enable(enc.handle, timing_class, steps * dims.n_layers)
+    # Eager passes over the same steps, one per timed kernel class: the library
+    # records HIP events around every launch of that class on the launch stream.
+    kern = {}
     torch.cuda.synchronize()
     te = time.perf_counter()
     for _ in range(steps):
         step()
     torch.cuda.synchronize()
     eager_s = time.perf_counter() - te
-    if timing_class is not None:
-        kern = B.mte_timing_read(enc.handle)
+    for cls in timing_classes:
+        B.mte_timing_enable(enc.handle, cls, steps * dims.n_layers)
+        for _ in range(steps):
+            step()
+        kern[cls] = B.mte_timing_read(enc.handle)
         B.mte_timing_disable(enc.handle)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -150,11 +193,12 @@ def run_workload(torch, name, steps, warmup, timing_class=None, use_graph=True, 
                 eager_s=eager_s, graph=graph is not None, stats=stats)
 
 
-def cpu_baseline(min_seconds=10.0):
-    """The fp64 oracle on the host cores, on a bounded sample of the 16 x 96-token batch:
-    whole 28-layer forwards of its frames one at a time (frames are independent
-    sequences), frame 0, 1, ... until at least `min_seconds` have been timed."""
-    import numpy as np
+def cpu_baseline():
+    """The fp64 oracle on the host cores, once over each workload of the survey's
+    configurations 0-3: the tiny fp32 decoder (32 tokens), one full-width layer (96
+    tokens) and the 28-layer stack at one frame (96 tokens), 8 frames and 16 frames
+    (packed batches of 96-token frames). `value` is the 16-frame rate, the benchmark's
+    own workload; about 15 s of host time in all."""
     from oracle import te_oracle as O
     from synth import workloads as W
     try:
@@ -162,34 +206,43 @@ def cpu_baseline(min_seconds=10.0):
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:
         cores = os.cpu_count() or 1
-    wl = W.workload("stack_b16")
-    dims = wl.dims
-    lens = W.seq_lens(wl.layouts)
-    emb = W.embeddings(dims, wl.layouts)
-    pos = O.positions(wl.layouts)
-    ws = [W.layer_weights(dims, l) for l in range(dims.n_layers)]
-    fin = W.final_norm_gain(dims)
-    starts = np.cumsum([0] + lens)
-    frames, toks, t0 = 0, 0, time.perf_counter()
-    while True:
-        f = frames % len(lens)
-        sl = slice(starts[f], starts[f + 1])
-        O.encode(emb[sl], pos[:, sl], [lens[f]], dims, lambda l: ws[l], fin)
-        frames += 1
-        toks += lens[f]
-        dt = time.perf_counter() - t0
-        if dt >= min_seconds:
-            break
+
+    def rate(name, min_s):
+        wl = W.workload(name)
+        dims = wl.dims
+        lens = W.seq_lens(wl.layouts)
+        emb = W.embeddings(dims, wl.layouts)
+        pos = O.positions(wl.layouts)
+        ws = [W.layer_weights(dims, l) for l in range(dims.n_layers)]
+        fin = W.final_norm_gain(dims)
+        runs, t0 = 0, time.perf_counter()
+        while True:
+            O.encode(emb, pos, lens, dims, lambda l: ws[l], fin)
+            runs += 1
+            dt = time.perf_counter() - t0
+            if dt >= min_s:
+                break
+        T = sum(lens)
+        return {"workload": name, "layers": dims.n_layers, "tokens": T, "runs": runs,
+                "seconds": round(dt, 2), "tokens_per_s": round(T * runs / dt, 2),
+                "frames_per_s": round(len(lens) * runs / dt, 3)}
+
+    cfgs = {"tiny_fp32": rate("tiny_fp32", 1.0), "layer1_b1": rate("layer1_b1", 2.0),
+            "stack_b1": rate("stack_b1", 0.0), "stack_b8": rate("stack_b8", 0.0),
+            "stack_b16": rate("stack_b16", 0.0)}
     cpu = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
             cpu = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
     except (OSError, StopIteration):
         pass
-    return {"value": round(toks / dt, 2), "unit": "tokens/s", "cores": int(cores),
+    main = cfgs["stack_b16"]
+    return {"value": main["tokens_per_s"], "unit": "tokens/s", "cores": int(cores),
             "kind": "oracle", "cpu_model": cpu, "host_cpus": os.cpu_count(),
-            "sample": f"{frames} frame(s) of the 16 x 96-token batch, each a whole 28-layer "
-                      f"forward ({toks} tokens in {dt:.1f} s, fp64 numpy oracle)"}
+            "sample": f"the 16 x 96-token batch as one packed batch, one whole 28-layer forward "
+                      f"({main['tokens']} tokens in {main['seconds']} s, fp64 numpy oracle); the other "
+                      "configurations' rates in 'configs'",
+            "configs": cfgs}
 
 
 def run_overlap(torch, name, steps, warmup):
@@ -347,9 +400,8 @@ def run_prefix(torch, prefix, steps, warmup, frames=16):
     then each frame's own 96 tokens attending to its cached keys / values); both captured as
     HIP graphs and replayed."""
     import numpy as np
-    from oracle import te_oracle as O   # positions of the full sequences (input preparation)
     from paper_2606_05981_amd import binding as B
-    from paper_2606_05981_amd.encoder import TextEncoder
+    from paper_2606_05981_amd.encoder import TextEncoder, build_positions
     from synth import workloads as W
 
     dims = W.DIMS_FULL
@@ -365,12 +417,14 @@ def run_prefix(torch, prefix, steps, warmup, frames=16):
                                 W.final_norm_gain(dims))
     enc.reserve_prefix(prefix)
     emb_np = W.embeddings(dims, full)
-    pos_np = O.positions(full).astype(np.int32)
     own = np.concatenate([np.arange(f * L + prefix, (f + 1) * L) for f in range(frames)])
     dev = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to("cuda", dt)
-    emb, pos = dev(emb_np, torch.bfloat16), dev(pos_np, torch.int32)
-    p_emb, p_pos = dev(emb_np[:prefix], torch.bfloat16), dev(pos_np[:, :prefix], torch.int32)
-    o_emb, o_pos = dev(emb_np[own], torch.bfloat16), dev(pos_np[:, own], torch.int32)
+    emb = dev(emb_np, torch.bfloat16)
+    # positions of the full sequences, built on the device (mte_build_positions)
+    pos = build_positions([(q.n_text_before, q.grid_t, q.grid_h, q.grid_w, q.n_text_after) for q in full])
+    own_g = torch.from_numpy(own).cuda()
+    p_emb, p_pos = dev(emb_np[:prefix], torch.bfloat16), pos[:, :prefix].contiguous()
+    o_emb, o_pos = dev(emb_np[own], torch.bfloat16), pos[:, own_g].contiguous()
     out = torch.empty((T, dims.hidden), dtype=torch.float32, device="cuda")
     out_p = torch.empty((prefix, dims.hidden), dtype=torch.float32, device="cuda")
     out_o = torch.empty((len(own), dims.hidden), dtype=torch.float32, device="cuda")
@@ -404,7 +458,7 @@ def run_prefix(torch, prefix, steps, warmup, frames=16):
         torch.cuda.synchronize()
         dt = (time.perf_counter() - t0) / steps
         res[name] = {"ms_per_step": round(dt * 1e3, 4), "frames_per_s": round(frames / dt, 1)}
-    dev_err = float((out[torch.from_numpy(own).cuda()] - out_o).abs().max() / out.pow(2).mean().sqrt())
+    dev_err = float((out[own_g] - out_o).abs().max() / out.pow(2).mean().sqrt())
     enc.close()
     res.update({"workload": f"{frames} frames x ({prefix} shared prefix + 8x8 image + 32 instruction) "
                             "tokens, 28 layers",
@@ -584,11 +638,29 @@ def copy_bandwidth(torch, mib=1024, reps=10):
     return round(2 * mib * (1 << 20) / dt / 1e9, 1)
 
 
+def _probe_lib():
+    """The measurement-only probe library (paper_2606_05981_amd/libmte_probe.so), built next
+    to libmte by the package's build step; it is not part of the encoder's C ABI."""
+    import ctypes
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2606_05981_amd", "libmte_probe.so"))
+    lib.mte_probe_mfma.restype = ctypes.c_int
+    lib.mte_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    return lib
+
+
 def mfma_rate(torch, blocks=512, iters=20000):
     """Dense fp16 matrix-core rate the device sustains under load (mte_probe_mfma: independent
     32x32x16 MFMA chains, no memory traffic), TFLOP/s: the measured counterpart of the
     published 2.5 PFLOP/s, which assumes the 2.4 GHz peak clock."""
-    from paper_2606_05981_amd import binding as B
+    lib = _probe_lib()
+
+    class _P:
+        @staticmethod
+        def mte_probe_mfma(b, i, sink, st):
+            if lib.mte_probe_mfma(b, i, sink, st) != 0:
+                raise RuntimeError("mte_probe_mfma failed")
+
+    B = _P
     sink = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
     st = torch.cuda.current_stream().cuda_stream
     B.mte_probe_mfma(blocks, iters // 10, sink.data_ptr(), st)
@@ -637,8 +709,10 @@ def main():
                     help="only run the vision tower and print its figures (for profiling)")
     ap.add_argument("--no-vision", action="store_true",
                     help="skip the vision-tower run (16 images of 256x256)")
-    ap.add_argument("--overlap", action="store_true",
-                    help="also measure the encoder on a side stream beside a main-stream GEMM load")
+    ap.add_argument("--profile-pass", action="store_true",
+                    help="only the main workload's warm-up and timed steps (for counter runs under rocprofv3)")
+    ap.add_argument("--no-overlap", action="store_true",
+                    help="skip the encoder on a side stream beside a main-stream GEMM load")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); frames are independent, "
@@ -654,13 +728,18 @@ def main():
         print(json.dumps({"vision_tower": run_vision(torch, args.steps, args.warmup)}), flush=True)
         return
 
-    main_run = run_workload(torch, args.workload, args.steps, args.warmup, timing_class=3)
+    if args.profile_pass:
+        r = run_workload(torch, args.workload, args.steps, args.warmup)
+        print(json.dumps({"profile_pass": args.workload, "ms_per_step": round(r["wall_s"] * 1e3 / args.steps, 4)}),
+              flush=True)
+        return
+    main_run = run_workload(torch, args.workload, args.steps, args.warmup, timing_classes=(0, 1, 2, 3, 4))
     dims, T = main_run["dims"], main_run["T"]
     K = args.steps
     ms_step = main_run["wall_s"] * 1e3 / K
     tok_s = T * K / main_run["wall_s"]
     frames_s = len(main_run["lens"]) * K / main_run["wall_s"]
-    n_launch, kern_ms = main_run["kern"]
+    n_launch, kern_ms = main_run["kern"][3]
     gu_flops = gemm_flops(dims, T)["gate_up"]
     # fp16 weights + fp16 normalised input + fp16 SwiGLU output
     gu_bytes = 2 * dims.ffn * dims.hidden * 2 + T * dims.hidden * 2 + T * dims.ffn * 2
@@ -681,8 +760,9 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "f16",
-        "precision": ("projections: fp16 MFMA operands (bf16 weights held exactly as "
-                      "power-of-two scaled fp16; activations rounded once to fp16), fp32 "
+        "precision": ("projections: fp16 MFMA operands (bf16 weights as power-of-two scaled "
+                      "fp16, exact for every weight down to 2^-31 of its matrix's largest "
+                      "magnitude; activations rounded once to fp16), fp32 "
                       "accumulate; attention: bf16 hi+lo split operands, fp32 softmax; fp32 "
                       "residual stream and norms"),
         "data": "synthetic (seeded random-init weights and embeddings)",
@@ -702,13 +782,17 @@ def main():
                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic(),
                      "algorithmic_bytes_per_launch": gu_bytes,
                      "avg_launch_us": round(avg_us, 2), "launches": n_launch,
-                     "flops_per_launch": gu_flops},
+                     "flops_per_launch": gu_flops,
+                     # the whole step (all kernels, algorithmic flops) against the same peak
+                     "step_achieved": round(total_tflops, 1),
+                     "step_frac": round(total_tflops / PEAK_BF16_TFLOPS, 4),
+                     "kernels": kernel_table(dims, main_run["lens"], main_run["kern"])},
     }
     measured = mfma_rate(torch)
     res["mfma_f16_tflops_measured"] = measured
     res["roofline"]["frac_of_measured_peak"] = round(achieved / measured, 4)
     if not args.no_batch1:
-        b1 = run_workload(torch, "stack_b1", K, args.warmup)
+        b1 = run_workload(torch, "stack_b1", K, args.warmup, timing_classes=(0, 1, 2, 3, 4))
         t1 = b1["wall_s"] / K
         wbytes = dims.n_layers * dims.params_per_layer * 2 + 2 * b1["T"] * dims.hidden * 2
         res["batch1"] = {"workload": "stack_b1: 1 frame x 96 tokens, 28 layers",
@@ -719,7 +803,9 @@ def main():
                          "hbm_roofline": {"bound": "hbm", "achieved": round(wbytes / t1 / 1e9, 1),
                                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                           "frac": round(wbytes / t1 / 1e9 / PEAK_HBM_GBS, 4),
-                                          "bytes_per_step": wbytes}}
+                                          "bytes_per_step": wbytes,
+                                          "frac_of_measured_copy": round(wbytes / t1 / 1e9 / res["hbm_copy_gbs_measured"], 4),
+                                          "kernels": kernel_table(dims, b1["lens"], b1["kern"])}}
     if not args.no_regimes:
         res["other_regimes"] = run_regimes(torch, min(K, 10), args.warmup)
     if not args.no_vision:
@@ -728,7 +814,7 @@ def main():
             res["frames_to_hidden"] = run_pipeline(torch, K, args.warmup)
     if not args.no_e4m3:
         res["e4m3_weights"] = run_e4m3(torch, args.workload, K, args.warmup, dims, not args.no_batch1)
-    if args.overlap:
+    if not args.no_overlap:
         res["side_stream_overlap"] = {
             "batch16": run_overlap(torch, args.workload, K, args.warmup),
             "batch1": run_overlap(torch, "stack_b1", K, args.warmup)}

@@ -80,9 +80,15 @@ typedef enum { MTE_WEIGHTS_DTYPE = 0, MTE_WEIGHTS_E4M3 = 1 } mte_weight_format;
  *  j%3==1 && j<3*s_h, w-driven if j%3==2 && j<3*s_w, t-driven otherwise.
  *  qk_norm: 1 applies a per-head RMSNorm (gain q_norm / k_norm) to q and k
  *  before the rotation.
- *  dtype: storage type of the weights, the embeddings and the bf16/f32
- *  GEMM operands (MTE_BF16: bf16 with fp32 accumulation and an fp32 residual
- *  stream; MTE_F32: fp32 throughout). out_dtype: type of out_hidden.
+ *  dtype: storage type of the weights and the embeddings (MTE_BF16: bf16
+ *  storage, fp32 accumulation and an fp32 residual stream; MTE_F32: fp32
+ *  throughout). With MTE_BF16 the projections run on fp16 matrix-core
+ *  operands: each weight matrix is converted at creation to fp16 times a
+ *  power of two that puts its largest magnitude in [2^14, 2^15), which holds
+ *  every bf16 weight of magnitude at least 2^-31 of that maximum exactly
+ *  (smaller ones round, with an absolute error below 2^-40 of the maximum);
+ *  activations are rounded once to fp16 behind power-of-two pre-scales
+ *  derived from static bounds. out_dtype: type of out_hidden.
  *  max_tokens / max_batch / max_seq: capacity the workspace is sized for.
  *  weight_format: mte_weight_format (MTE_WEIGHTS_E4M3 needs dtype MTE_BF16,
  *  else MTE_E_UNSUPPORTED). With e4m3 weights the encoder computes the same
@@ -172,7 +178,13 @@ int mte_encode_layers(mte_encoder *enc, const float *h_in, const int32_t *pos_th
                       const int32_t *seq_lens, int32_t batch, int32_t layer_begin,
                       int32_t layer_end, float *h_out, hipStream_t stream);
 
-/* Builds the (t,h,w) positions of a packed batch on the device.
+/* Builds the (t,h,w) positions of a packed batch on the device. This is the
+ * step whose host round trip the paper's encoder pays inside its rotary-position
+ * code and has to hide on a side stream (Sec. I; Sec. III-B, "CUDA-stream
+ * pipelining"); here the positions follow from the host layout descriptors
+ * alone and are written by one kernel, so no device value is ever read back.
+ * Each sequence is one frame's source-image grid and its instruction, attended
+ * jointly (Sec. I; Sec. III-A, "Notation and Setup").
  *  layouts: HOST [batch]; pos_thw: device int32 [3, T], T = sum of lengths.
  * Text before an image counts up t=h=w=i; image token k of a (gt,gh,gw) grid
  * after o text tokens gets (o + k/(gh*gw), o + (k/gw)%gh, o + k%gw); text
@@ -223,16 +235,6 @@ int mte_encode_prefixed(mte_encoder *enc, const void *prefix_embeds, const int32
 /* Frees the encoder (synchronises the device first). NULL is a no-op. */
 void mte_encoder_destroy(mte_encoder *enc);
 
-/* Measurement helper (no part of the encoder): enqueues a kernel of `blocks`
- * workgroups of 4 waves in which every wave runs `iters` rounds of eight
- * independent fp16 32x32x16 matrix-core operations (v_mfma_f32_32x32x16_f16,
- * 32768 flops each) with no memory traffic, so that flops / duration is the
- * dense fp16 rate the device sustains under matrix-core load (its clock
- * drops below the 2.4 GHz the published peak assumes). sink: device float
- * [blocks * 256], overwritten. Errors: MTE_E_INVALID (null sink, blocks or
- * iters <= 0), MTE_E_HIP. */
-int mte_probe_mfma(int32_t blocks, int32_t iters, float *sink, hipStream_t stream);
-
 /* OCP fp8 e4m3 quantisation of the rows of a matrix, the weight format of
  * MTE_WEIGHTS_E4M3 (e4m3: sign, 4 exponent bits of bias 7, 3 significand
  * bits; subnormals below 2^-6 in steps of 2^-9; largest finite 448; codes
@@ -254,7 +256,8 @@ int mte_quantize_e4m3_rows(const void *src, int32_t src_dtype, int32_t rows, int
 /* Static description of a status code. Never NULL. */
 const char *mte_status_string(int status);
 
-/* Kernel timing for roofline measurements. While enabled for a kernel class,
+/* Kernel timing for roofline measurements (measurement hooks, no part of the
+ * forward; they add nothing to a call while disabled). While enabled for a kernel class,
  * every launch of that class inside mte_encode / mte_encode_layers is
  * bracketed by HIP events on the launch stream (at most `capacity` pairs
  * are kept; `capacity` is allocated here, not in the encode calls).

@@ -102,7 +102,6 @@ _sig = {
     "mte_timing_read": (C.c_int, [_P, C.POINTER(C.c_int32), C.POINTER(C.c_double)]),
     "mte_timing_disable": (C.c_int, [_P]),
     "mte_quantize_e4m3_rows": (C.c_int, [_P, C.c_int32, C.c_int32, C.c_int32, _P, _P, _P]),
-    "mte_probe_mfma": (C.c_int, [C.c_int32, C.c_int32, _P, _P]),
     "mte_vision_config_validate": (C.c_int, [C.POINTER(mte_vision_config)]),
     "mte_vision_create": (C.c_int, [C.POINTER(mte_vision_config), C.POINTER(mte_vision_weights), _P,
                                     C.POINTER(_P)]),
@@ -271,6 +270,3 @@ def mte_vision_encode_strided(enc: int, pixels: int, n_images: int, height: int,
     return _check(lib.mte_vision_encode_strided(enc, pixels, n_images, height, width, out, image_stride, stream),
                   "mte_vision_encode_strided")
 
-
-def mte_probe_mfma(blocks: int, iters: int, sink: int, stream: int) -> int:
-    return _check(lib.mte_probe_mfma(blocks, iters, sink, stream), "mte_probe_mfma")

@@ -1,8 +1,10 @@
-"""Builds libmte.so (the HIP kernels and the C ABI) for gfx950 with hipcc.
+"""Builds libmte.so (the HIP kernels and the C ABI) for gfx950 with hipcc, and
+libmte_probe.so, the benchmark's matrix-core throughput probe (no part of the
+encoder's ABI).
 
 Usage: python -m paper_2606_05981_amd.build   (or build() from Python)
 
-The library is written next to this file so it travels with the source tree.
+The libraries are written next to this file so they travel with the source tree.
 """
 from __future__ import annotations
 
@@ -15,9 +17,11 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libmte.so")
+PROBE_OUT = os.path.join(HERE, "libmte_probe.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["gemm.hip", "gemm_f8.hip", "attention.hip", "norm_rope.hip", "vision_kernels.hip", "probe.hip",
+SOURCES = ["gemm.hip", "gemm_f8.hip", "attention.hip", "norm_rope.hip", "vision_kernels.hip",
            "api.cpp", "vision.cpp"]
+PROBE_SOURCES = ["probe.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -38,18 +42,24 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD_DIR, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = OUT + ".tmp"
+def _link(objs, out: str) -> None:
+    tmp = out + ".tmp"
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, OUT)
+    os.replace(tmp, out)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    srcs = SOURCES + PROBE_SOURCES
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        objs = list(ex.map(_compile, srcs))
+    _link(objs[:len(SOURCES)], OUT)
+    _link(objs[len(SOURCES):], PROBE_OUT)
     if verbose:
-        print(f"built {OUT}")
+        print(f"built {OUT} and {PROBE_OUT}")
     return OUT
 
 

@@ -52,6 +52,22 @@ int act_shift(double bound) { return std::max(0, exp2_of(bound) - 15); }
 
 }  // namespace
 
+// The activations of one forward: fp32 residual stream h [T, D]; normalised
+// GEMM input xn [T, D]; fp32 qkv [T, (Hq + 2 Hkv) d]; attention output
+// [T, Hq d]; SwiGLU output [T, F]; partial sums of K-split projections (small
+// batches: written by one GEMM, added up by the kernel that consumes its
+// product); the rotary table of the batch [T, d/2] twice.
+struct Work {
+  float *h = nullptr;
+  void *xn = nullptr;
+  float *qkv = nullptr;
+  void *attn = nullptr;
+  void *act = nullptr;
+  float *ws = nullptr;
+  size_t ws_elems = 0;
+  float *rcos = nullptr, *rsin = nullptr;
+};
+
 struct mte_encoder {
   mte_config cfg;
   int device = 0;
@@ -63,16 +79,7 @@ struct mte_encoder {
   int mode = MODE_F32;
   int gmode = MODE_F32;      // of the projection GEMMs: mode, or MODE_F8W for e4m3 weights
   int act_fmt = FMT_F32;
-  float *h = nullptr;        // [max_tokens, D] fp32 residual stream
-  void *xn = nullptr;        // [max_tokens, D] normalised GEMM input
-  float *qkv = nullptr;      // [max_tokens, (Hq + 2 Hkv) d] fp32
-  void *attn = nullptr;      // [max_tokens, Hq d] attention output
-  void *act = nullptr;       // [max_tokens, F] SwiGLU output
-  // Partial sums of K-split projections (small batches): written by one
-  // GEMM, added up by the kernel that consumes its product.
-  float *ws = nullptr;
-  size_t ws_elems = 0;
-  float *rcos = nullptr, *rsin = nullptr;   // [max_tokens, d/2] rotary table of the current batch
+  Work w;                    // workspace for max_tokens, allocated at creation
   // Shared-prefix cache: per layer the prefix's packed q/k/v rows
   // [max_prefix, (Hq + 2 Hkv) d] (k and v are what later sequences read).
   float *pkv = nullptr;
@@ -186,14 +193,14 @@ void mte_encoder_destroy(mte_encoder *e) {
   for (hipEvent_t ev : e->ev) hipEventDestroy(ev);
   hipFree(e->wbuf);
   hipFree(e->gbuf);
-  hipFree(e->h);
-  hipFree(e->xn);
-  hipFree(e->qkv);
-  hipFree(e->attn);
-  hipFree(e->act);
-  hipFree(e->ws);
-  hipFree(e->rcos);
-  hipFree(e->rsin);
+  hipFree(e->w.h);
+  hipFree(e->w.xn);
+  hipFree(e->w.qkv);
+  hipFree(e->w.attn);
+  hipFree(e->w.act);
+  hipFree(e->w.ws);
+  hipFree(e->w.rcos);
+  hipFree(e->w.rsin);
   hipFree(e->pkv);
   hipSetDevice(cur);
   delete e;
@@ -236,18 +243,19 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
   e->mode = c.dtype == MTE_BF16 ? MODE_F16 : MODE_F32;
   e->gmode = w8 ? MODE_F8W : e->mode;
   e->act_fmt = c.dtype == MTE_BF16 ? FMT_F16 : FMT_F32;
-  if (hipMalloc((void **)&e->h, MT * D * sizeof(float)) != hipSuccess ||
-      hipMalloc(&e->xn, MT * D * es) != hipSuccess ||
-      hipMalloc((void **)&e->qkv, MT * nqkv * sizeof(float)) != hipSuccess ||
-      hipMalloc(&e->attn, MT * Hq * d * es) != hipSuccess ||
-      hipMalloc(&e->act, MT * F * es) != hipSuccess)
+  Work &wk = e->w;
+  if (hipMalloc((void **)&wk.h, MT * D * sizeof(float)) != hipSuccess ||
+      hipMalloc(&wk.xn, MT * D * es) != hipSuccess ||
+      hipMalloc((void **)&wk.qkv, MT * nqkv * sizeof(float)) != hipSuccess ||
+      hipMalloc(&wk.attn, MT * Hq * d * es) != hipSuccess ||
+      hipMalloc(&wk.act, MT * F * es) != hipSuccess)
     return fail(MTE_E_OOM);
   // K splits are planned for at most 8 splits of up to 256 rows, or 2 of up to 2048.
-  e->ws_elems = std::max(8 * std::min<size_t>(MT, 256), 2 * std::min<size_t>(MT, 2048)) *
+  wk.ws_elems = std::max(8 * std::min<size_t>(MT, 256), 2 * std::min<size_t>(MT, 2048)) *
                 std::max(std::max(nqkv, 2 * F), D);
-  if (hipMalloc((void **)&e->ws, e->ws_elems * sizeof(float)) != hipSuccess ||
-      hipMalloc((void **)&e->rcos, MT * (d / 2) * sizeof(float)) != hipSuccess ||
-      hipMalloc((void **)&e->rsin, MT * (d / 2) * sizeof(float)) != hipSuccess)
+  if (hipMalloc((void **)&wk.ws, wk.ws_elems * sizeof(float)) != hipSuccess ||
+      hipMalloc((void **)&wk.rcos, MT * (d / 2) * sizeof(float)) != hipSuccess ||
+      hipMalloc((void **)&wk.rsin, MT * (d / 2) * sizeof(float)) != hipSuccess)
     return fail(MTE_E_OOM);
 
   const int sf = in_fmt(c.dtype);
@@ -434,15 +442,15 @@ struct PrefixCtx {
 };
 
 // Runs layers [l0, l1) on the fp32 residual stream `h` (T rows).
-hipError_t run_layers(mte_encoder *e, float *h, const std::vector<int32_t> &cu, int batch, int T, int l0,
+hipError_t run_layers(mte_encoder *e, const Work &wk, float *h, const int32_t *cu, int batch, int T, int l0,
                       int l1, bool first_norm_done, int *pending, hipStream_t s,
                       const PrefixCtx *pre = nullptr) {
   const mte_config &c = e->cfg;
   const int D = c.hidden, d = c.head_dim, Hq = c.n_q_heads, Hkv = c.n_kv_heads, F = c.ffn;
   const int nqkv = (Hq + 2 * Hkv) * d;
   const int mode = e->mode, gm = e->gmode, af = e->act_fmt;
-  float *ws = e->ws;
-  const size_t wn = e->ws_elems;
+  float *ws = wk.ws;
+  const size_t wn = wk.ws_elems;
   // `*pending` counts the partial sums of a K-split residual projection
   // still in ws, to be added into h by the next RMSNorm.
   int np = *pending;
@@ -451,43 +459,43 @@ hipError_t run_layers(mte_encoder *e, float *h, const std::vector<int32_t> &cu, 
   for (int l = l0; l < l1; ++l) {
     const LayerW &W = e->layers[l];
     if (!(l == l0 && first_norm_done))
-      MTE_TRY(launch_rmsnorm(FMT_F32, af, h, np ? h : nullptr, np ? ws : nullptr, np, W.attn_norm, e->xn, T,
+      MTE_TRY(launch_rmsnorm(FMT_F32, af, h, np ? h : nullptr, np ? ws : nullptr, np, W.attn_norm, wk.xn, T,
                              D, c.rms_eps, s));
     int sp = 0;
-    const QkvEpi qe{e->rcos, e->rsin, c.qk_norm ? W.q_norm : nullptr, c.qk_norm ? W.k_norm : nullptr,
+    const QkvEpi qe{wk.rcos, wk.rsin, c.qk_norm ? W.q_norm : nullptr, c.qk_norm ? W.k_norm : nullptr,
                     (Hq + Hkv) * d, Hq * d, d, c.rms_eps};
     {
       Timer t(e, 0, s);
-      MTE_TRY(launch_gemm(gm, EPI_QKV, e->xn, W.w_qkv, e->qkv, T, nqkv, D, nqkv, W.s_qkv, 1.f, ws, wn,
+      MTE_TRY(launch_gemm(gm, EPI_QKV, wk.xn, W.w_qkv, wk.qkv, T, nqkv, D, nqkv, W.s_qkv, 1.f, ws, wn,
                           &sp, &qe, s, W.cs_qkv));
     }
-    if (sp) MTE_TRY(launch_qkv_parts(e->qkv, ws, sp, T, Hq, Hkv, qe, s));
+    if (sp) MTE_TRY(launch_qkv_parts(wk.qkv, ws, sp, T, Hq, Hkv, qe, s));
     {
       Timer t(e, 1, s);
       const size_t lstride = (size_t)e->max_prefix * nqkv;
       if (pre && pre->record)
-        MTE_TRY(hipMemcpyAsync(pre->cache + l * lstride, e->qkv, (size_t)T * nqkv * sizeof(float),
+        MTE_TRY(hipMemcpyAsync(pre->cache + l * lstride, wk.qkv, (size_t)T * nqkv * sizeof(float),
                                hipMemcpyDeviceToDevice, s));
       const bool use = pre && !pre->record;
-      MTE_TRY(launch_attention(mode, e->qkv, use ? pre->cache + l * lstride : nullptr, use ? pre->P : 0,
-                               e->attn, W.o_pre, cu.data(), batch, Hq, Hkv, d, s));
+      MTE_TRY(launch_attention(mode, wk.qkv, use ? pre->cache + l * lstride : nullptr, use ? pre->P : 0,
+                               wk.attn, W.o_pre, cu, batch, Hq, Hkv, d, s));
     }
     {
       Timer t(e, 2, s);
-      MTE_TRY(launch_gemm(gm, EPI_RESID, e->attn, W.w_o, h, T, D, Hq * d, D, W.s_o, 1.f, ws, wn, &np,
+      MTE_TRY(launch_gemm(gm, EPI_RESID, wk.attn, W.w_o, h, T, D, Hq * d, D, W.s_o, 1.f, ws, wn, &np,
                           nullptr, s, W.cs_o));
     }
-    MTE_TRY(launch_rmsnorm(FMT_F32, af, h, np ? h : nullptr, np ? ws : nullptr, np, W.mlp_norm, e->xn, T, D,
+    MTE_TRY(launch_rmsnorm(FMT_F32, af, h, np ? h : nullptr, np ? ws : nullptr, np, W.mlp_norm, wk.xn, T, D,
                            c.rms_eps, s));
     {
       Timer t(e, 3, s);
-      MTE_TRY(launch_gemm(gm, EPI_SWIGLU, e->xn, W.w_gu, e->act, T, 2 * F, D, F, W.s_gu, W.y_pre, ws, wn,
+      MTE_TRY(launch_gemm(gm, EPI_SWIGLU, wk.xn, W.w_gu, wk.act, T, 2 * F, D, F, W.s_gu, W.y_pre, ws, wn,
                           &sp, nullptr, s, W.cs_gu));
     }
-    if (sp) MTE_TRY(launch_swiglu_parts(af, ws, sp, T, F, e->act, W.y_pre, s));
+    if (sp) MTE_TRY(launch_swiglu_parts(af, ws, sp, T, F, wk.act, W.y_pre, s));
     {
       Timer t(e, 4, s);
-      MTE_TRY(launch_gemm(gm, EPI_RESID, e->act, W.w_d, h, T, D, F, D, W.s_d, 1.f, ws, wn, &np, nullptr, s,
+      MTE_TRY(launch_gemm(gm, EPI_RESID, wk.act, W.w_d, h, T, D, F, D, W.s_d, 1.f, ws, wn, &np, nullptr, s,
                           W.cs_d));
     }
   }
@@ -511,39 +519,61 @@ struct DeviceGuard {
 
 extern "C" {
 
-int mte_encode(mte_encoder *e, const void *embeds, const int32_t *pos_thw, const int32_t *seq_lens,
-               int32_t batch, void *out_hidden, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// The whole forward of mte_encode on workspace `wk`, after the host checks;
+// cu: host [batch + 1] sequence offsets.
+hipError_t encode_on(mte_encoder *e, const Work &wk, const void *embeds, const int32_t *pos_thw,
+                     const int32_t *cu, int32_t batch, int32_t T, void *out_hidden, hipStream_t stream) {
+  const mte_config &c = e->cfg;
+  const int out_fmt = in_fmt(c.out_dtype);
+  if (c.n_layers == 0)
+    return launch_rmsnorm(in_fmt(c.dtype), out_fmt, embeds, nullptr, nullptr, 0, e->final_norm, out_hidden, T,
+                          c.hidden, c.rms_eps, stream);
+  hipError_t err = launch_rope_table(pos_thw, T, c.head_dim / 2, e->rope, wk.rcos, wk.rsin, stream);
+  // Layer 0's attention norm also seeds the fp32 residual stream from the embeddings.
+  if (err == hipSuccess)
+    err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, embeds, wk.h, nullptr, 0, e->layers[0].attn_norm, wk.xn,
+                         T, c.hidden, c.rms_eps, stream);
+  int np = 0;
+  if (err == hipSuccess) err = run_layers(e, wk, wk.h, cu, batch, T, 0, c.n_layers, true, &np, stream);
+  if (err == hipSuccess)
+    err = launch_rmsnorm(FMT_F32, out_fmt, wk.h, nullptr, np ? wk.ws : nullptr, np, e->final_norm, out_hidden, T,
+                         c.hidden, c.rms_eps, stream);
+  return err;
+}
+
+// Host checks shared by mte_encode and its variants: pointers, the batch
+// against the configuration, embeds / out_hidden disjoint.
+int check_encode(const mte_encoder *e, const void *embeds, const int32_t *pos_thw, const int32_t *seq_lens,
+                 int32_t batch, const void *out_hidden, int32_t *T) {
   if (!e || !embeds || !pos_thw || !out_hidden) return MTE_E_INVALID;
-  int32_t T = 0;
-  int st = mte_check_batch(&e->cfg, seq_lens, batch, &T);
+  int st = mte_check_batch(&e->cfg, seq_lens, batch, T);
   if (st != MTE_OK) return st;
   const mte_config &c = e->cfg;
-  const size_t in_bytes = (size_t)T * c.hidden * esize(c.dtype);
-  const size_t out_bytes = (size_t)T * c.hidden * esize(c.out_dtype);
+  const size_t in_bytes = (size_t)*T * c.hidden * esize(c.dtype);
+  const size_t out_bytes = (size_t)*T * c.hidden * esize(c.out_dtype);
   const char *ib = (const char *)embeds, *ob = (const char *)out_hidden;
   if (ib < ob + out_bytes && ob < ib + in_bytes) return MTE_E_INVALID;
+  return MTE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mte_encode(mte_encoder *e, const void *embeds, const int32_t *pos_thw, const int32_t *seq_lens,
+               int32_t batch, void *out_hidden, hipStream_t stream) {
+  int32_t T = 0;
+  const int st = check_encode(e, embeds, pos_thw, seq_lens, batch, out_hidden, &T);
+  if (st != MTE_OK) return st;
   std::vector<int32_t> cu(batch + 1, 0);
   for (int i = 0; i < batch; ++i) cu[i + 1] = cu[i] + seq_lens[i];
   DeviceGuard g(e->device);
-  hipError_t err;
-  const int out_fmt = in_fmt(c.out_dtype);
-  if (c.n_layers == 0) {
-    err = launch_rmsnorm(in_fmt(c.dtype), out_fmt, embeds, nullptr, nullptr, 0, e->final_norm,
-                         out_hidden, T, c.hidden, c.rms_eps, stream);
-    return err == hipSuccess ? MTE_OK : MTE_E_HIP;
-  }
-  err = launch_rope_table(pos_thw, T, c.head_dim / 2, e->rope, e->rcos, e->rsin, stream);
-  // Layer 0's attention norm also seeds the fp32 residual stream from the embeddings.
-  if (err == hipSuccess)
-    err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, embeds, e->h, nullptr, 0, e->layers[0].attn_norm,
-                         e->xn, T, c.hidden, c.rms_eps, stream);
-  int np = 0;
-  if (err == hipSuccess)
-    err = run_layers(e, e->h, cu, batch, T, 0, c.n_layers, true, &np, stream);
-  if (err == hipSuccess)
-    err = launch_rmsnorm(FMT_F32, out_fmt, e->h, nullptr, np ? e->ws : nullptr, np, e->final_norm,
-                         out_hidden, T, c.hidden, c.rms_eps, stream);
-  return err == hipSuccess ? MTE_OK : MTE_E_HIP;
+  return encode_on(e, e->w, embeds, pos_thw, cu.data(), batch, T, out_hidden, stream) == hipSuccess ? MTE_OK
+                                                                                                  : MTE_E_HIP;
 }
 
 int mte_encode_layers(mte_encoder *e, const float *h_in, const int32_t *pos_thw,
@@ -563,11 +593,11 @@ int mte_encode_layers(mte_encoder *e, const float *h_in, const int32_t *pos_thw,
   hipError_t err = hipSuccess;
   if (h_out != h_in) err = hipMemcpyAsync(h_out, h_in, bytes, hipMemcpyDeviceToDevice, stream);
   if (err == hipSuccess)
-    err = launch_rope_table(pos_thw, T, e->cfg.head_dim / 2, e->rope, e->rcos, e->rsin, stream);
+    err = launch_rope_table(pos_thw, T, e->cfg.head_dim / 2, e->rope, e->w.rcos, e->w.rsin, stream);
   int np = 0;
   if (err == hipSuccess)
-    err = run_layers(e, h_out, cu, batch, T, layer_begin, layer_end, false, &np, stream);
-  if (err == hipSuccess && np) err = launch_resid_add(h_out, e->ws, np, T, e->cfg.hidden, stream);
+    err = run_layers(e, e->w, h_out, cu.data(), batch, T, layer_begin, layer_end, false, &np, stream);
+  if (err == hipSuccess && np) err = launch_resid_add(h_out, e->w.ws, np, T, e->cfg.hidden, stream);
   return err == hipSuccess ? MTE_OK : MTE_E_HIP;
 }
 
@@ -622,14 +652,15 @@ int mte_encode_prefixed(mte_encoder *e, const void *prefix_embeds, const int32_t
   {
     std::vector<int32_t> cu{0, prefix_len};
     const PrefixCtx rec{e->pkv, prefix_len, true};
-    err = launch_rope_table(prefix_pos, prefix_len, c.head_dim / 2, e->rope, e->rcos, e->rsin, stream);
+    err = launch_rope_table(prefix_pos, prefix_len, c.head_dim / 2, e->rope, e->w.rcos, e->w.rsin, stream);
     if (err == hipSuccess)
-      err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, prefix_embeds, e->h, nullptr, 0, e->layers[0].attn_norm,
-                           e->xn, prefix_len, c.hidden, c.rms_eps, stream);
+      err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, prefix_embeds, e->w.h, nullptr, 0, e->layers[0].attn_norm,
+                           e->w.xn, prefix_len, c.hidden, c.rms_eps, stream);
     int np = 0;
-    if (err == hipSuccess) err = run_layers(e, e->h, cu, 1, prefix_len, 0, c.n_layers, true, &np, stream, &rec);
     if (err == hipSuccess)
-      err = launch_rmsnorm(FMT_F32, out_fmt, e->h, nullptr, np ? e->ws : nullptr, np, e->final_norm, out_prefix,
+      err = run_layers(e, e->w, e->w.h, cu.data(), 1, prefix_len, 0, c.n_layers, true, &np, stream, &rec);
+    if (err == hipSuccess)
+      err = launch_rmsnorm(FMT_F32, out_fmt, e->w.h, nullptr, np ? e->w.ws : nullptr, np, e->final_norm, out_prefix,
                            prefix_len, c.hidden, c.rms_eps, stream);
   }
   // 2. The sequences' own tokens, attending to the cached prefix first.
@@ -637,14 +668,15 @@ int mte_encode_prefixed(mte_encoder *e, const void *prefix_embeds, const int32_t
     std::vector<int32_t> cu(batch + 1, 0);
     for (int i = 0; i < batch; ++i) cu[i + 1] = cu[i] + seq_lens[i];
     const PrefixCtx use{e->pkv, prefix_len, false};
-    err = launch_rope_table(pos_thw, T, c.head_dim / 2, e->rope, e->rcos, e->rsin, stream);
+    err = launch_rope_table(pos_thw, T, c.head_dim / 2, e->rope, e->w.rcos, e->w.rsin, stream);
     if (err == hipSuccess)
-      err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, embeds, e->h, nullptr, 0, e->layers[0].attn_norm, e->xn,
+      err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, embeds, e->w.h, nullptr, 0, e->layers[0].attn_norm, e->w.xn,
                            T, c.hidden, c.rms_eps, stream);
     int np = 0;
-    if (err == hipSuccess) err = run_layers(e, e->h, cu, batch, T, 0, c.n_layers, true, &np, stream, &use);
     if (err == hipSuccess)
-      err = launch_rmsnorm(FMT_F32, out_fmt, e->h, nullptr, np ? e->ws : nullptr, np, e->final_norm, out_hidden,
+      err = run_layers(e, e->w, e->w.h, cu.data(), batch, T, 0, c.n_layers, true, &np, stream, &use);
+    if (err == hipSuccess)
+      err = launch_rmsnorm(FMT_F32, out_fmt, e->w.h, nullptr, np ? e->w.ws : nullptr, np, e->final_norm, out_hidden,
                            T, c.hidden, c.rms_eps, stream);
   }
   return err == hipSuccess ? MTE_OK : MTE_E_HIP;
@@ -688,11 +720,6 @@ int mte_quantize_e4m3_rows(const void *src, int32_t src_dtype, int32_t rows, int
                  hipSuccess
              ? MTE_OK
              : MTE_E_HIP;
-}
-
-int mte_probe_mfma(int32_t blocks, int32_t iters, float *sink, hipStream_t stream) {
-  if (!sink || blocks <= 0 || iters <= 0) return MTE_E_INVALID;
-  return launch_mfma_probe(blocks, iters, sink, stream) == hipSuccess ? MTE_OK : MTE_E_HIP;
 }
 
 int mte_timing_disable(mte_encoder *e) {

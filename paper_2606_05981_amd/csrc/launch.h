@@ -172,11 +172,6 @@ hipError_t launch_layernorm(const float *x, const float *g, const float *b, int 
 hipError_t launch_scatter_rows(const float *src, int dst_fmt, void *dst, int rows, int cols, int group,
                                int group_stride, hipStream_t s);
 
-// Matrix-core throughput probe: `blocks` workgroups of four waves, each wave
-// `iters` rounds of 8 independent 32x32x16 fp16 MFMAs (32768 flops each);
-// sink: float [blocks * 256] (one value per thread, written once).
-hipError_t launch_mfma_probe(int blocks, int iters, float *sink, hipStream_t s);
-
 // OCP e4m3 quantisation of the rows of a [rows, cols] matrix (format src_fmt,
 // FMT_F32 or FMT_BF16): row r gets the scale 2^e_r with e_r the smallest
 // integer such that max_c |src[r, c]| <= 448 * 2^e_r (e_r = 0 for an

@@ -22,6 +22,29 @@ def _stream(stream: Optional[torch.cuda.Stream]) -> int:
     return (stream or torch.cuda.current_stream()).cuda_stream
 
 
+def _check(name: str, t, dtype: torch.dtype, shape, device: torch.device) -> None:
+    """Raises ValueError unless t is a contiguous tensor of `dtype` and exactly `shape` on
+    `device`: the C ABI takes bare addresses, so a host tensor or a short buffer would
+    otherwise reach the kernels."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name}: expected a torch.Tensor")
+    if not t.is_cuda or t.device != device:
+        raise ValueError(f"{name}: expected a tensor on {device}, got one on {t.device}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name}: expected dtype {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: expected a contiguous tensor")
+
+
+def _total(seq_lens: Sequence[int]) -> int:
+    lens = [int(x) for x in seq_lens]
+    if not lens or min(lens) <= 0:
+        raise ValueError("seq_lens must be a non-empty list of positive lengths")
+    return sum(lens)
+
+
 class TextEncoder:
     """Owns one mte_encoder. Weights are copied into the library at creation."""
 
@@ -30,13 +53,19 @@ class TextEncoder:
         self.cfg = cfg
         self.dtype = TORCH_DTYPE[cfg.dtype]
         self.out_dtype = TORCH_DTYPE[cfg.out_dtype]
+        if not final_norm.is_cuda:
+            raise ValueError("final_norm: expected a tensor on the GPU")
+        # the encoder lives on the device its weights are on (mte_encoder_create
+        # allocates on the current device, made that one here)
+        self.device = final_norm.device
         for L in layers:
             for k, t in L.items():
-                if t is not None and (t.dtype != self.dtype or not t.is_cuda or not t.is_contiguous()):
-                    raise ValueError(f"weight {k}: expected contiguous {self.dtype} on the GPU")
+                if t is not None and (t.dtype != self.dtype or t.device != self.device or not t.is_contiguous()):
+                    raise ValueError(f"weight {k}: expected contiguous {self.dtype} on {self.device}")
         ptrs = [{k: (L[k].data_ptr() if L.get(k) is not None else None) for k in WEIGHT_KEYS}
                 for L in layers]
-        self.handle = B.mte_encoder_create(cfg, ptrs, final_norm.data_ptr(), _stream(stream))
+        with torch.cuda.device(self.device):
+            self.handle = B.mte_encoder_create(cfg, ptrs, final_norm.data_ptr(), _stream(stream))
 
     @classmethod
     def from_host(cls, cfg: B.mte_config, layer_arrays, final_norm, device="cuda",
@@ -56,13 +85,13 @@ class TextEncoder:
     def encode(self, embeds: torch.Tensor, pos_thw: torch.Tensor, seq_lens: Sequence[int],
                out: Optional[torch.Tensor] = None,
                stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
-        T = int(sum(seq_lens))
-        if embeds.dtype != self.dtype or embeds.shape != (T, self.cfg.hidden) or not embeds.is_contiguous():
-            raise ValueError("embeds must be a contiguous [T, hidden] tensor of the encoder dtype")
-        if pos_thw.dtype != torch.int32 or pos_thw.shape != (3, T) or not pos_thw.is_contiguous():
-            raise ValueError("pos_thw must be a contiguous int32 [3, T] tensor")
+        T = _total(seq_lens)
+        D = self.cfg.hidden
+        _check("embeds", embeds, self.dtype, (T, D), self.device)
+        _check("pos_thw", pos_thw, torch.int32, (3, T), self.device)
         if out is None:
-            out = torch.empty((T, self.cfg.hidden), dtype=self.out_dtype, device=embeds.device)
+            out = torch.empty((T, D), dtype=self.out_dtype, device=self.device)
+        _check("out", out, self.out_dtype, (T, D), self.device)
         B.mte_encode(self.handle, embeds.data_ptr(), pos_thw.data_ptr(), list(seq_lens),
                      len(seq_lens), out.data_ptr(), _stream(stream))
         return out
@@ -70,11 +99,13 @@ class TextEncoder:
     def encode_layers(self, h_in: torch.Tensor, pos_thw: torch.Tensor, seq_lens: Sequence[int],
                       layer_begin: int, layer_end: int, h_out: Optional[torch.Tensor] = None,
                       stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
-        T = int(sum(seq_lens))
-        if h_in.dtype != torch.float32 or h_in.shape != (T, self.cfg.hidden) or not h_in.is_contiguous():
-            raise ValueError("h_in must be a contiguous float32 [T, hidden] tensor")
+        T = _total(seq_lens)
+        D = self.cfg.hidden
+        _check("h_in", h_in, torch.float32, (T, D), self.device)
+        _check("pos_thw", pos_thw, torch.int32, (3, T), self.device)
         if h_out is None:
             h_out = torch.empty_like(h_in)
+        _check("h_out", h_out, torch.float32, (T, D), self.device)
         B.mte_encode_layers(self.handle, h_in.data_ptr(), pos_thw.data_ptr(), list(seq_lens),
                             len(seq_lens), layer_begin, layer_end, h_out.data_ptr(), _stream(stream))
         return h_out
@@ -86,15 +117,17 @@ class TextEncoder:
                         embeds: torch.Tensor, pos_thw: torch.Tensor, seq_lens: Sequence[int],
                         stream: Optional[torch.cuda.Stream] = None):
         """Sequences sharing a prefix -> (prefix rows [P, D], own rows [T, D])."""
-        P, T = prefix_embeds.shape[0], int(sum(seq_lens))
-        for name, t, rows in (("prefix_embeds", prefix_embeds, P), ("embeds", embeds, T)):
-            if t.dtype != self.dtype or t.shape != (rows, self.cfg.hidden) or not t.is_contiguous():
-                raise ValueError(f"{name} must be a contiguous [rows, hidden] tensor of the encoder dtype")
-        for name, t, rows in (("prefix_pos", prefix_pos, P), ("pos_thw", pos_thw, T)):
-            if t.dtype != torch.int32 or t.shape != (3, rows) or not t.is_contiguous():
-                raise ValueError(f"{name} must be a contiguous int32 [3, rows] tensor")
-        out_p = torch.empty((P, self.cfg.hidden), dtype=self.out_dtype, device=embeds.device)
-        out = torch.empty((T, self.cfg.hidden), dtype=self.out_dtype, device=embeds.device)
+        T = _total(seq_lens)
+        D = self.cfg.hidden
+        if not isinstance(prefix_embeds, torch.Tensor) or prefix_embeds.dim() != 2:
+            raise ValueError("prefix_embeds: expected a 2-D tensor")
+        P = int(prefix_embeds.shape[0])
+        _check("prefix_embeds", prefix_embeds, self.dtype, (P, D), self.device)
+        _check("embeds", embeds, self.dtype, (T, D), self.device)
+        _check("prefix_pos", prefix_pos, torch.int32, (3, P), self.device)
+        _check("pos_thw", pos_thw, torch.int32, (3, T), self.device)
+        out_p = torch.empty((P, D), dtype=self.out_dtype, device=self.device)
+        out = torch.empty((T, D), dtype=self.out_dtype, device=self.device)
         B.mte_encode_prefixed(self.handle, prefix_embeds.data_ptr(), prefix_pos.data_ptr(), P,
                               embeds.data_ptr(), pos_thw.data_ptr(), list(seq_lens), len(seq_lens),
                               out_p.data_ptr(), out.data_ptr(), _stream(stream))

@@ -139,10 +139,15 @@ def test_e4m3_config_valid(B):
     assert ctypes.sizeof(B.mte_config) == 4 * 19   # 19 four-byte fields, as in mte.h
 
 
-def test_probe_rejects_bad_arguments(B):
-    assert B.lib.mte_probe_mfma(0, 10, 4096, None) == -1
-    assert B.lib.mte_probe_mfma(4, 0, 4096, None) == -1
-    assert B.lib.mte_probe_mfma(4, 10, None, None) == -1
+def test_probe_is_not_in_the_encoder_library(B):
+    """The matrix-core probe is a benchmark instrument in its own library, not part of the
+    encoder's ABI; it rejects bad arguments before any HIP call."""
+    assert not hasattr(ctypes.CDLL(B.LIB_PATH), "mte_probe_mfma")
+    probe = ctypes.CDLL(os.path.join(os.path.dirname(B.LIB_PATH), "libmte_probe.so"))
+    probe.mte_probe_mfma.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    assert probe.mte_probe_mfma(0, 10, 4096, None) == -1
+    assert probe.mte_probe_mfma(4, 0, 4096, None) == -1
+    assert probe.mte_probe_mfma(4, 10, None, None) == -1
 
 
 def test_quantize_rejects_bad_arguments(B):

@@ -1,14 +1,15 @@
 """The encoder on a side stream beside other GPU work (the paper's pipelining: the text
 encoder runs on a side stream while the main stream denoises, Alg. 1). A captured encode
-graph replays on a side stream while the main stream runs a GEMM load; its output must be
-bit-identical to a solo run (the kernels' arithmetic does not depend on what else runs)."""
+graph replays on a side stream while the main stream runs a GEMM load; its output must match
+the fp64 oracle (stack bar) and be bit-identical to a solo run (the kernels' arithmetic does
+not depend on what else runs)."""
 import sys
 
 import numpy as np
 import pytest
 
 from synth import workloads as W
-from tests.gpu_common import layout_tuples, make_encoder
+from tests.gpu_common import layout_tuples, make_encoder, oracle_encode, rel_err, seq_slices
 
 pytestmark = pytest.mark.gpu
 
@@ -26,6 +27,7 @@ def test_side_stream_graph_concurrent_with_main_stream_load():
     lens = W.seq_lens(layouts)
     solo = enc.encode(x, pos, lens).clone()
     torch.cuda.synchronize()
+    ref = oracle_encode(dims, emb, layouts)
     out = torch.empty_like(solo)
     main = torch.cuda.current_stream()
     side = torch.cuda.Stream()
@@ -48,5 +50,9 @@ def test_side_stream_graph_concurrent_with_main_stream_load():
         main.wait_stream(side)
         torch.cuda.synchronize()
         print("replay", r, file=sys.stderr, flush=True)
+        got = out.cpu().numpy()
+        for i, sl in enumerate(seq_slices(layouts)):
+            e = rel_err(got[sl], ref[sl])
+            assert e <= 3e-2, (r, i, e)
         assert torch.equal(out, solo), r
     enc.close()

@@ -229,15 +229,68 @@ def test_stack_b1_and_per_layer(torch, full_enc):
         assert e <= TOL_LAYER
 
 
+def _oracle_batch_with_layer_inputs(dims, emb, layouts, keep):
+    ref = oracle_encode(dims, emb, layouts, keep=keep)
+    return ref, dict(O.encode.kept)
+
+
+def _per_layer(torch, enc, dims, layouts, kept, layers, tag):
+    """Each layer l of `layers` run alone on the GPU from the oracle's exact input of that
+    layer (the whole packed batch), against the oracle's output of the same layer."""
+    from paper_2606_05981_amd.encoder import build_positions
+    lens = W.seq_lens(layouts)
+    pos_g = build_positions(layout_tuples(layouts))
+    pos = O.positions(layouts)
+    for l in layers:
+        x = kept[l].astype(np.float32)
+        h = enc.encode_layers(torch.from_numpy(x).cuda(), pos_g, lens, l, l + 1)
+        torch.cuda.synchronize()
+        r = O.layer_forward(x, pos, lens, layer_w(dims, l), dims)
+        e = rel_err(h.cpu().numpy(), r)
+        _say(f"  {tag}: layer {l} (T={sum(lens)}) err {e:.3e}")
+        assert e <= TOL_LAYER, (tag, l, e)
+
+
+@pytest.mark.parametrize("name", ["stack_b16", "stack_b8"])
+def test_stack_batched_every_frame_and_per_layer(torch, full_enc, name):
+    """The benchmark's batched configurations, checked in full: every frame of the packed
+    batch against the oracle run on the same packed batch (stack bar), and layers 0, 13 and
+    27 each run alone from the oracle's exact input at the batch's token count (per-layer
+    bar), so the tile plans and K splits used at that row count meet both bars."""
+    wl = W.workload(name)
+    dims = wl.dims
+    emb = W.embeddings(dims, wl.layouts)
+    _say(name, "T =", wl.tokens)
+    got = _gpu_encode(torch, full_enc, dims, emb, wl.layouts)
+    keep = (0, 13, 27)
+    ref, kept = _oracle_batch_with_layer_inputs(dims, emb, wl.layouts, keep)
+    worst = 0.0
+    for i, sl in enumerate(seq_slices(wl.layouts)):
+        e = rel_err(got[sl], ref[sl])
+        worst = max(worst, e)
+        assert e <= TOL_STACK, (i, e)
+    _say(f"  every frame <= {worst:.3e}; whole batch {rel_err(got, ref):.3e}")
+    assert rel_err(got, ref) <= TOL_STACK
+    _per_layer(torch, full_enc, dims, wl.layouts, kept, keep, name)
+
+
+@pytest.mark.parametrize("name", ["stack_b32_l320", "stack_mixed32"])
+def test_layer0_per_layer_at_large_token_counts(torch, full_enc, name):
+    """Layer 0 from the embeddings at 10240 (32 x 320) and 6759 (32 mixed lengths) rows:
+    the large-M tile plans meet the per-layer bar on the whole packed batch."""
+    wl = W.workload(name)
+    emb = W.embeddings(wl.dims, wl.layouts)
+    _per_layer(torch, full_enc, wl.dims, wl.layouts, {0: emb}, (0,), name)
+
+
 @pytest.mark.parametrize("name,sample", [
-    ("stack_b16", (0, 7, 15)),
-    ("stack_b8", (3,)),
     ("stack_mixed32", "minmax"),
-    ("stack_b32_l320", (31,)),
+    ("stack_b32_l320", (0, 15, 31)),
 ])
 def test_stack_batched_sampled_sequences(torch, full_enc, name, sample):
     """The whole batch runs on the GPU; sampled sequences are re-run alone in the oracle
-    (sequences are independent: the oracle pins packed == alone)."""
+    (sequences are independent: the oracle pins packed == alone). The 28-layer oracle of all
+    6759 or 10240 tokens would take minutes; layer 0 of the whole batch is checked above."""
     wl = W.workload(name)
     dims = wl.dims
     emb = W.embeddings(dims, wl.layouts)
@@ -245,13 +298,97 @@ def test_stack_batched_sampled_sequences(torch, full_enc, name, sample):
     got = _gpu_encode(torch, full_enc, dims, emb, wl.layouts)
     lens = W.seq_lens(wl.layouts)
     if sample == "minmax":
-        sample = (int(np.argmin(lens)), int(np.argmax(lens)))
+        sample = (0, int(np.argmin(lens)), int(np.argmax(lens)), len(lens) - 1)
     sl = seq_slices(wl.layouts)
     for i in sample:
         ref = oracle_encode(dims, emb[sl[i]], [wl.layouts[i]])
         e = rel_err(got[sl[i]], ref)
         _say(f"  seq {i} (L={lens[i]}) err", e)
         assert e <= TOL_STACK
+
+
+# Ragged lengths through the measured bf16 path (fp16 operands, K-split small-M tiles,
+# the bf16 hi/lo attention): 1, 2, the 32-row tile edges, 64/65 and 129.
+RAGGED = (W.SeqLayout(1, 0, 0, 0, 0), W.SeqLayout(0, 1, 1, 1, 1), W.SeqLayout(0, 1, 4, 4, 15),
+          W.SeqLayout(0, 1, 4, 4, 16), W.SeqLayout(0, 1, 4, 4, 17), W.SeqLayout(0, 1, 6, 5, 34),
+          W.SeqLayout(0, 1, 8, 8, 1), W.SeqLayout(0, 1, 8, 8, 65), W.SeqLayout(5, 1, 8, 8, 27))
+DIMS_2L = W.DIMS_FULL.with_(n_layers=2)
+
+
+@pytest.fixture(scope="module")
+def enc_2l(torch):
+    enc = make_encoder(DIMS_2L, max_tokens=4096, max_batch=512, max_seq=4096)
+    yield enc
+    enc.close()
+
+
+def test_bf16_ragged_edges_packed(torch, enc_2l):
+    """One packed batch of lengths 1, 2, 31, 32, 33, 64, 65, 129 and 96 at full width:
+    both layers from the oracle's inputs (per-layer bar) and the two-layer output of every
+    sequence (stack bar)."""
+    dims, layouts = DIMS_2L, RAGGED
+    lens = W.seq_lens(layouts)
+    assert lens == [1, 2, 31, 32, 33, 64, 65, 129, 96]
+    emb = W.embeddings(dims, layouts)
+    got = _gpu_encode(torch, enc_2l, dims, emb, layouts)
+    ref, kept = _oracle_batch_with_layer_inputs(dims, emb, layouts, (0, 1))
+    for i, sl in enumerate(seq_slices(layouts)):
+        e = rel_err(got[sl], ref[sl])
+        _say(f"  L={lens[i]}: {e:.3e}")
+        assert e <= TOL_STACK, (lens[i], e)
+    _per_layer(torch, enc_2l, dims, layouts, kept, (0, 1), "ragged")
+
+
+@pytest.mark.parametrize("idx", [0, 1, 4, 6, 7, 8])
+def test_bf16_single_sequence_lengths(torch, enc_2l, idx):
+    """One sequence per call at lengths 1, 2, 33, 65, 129 and 96: the batch-of-one row
+    counts, whose plans take the 4- and 8-way K splits, at both bars."""
+    dims, layouts = DIMS_2L, (RAGGED[idx],)
+    emb = W.embeddings(dims, layouts)
+    got = _gpu_encode(torch, enc_2l, dims, emb, layouts)
+    ref, kept = _oracle_batch_with_layer_inputs(dims, emb, layouts, (0, 1))
+    e = rel_err(got, ref)
+    _say(f"  alone L={W.seq_lens(layouts)[0]}: {e:.3e}")
+    assert e <= TOL_STACK
+    _per_layer(torch, enc_2l, dims, layouts, kept, (0, 1), f"alone L={W.seq_lens(layouts)[0]}")
+
+
+def test_bf16_many_short_sequences(torch, enc_2l):
+    """300 sequences of 1..8 tokens at full width: past the 256-sequence attention launch
+    chunk and the 128-sequence position chunk; every sequence against the oracle."""
+    dims = DIMS_2L
+    layouts = tuple(W.SeqLayout(1 + i % 3, 1 if i % 4 else 0, 1 if i % 4 else 0, 1 + i % 2 if i % 4 else 0,
+                                i % 4) for i in range(300))
+    lens = W.seq_lens(layouts)
+    assert len(lens) > 256
+    emb = W.embeddings(dims, layouts)
+    got = _gpu_encode(torch, enc_2l, dims, emb, layouts)
+    ref, kept = _oracle_batch_with_layer_inputs(dims, emb, layouts, (0,))
+    sl = seq_slices(layouts)
+    worst = max(rel_err(got[s], ref[s]) for s in sl)
+    _say(f"  300 short sequences, worst {worst:.3e}")
+    assert worst <= TOL_STACK
+    _per_layer(torch, enc_2l, dims, layouts, kept, (0,), "300 short")
+
+
+def test_no_leak_between_sequences_bit_exact(torch, enc_2l):
+    """Replacing one sequence's embeddings by other values of the same length leaves every
+    other sequence's output bit-identical: the launch plan depends on the token count only,
+    and no step mixes rows of different sequences."""
+    dims = DIMS_2L
+    layouts = (W.FRAME_96, W.SeqLayout(0, 1, 10, 9, 41), W.SeqLayout(0, 1, 8, 8, 1), W.FRAME_96)
+    emb = W.embeddings(dims, layouts)
+    base = _gpu_encode(torch, enc_2l, dims, emb, layouts)
+    sl = seq_slices(layouts)
+    for i in range(len(layouts)):
+        alt = emb.copy()
+        alt[sl[i]] = W.round_to_bf16(np.random.default_rng(90 + i).standard_normal(
+            alt[sl[i]].shape).astype(np.float32) * np.float32(0.02))
+        out = _gpu_encode(torch, enc_2l, dims, alt, layouts)
+        assert not np.array_equal(out[sl[i]], base[sl[i]])
+        for j in range(len(layouts)):
+            if j != i:
+                np.testing.assert_array_equal(out[sl[j]], base[sl[j]], err_msg=f"{i} -> {j}")
 
 
 def test_stack_wide_range_inputs(torch, full_enc):
