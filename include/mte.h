@@ -169,6 +169,32 @@ int mte_encode(mte_encoder *enc, const void *embeds, const int32_t *pos_thw,
                const int32_t *seq_lens, int32_t batch, void *out_hidden,
                hipStream_t stream);
 
+/* mte_encode for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same forward, arguments and errors as mte_encode, with the activations
+ * held in the library's static device array of MTE_STATIC_SCRATCH_BYTES
+ * (one per GPU, reserved when the library's device code is loaded on that
+ * GPU and kept until the process ends) instead of the encoder's workspace.
+ * It calls no hipMalloc / hipFree or other allocating routine and only
+ * enqueues work on `stream`.
+ * Capacity: at most MTE_STATIC_MAX_BATCH sequences, and the activations of
+ * T = sum(seq_lens) tokens, T * (4 D + 4 (Hq + 2 Hkv) d + 4 d + e (D + Hq d
+ * + F)) bytes with e = 2 for MTE_BF16 (4 for MTE_F32) plus 256-byte
+ * alignment of seven regions, must fit MTE_STATIC_SCRATCH_BYTES (about 736
+ * tokens of the 2048-wide bf16 model); the rest of the array holds K-split
+ * partial sums. Beyond that: MTE_E_CAPACITY, checked before any HIP call.
+ * The usual mte_encode limits (max_batch, max_seq, max_tokens) apply too.
+ * Every call on one GPU shares that GPU's array, whichever encoder it
+ * serves: calls that overlap in time on one GPU race. No part of the array
+ * needs to start at zero (every value is written before it is read).
+ * Results equal mte_encode's bit for bit whenever the batch's K-split
+ * partial sums fit the array (then both take the same launch plan). */
+#define MTE_STATIC_SCRATCH_BYTES (32u << 20)
+#define MTE_STATIC_MAX_BATCH 1024
+int mte_encode_static(mte_encoder *enc, const void *embeds, const int32_t *pos_thw,
+                      const int32_t *seq_lens, int32_t batch, void *out_hidden,
+                      hipStream_t stream);
+
 /* Runs decoder layers [layer_begin, layer_end) on an fp32 residual stream
  * without the final norm: h_out = layers(h_in). h_in / h_out: device float
  * [T, D] (they may be the same buffer). Other arguments as mte_encode.

@@ -90,6 +90,7 @@ _sig = {
     "mte_encoder_create": (C.c_int, [C.POINTER(mte_config), C.POINTER(mte_weights), _P,
                                      C.POINTER(_P)]),
     "mte_encode": (C.c_int, [_P, _P, _P, C.POINTER(C.c_int32), C.c_int32, _P, _P]),
+    "mte_encode_static": (C.c_int, [_P, _P, _P, C.POINTER(C.c_int32), C.c_int32, _P, _P]),
     "mte_encode_layers": (C.c_int, [_P, _P, _P, C.POINTER(C.c_int32), C.c_int32, C.c_int32,
                                     C.c_int32, _P, _P]),
     "mte_build_positions": (C.c_int, [C.POINTER(mte_seq_layout), C.c_int32, _P, _P]),
@@ -173,6 +174,12 @@ def mte_encode(enc: int, embeds: int, pos_thw: int, seq_lens: Sequence[int], bat
                out_hidden: int, stream: int) -> int:
     return _check(lib.mte_encode(enc, embeds, pos_thw, _i32(seq_lens), batch, out_hidden, stream),
                   "mte_encode")
+
+
+def mte_encode_static(enc: int, embeds: int, pos_thw: int, seq_lens: Sequence[int], batch: int,
+                      out_hidden: int, stream: int) -> int:
+    return _check(lib.mte_encode_static(enc, embeds, pos_thw, _i32(seq_lens), batch, out_hidden, stream),
+                  "mte_encode_static")
 
 
 def mte_encode_layers(enc: int, h_in: int, pos_thw: int, seq_lens: Sequence[int], batch: int,

@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -49,6 +50,34 @@ int weight_shift(double maxabs) { return maxabs > 0.0 ? 15 - exp2_of(maxabs) : 0
 // Activation pre-scale exponent (>= 0, applied as 2^-k): values bounded by
 // `bound` stay within 2^15 after scaling, well inside fp16's range.
 int act_shift(double bound) { return std::max(0, exp2_of(bound) - 15); }
+
+}  // namespace
+
+// Workspace of mte_encode_static: a file-scope device array, one copy per
+// GPU, never allocated or freed by the library. In host code `scratch` names
+// a host-side stand-in, not device memory: its device address on each GPU
+// comes from hipGetSymbolAddress (made with that GPU current) and only that
+// address is handed to kernels.
+__device__ __align__(256) unsigned char scratch[MTE_STATIC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on `dev` (the current device), resolved once per
+// device; nullptr if the runtime cannot provide it.
+void *scratch_on(int dev) {
+  if (dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) == hipSuccess) g_scratch_ptr[dev] = p;
+    else (void)hipGetLastError();   // clear the sticky error; the caller reports MTE_E_HIP
+  }
+  return g_scratch_ptr[dev];
+}
 
 }  // namespace
 
@@ -223,6 +252,8 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
   if (!e) return MTE_E_OOM;
   e->cfg = c;
   if (hipGetDevice(&e->device) != hipSuccess) { delete e; return MTE_E_HIP; }
+  // set-up of mte_encode_static on this device (a failure here is reported by that call)
+  scratch_on(e->device);
 
   const size_t es = esize(c.dtype);              // activations: fp16 or fp32
   const bool w8 = c.weight_format == MTE_WEIGHTS_E4M3;
@@ -574,6 +605,50 @@ int mte_encode(mte_encoder *e, const void *embeds, const int32_t *pos_thw, const
   DeviceGuard g(e->device);
   return encode_on(e, e->w, embeds, pos_thw, cu.data(), batch, T, out_hidden, stream) == hipSuccess ? MTE_OK
                                                                                                   : MTE_E_HIP;
+}
+
+int mte_encode_static(mte_encoder *e, const void *embeds, const int32_t *pos_thw, const int32_t *seq_lens,
+                      int32_t batch, void *out_hidden, hipStream_t stream) {
+  int32_t T = 0;
+  const int st = check_encode(e, embeds, pos_thw, seq_lens, batch, out_hidden, &T);
+  if (st != MTE_OK) return st;
+  if (batch > MTE_STATIC_MAX_BATCH) return MTE_E_CAPACITY;
+  const mte_config &c = e->cfg;
+  const size_t es = esize(c.dtype), D = c.hidden, F = c.ffn, d = c.head_dim, Hq = c.n_q_heads;
+  const size_t nqkv = (Hq + 2 * (size_t)c.n_kv_heads) * d;
+  auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
+  // the activations of T tokens, each region 256-byte aligned; the rest holds K-split partials
+  const size_t sizes[7] = {T * D * 4, T * D * es, T * nqkv * 4, T * Hq * d * es, T * F * es,
+                           T * (d / 2) * 4, T * (d / 2) * 4};
+  size_t used = 0;
+  for (size_t b : sizes) used += up(b);
+  if (used > (size_t)MTE_STATIC_SCRATCH_BYTES) return MTE_E_CAPACITY;
+  int32_t cu[MTE_STATIC_MAX_BATCH + 1];
+  cu[0] = 0;
+  for (int i = 0; i < batch; ++i) cu[i + 1] = cu[i] + seq_lens[i];
+  DeviceGuard g(e->device);
+  unsigned char *base = (unsigned char *)scratch_on(e->device);
+  if (!base) return MTE_E_HIP;
+  unsigned char *ptr[7];
+  size_t off = 0;
+  for (int i = 0; i < 7; ++i) {
+    ptr[i] = base + off;
+    off += up(sizes[i]);
+  }
+  Work wk;
+  wk.h = (float *)ptr[0];
+  wk.xn = ptr[1];
+  wk.qkv = (float *)ptr[2];
+  wk.attn = ptr[3];
+  wk.act = ptr[4];
+  wk.rcos = (float *)ptr[5];
+  wk.rsin = (float *)ptr[6];
+  // the encoder's own bound as well, so that a batch gets the same launch plan
+  // (hence bit-identical results) as through mte_encode whenever its partial
+  // sums fit here
+  wk.ws = (float *)(base + off);
+  wk.ws_elems = std::min(((size_t)MTE_STATIC_SCRATCH_BYTES - off) / sizeof(float), e->w.ws_elems);
+  return encode_on(e, wk, embeds, pos_thw, cu, batch, T, out_hidden, stream) == hipSuccess ? MTE_OK : MTE_E_HIP;
 }
 
 int mte_encode_layers(mte_encoder *e, const float *h_in, const int32_t *pos_thw,
