@@ -32,6 +32,10 @@ struct LayerW {
   // activation's power-of-two pre-scales); the attention output and the
   // SwiGLU output are pre-scaled by o_pre / y_pre before rounding to fp16.
   float s_qkv = 1.f, s_o = 1.f, s_gu = 1.f, s_d = 1.f, o_pre = 1.f, y_pre = 1.f;
+  // fp16 attention operands: q and k are stored times q_pre / k_pre (v times
+  // o_pre); att_sc = log2(e) / sqrt(d) / (q_pre k_pre) turns their products
+  // into scores in log2 units.
+  float q_pre = 1.f, k_pre = 1.f, att_sc = 1.f;
 };
 
 size_t esize(int dtype) { return dtype == MTE_BF16 ? 2 : 4; }
@@ -50,6 +54,19 @@ int weight_shift(double maxabs) { return maxabs > 0.0 ? 15 - exp2_of(maxabs) : 0
 // Activation pre-scale exponent (>= 0, applied as 2^-k): values bounded by
 // `bound` stay within 2^15 after scaling, well inside fp16's range.
 int act_shift(double bound) { return std::max(0, exp2_of(bound) - 15); }
+
+// Bytes of the fp16 attention operands of T tokens (fp16 modes): q/k rows
+// [T, (Hq + Hkv) d] (256-byte aligned), then V^T tiles [ceil(T / 32)][Hkv][d][32].
+size_t qk_bytes(const mte_config &c, size_t T) {
+  return ((T * (c.n_q_heads + c.n_kv_heads) * c.head_dim * 2) + 255) & ~(size_t)255;
+}
+size_t vt_bytes(const mte_config &c, size_t T) { return (T + 31) / 32 * 32 * c.n_kv_heads * c.head_dim * 2; }
+// Bytes of the qkv region: fp32 rows [T, (Hq + 2 Hkv) d] (fp32 mode; also the
+// bound used for the region in every mode), or the fp16 attention operands.
+size_t qkv_bytes(const mte_config &c, size_t T) {
+  const size_t rows = T * (c.n_q_heads + 2 * (size_t)c.n_kv_heads) * c.head_dim * 4;
+  return c.dtype == MTE_F32 ? rows : std::max(rows, qk_bytes(c, T) + vt_bytes(c, T));
+}
 
 }  // namespace
 
@@ -82,7 +99,8 @@ void *scratch_on(int dev) {
 }  // namespace
 
 // The activations of one forward: fp32 residual stream h [T, D]; normalised
-// GEMM input xn [T, D]; fp32 qkv [T, (Hq + 2 Hkv) d]; attention output
+// GEMM input xn [T, D]; fp32 qkv [T, (Hq + 2 Hkv) d] (fp16 modes: the fp16
+// q/k rows and V^T tiles the attention reads, in the same region); attention output
 // [T, Hq d]; SwiGLU output [T, F]; partial sums of K-split projections (small
 // batches: written by one GEMM, added up by the kernel that consumes its
 // product); the rotary table of the batch [T, d/2] twice.
@@ -90,6 +108,7 @@ struct Work {
   float *h = nullptr;
   void *xn = nullptr;
   float *qkv = nullptr;
+  f16 *qk = nullptr, *vt = nullptr;   // fp16 modes: the attention operands, inside the qkv region
   void *attn = nullptr;
   void *act = nullptr;
   float *ws = nullptr;
@@ -111,7 +130,8 @@ struct mte_encoder {
   Work w;                    // workspace for max_tokens, allocated at creation
   // Shared-prefix cache: per layer the prefix's packed q/k/v rows
   // [max_prefix, (Hq + 2 Hkv) d] (k and v are what later sequences read).
-  float *pkv = nullptr;
+  char *pkv = nullptr;
+  size_t pkv_stride = 0;     // bytes per layer
   int max_prefix = 0;
   RopeParams rope;
   // kernel timing
@@ -277,11 +297,13 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
   Work &wk = e->w;
   if (hipMalloc((void **)&wk.h, MT * D * sizeof(float)) != hipSuccess ||
       hipMalloc(&wk.xn, MT * D * es) != hipSuccess ||
-      hipMalloc((void **)&wk.qkv, MT * nqkv * sizeof(float)) != hipSuccess ||
+      hipMalloc((void **)&wk.qkv, qkv_bytes(c, MT)) != hipSuccess ||
       hipMalloc(&wk.attn, MT * Hq * d * es) != hipSuccess ||
       hipMalloc(&wk.act, MT * F * es) != hipSuccess)
     return fail(MTE_E_OOM);
   // K splits are planned for at most 8 splits of up to 256 rows, or 2 of up to 2048.
+  wk.qk = (f16 *)wk.qkv;
+  wk.vt = (f16 *)((char *)wk.qkv + qk_bytes(c, MT));
   wk.ws_elems = std::max(8 * std::min<size_t>(MT, 256), 2 * std::min<size_t>(MT, 2048)) *
                 std::max(std::max(nqkv, 2 * F), D);
   if (hipMalloc((void **)&wk.ws, wk.ws_elems * sizeof(float)) != hipSuccess ||
@@ -296,7 +318,7 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
   // Range analysis (bf16 weights only): per layer the max |w| of each
   // projection, the largest row norms of Wv, Wgate and Wup, and the largest
   // norm gains, from which the power-of-two pre-scales follow.
-  enum { S_Q, S_K, S_V, S_O, S_G, S_U, S_D, S_AN, S_MN, S_N };
+  enum { S_Q, S_K, S_V, S_O, S_G, S_U, S_D, S_AN, S_MN, S_QN, S_KN, S_N };
   std::vector<float> st_h;
   if (f16 && c.n_layers > 0) {
     float *st = nullptr;
@@ -309,9 +331,9 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
       const struct { const void *p; size_t rows, cols; } m[S_N] = {
           {L.w_q, Hq * d, D}, {L.w_k, Hkv * d, D}, {L.w_v, Hkv * d, D}, {L.w_o, D, Hq * d},
           {L.w_gate, F, D},   {L.w_up, F, D},      {L.w_down, D, F},    {L.attn_norm, 1, D},
-          {L.mlp_norm, 1, D}};
+          {L.mlp_norm, 1, D}, {L.q_norm, 1, d},    {L.k_norm, 1, d}};
       for (int k = 0; k < S_N && he == hipSuccess; ++k)
-        he = launch_matrix_stats(sf, m[k].p, (int)m[k].rows, (int)m[k].cols, sl + 2 * k, stream);
+        if (m[k].p) he = launch_matrix_stats(sf, m[k].p, (int)m[k].rows, (int)m[k].cols, sl + 2 * k, stream);
     }
     st_h.resize(nst);
     if (he == hipSuccess) he = hipMemcpyAsync(st_h.data(), st, nst * sizeof(float), hipMemcpyDeviceToHost, stream);
@@ -337,7 +359,7 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
     o.mlp_norm = gb + D;
     o.q_norm = gb + 2 * D;
     o.k_norm = gb + 2 * D + d;
-    int w_qkv = 0, w_o = 0, w_gu = 0, w_d = 0, ka = 0, km = 0, ko = 0, ky = 0;
+    int w_qkv = 0, w_o = 0, w_gu = 0, w_d = 0, ka = 0, km = 0, ko = 0, ky = 0, kq = 0, kk = 0;
     if (f16) {
       const float *sl = &st_h[(size_t)l * S_N * 2];
       auto mx = [&](int k) { return (double)sl[2 * k]; };
@@ -359,6 +381,13 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
       km = act_shift(bm);
       ko = act_shift(ba * rn(S_V) * q8);
       ky = act_shift((bm * rn(S_G) * q8) * (bm * rn(S_U) * q8));
+      // fp16 q and k of the attention: with QK-norm every element of a head
+      // is at most its norm, sqrt(d) max|g_q| (resp. g_k), and the rotation
+      // keeps each pair's norm; without it, the row norms of Wq / Wk times the
+      // norm output's bound, times sqrt(2) for the rotation.
+      const double sd = std::sqrt((double)d);
+      kq = act_shift(c.qk_norm ? sd * mx(S_QN) : std::sqrt(2.0) * ba * rn(S_Q) * q8);
+      kk = act_shift(c.qk_norm ? sd * mx(S_KN) : std::sqrt(2.0) * ba * rn(S_K) * q8);
       if (w8) w_qkv = w_o = w_gu = w_d = 0;    // codes are not pre-scaled; the row scales apply
     }
     o.s_qkv = std::ldexp(1.f, ka - w_qkv);
@@ -367,6 +396,9 @@ int mte_encoder_create(const mte_config *cfg, const mte_weights *w, hipStream_t 
     o.s_d = std::ldexp(1.f, ky - w_d);
     o.o_pre = std::ldexp(1.f, -ko);
     o.y_pre = std::ldexp(1.f, -ky);
+    o.q_pre = std::ldexp(1.f, -kq);
+    o.k_pre = std::ldexp(1.f, -kk);
+    o.att_sc = (float)(1.4426950408889634 / std::sqrt((double)d) * std::ldexp(1.0, kq + kk));
     const int df = f16 ? FMT_F16 : FMT_F32;
     const size_t bq = Hq * d * D * es, bk = Hkv * d * D * es;
     const float sq = std::ldexp(1.f, w_qkv);
@@ -467,7 +499,8 @@ struct Timer {
 // attention reads the cache's first P rows as keys / values before each
 // sequence's own.
 struct PrefixCtx {
-  float *cache;      // [n_layers][max_prefix][(Hq + 2 Hkv) d]
+  char *cache;       // [n_layers][layer stride]: one layer's q/k/v of the prefix
+  size_t stride;     // bytes per layer
   int P;
   bool record;
 };
@@ -493,8 +526,17 @@ hipError_t run_layers(mte_encoder *e, const Work &wk, float *h, const int32_t *c
       MTE_TRY(launch_rmsnorm(FMT_F32, af, h, np ? h : nullptr, np ? ws : nullptr, np, W.attn_norm, wk.xn, T,
                              D, c.rms_eps, s));
     int sp = 0;
-    const QkvEpi qe{wk.rcos, wk.rsin, c.qk_norm ? W.q_norm : nullptr, c.qk_norm ? W.k_norm : nullptr,
-                    (Hq + Hkv) * d, Hq * d, d, c.rms_eps};
+    QkvEpi qe{wk.rcos, wk.rsin, c.qk_norm ? W.q_norm : nullptr, c.qk_norm ? W.k_norm : nullptr,
+              (Hq + Hkv) * d, Hq * d, d, c.rms_eps};
+    const bool half = mode != MODE_F32;   // fp16 attention operands
+    if (half) {
+      qe.qk = wk.qk;
+      qe.vt = wk.vt;
+      qe.q_pre = W.q_pre;
+      qe.k_pre = W.k_pre;
+      qe.v_pre = W.o_pre;
+      qe.hkv = Hkv;
+    }
     {
       Timer t(e, 0, s);
       MTE_TRY(launch_gemm(gm, EPI_QKV, wk.xn, W.w_qkv, wk.qkv, T, nqkv, D, nqkv, W.s_qkv, 1.f, ws, wn,
@@ -503,13 +545,26 @@ hipError_t run_layers(mte_encoder *e, const Work &wk, float *h, const int32_t *c
     if (sp) MTE_TRY(launch_qkv_parts(wk.qkv, ws, sp, T, Hq, Hkv, qe, s));
     {
       Timer t(e, 1, s);
-      const size_t lstride = (size_t)e->max_prefix * nqkv;
-      if (pre && pre->record)
-        MTE_TRY(hipMemcpyAsync(pre->cache + l * lstride, wk.qkv, (size_t)T * nqkv * sizeof(float),
-                               hipMemcpyDeviceToDevice, s));
+      // the prefix cache of layer l: fp32 rows [max_prefix, nqkv], or the fp16
+      // q/k rows [max_prefix, (Hq + Hkv) d] followed by V^T tiles
+      char *lc = pre ? pre->cache + l * pre->stride : nullptr;
+      const size_t cq = qk_bytes(c, e->max_prefix);
+      if (pre && pre->record) {
+        if (half) {
+          MTE_TRY(hipMemcpyAsync(lc, wk.qk, (size_t)T * (Hq + Hkv) * d * sizeof(f16), hipMemcpyDeviceToDevice, s));
+          MTE_TRY(hipMemcpyAsync(lc + cq, wk.vt, vt_bytes(c, T), hipMemcpyDeviceToDevice, s));
+        } else {
+          MTE_TRY(hipMemcpyAsync(lc, wk.qkv, (size_t)T * nqkv * sizeof(float), hipMemcpyDeviceToDevice, s));
+        }
+      }
       const bool use = pre && !pre->record;
-      MTE_TRY(launch_attention(mode, wk.qkv, use ? pre->cache + l * lstride : nullptr, use ? pre->P : 0,
-                               wk.attn, W.o_pre, cu, batch, Hq, Hkv, d, s));
+      if (half)
+        MTE_TRY(launch_attention_h(wk.qk, wk.vt, use ? (const f16 *)lc : nullptr,
+                                   use ? (const f16 *)(lc + cq) : nullptr, use ? pre->P : 0, (f16 *)wk.attn,
+                                   W.att_sc, cu, batch, T, Hq, Hkv, d, 1, s));
+      else
+        MTE_TRY(launch_attention(mode, wk.qkv, use ? (const float *)lc : nullptr, use ? pre->P : 0, wk.attn,
+                                 W.o_pre, cu, batch, Hq, Hkv, d, s));
     }
     {
       Timer t(e, 2, s);
@@ -618,7 +673,7 @@ int mte_encode_static(mte_encoder *e, const void *embeds, const int32_t *pos_thw
   const size_t nqkv = (Hq + 2 * (size_t)c.n_kv_heads) * d;
   auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
   // the activations of T tokens, each region 256-byte aligned; the rest holds K-split partials
-  const size_t sizes[7] = {T * D * 4, T * D * es, T * nqkv * 4, T * Hq * d * es, T * F * es,
+  const size_t sizes[7] = {T * D * 4, T * D * es, qkv_bytes(c, T), T * Hq * d * es, T * F * es,
                            T * (d / 2) * 4, T * (d / 2) * 4};
   size_t used = 0;
   for (size_t b : sizes) used += up(b);
@@ -639,6 +694,8 @@ int mte_encode_static(mte_encoder *e, const void *embeds, const int32_t *pos_thw
   wk.h = (float *)ptr[0];
   wk.xn = ptr[1];
   wk.qkv = (float *)ptr[2];
+  wk.qk = (f16 *)ptr[2];
+  wk.vt = (f16 *)(ptr[2] + qk_bytes(c, T));
   wk.attn = ptr[3];
   wk.act = ptr[4];
   wk.rcos = (float *)ptr[5];
@@ -687,8 +744,10 @@ int mte_encoder_reserve_prefix(mte_encoder *e, int32_t max_prefix) {
   hipFree(e->pkv);
   e->pkv = nullptr;
   e->max_prefix = 0;
-  if (hipMalloc((void **)&e->pkv, (size_t)c.n_layers * max_prefix * nqkv * sizeof(float)) != hipSuccess)
-    return MTE_E_OOM;
+  const size_t stride = c.dtype == MTE_F32 ? (size_t)max_prefix * nqkv * sizeof(float)
+                                           : qk_bytes(c, max_prefix) + vt_bytes(c, max_prefix);
+  if (hipMalloc((void **)&e->pkv, (size_t)c.n_layers * stride) != hipSuccess) return MTE_E_OOM;
+  e->pkv_stride = stride;
   e->max_prefix = max_prefix;
   return MTE_OK;
 }
@@ -726,7 +785,7 @@ int mte_encode_prefixed(mte_encoder *e, const void *prefix_embeds, const int32_t
   //    layer's q/k/v rows.
   {
     std::vector<int32_t> cu{0, prefix_len};
-    const PrefixCtx rec{e->pkv, prefix_len, true};
+    const PrefixCtx rec{e->pkv, e->pkv_stride, prefix_len, true};
     err = launch_rope_table(prefix_pos, prefix_len, c.head_dim / 2, e->rope, e->w.rcos, e->w.rsin, stream);
     if (err == hipSuccess)
       err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, prefix_embeds, e->w.h, nullptr, 0, e->layers[0].attn_norm,
@@ -742,7 +801,7 @@ int mte_encode_prefixed(mte_encoder *e, const void *prefix_embeds, const int32_t
   if (err == hipSuccess) {
     std::vector<int32_t> cu(batch + 1, 0);
     for (int i = 0; i < batch; ++i) cu[i + 1] = cu[i] + seq_lens[i];
-    const PrefixCtx use{e->pkv, prefix_len, false};
+    const PrefixCtx use{e->pkv, e->pkv_stride, prefix_len, false};
     err = launch_rope_table(pos_thw, T, c.head_dim / 2, e->rope, e->w.rcos, e->w.rsin, stream);
     if (err == hipSuccess)
       err = launch_rmsnorm(in_fmt(c.dtype), e->act_fmt, embeds, e->w.h, nullptr, 0, e->layers[0].attn_norm, e->w.xn,

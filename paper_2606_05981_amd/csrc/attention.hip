@@ -5,6 +5,12 @@
 // with k, v taken from kv head h / (Hq / Hkv) and j ranging over the same
 // sequence only (q and k arrive normalised and rotated).
 //
+// Two kernels. k_attn_h (at the end of this file) is the decoder's with bf16
+// storage: fp16 operands that the QKV projection already wrote in the
+// matrix-core layout, one wave per work item and no LDS. k_attn below serves
+// fp32 storage (fp32 operands) and the vision tower (fp32 q/k/v split into
+// bf16 hi + lo for the scores):
+//
 // One workgroup (4 waves) serves one kv head, one tile of query rows of one
 // sequence and the query heads of that kv head assigned to it; every wave
 // owns 32 query rows of one query head. Key/value tiles of 32 tokens are
@@ -536,6 +542,269 @@ hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int
       if (d == 128) { MTE_ATTN(MODE_F32, 128, false) } else { MTE_ATTN(MODE_F32, 64, false) }
     }
 #undef MTE_ATTN
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// ------------------------------------------------------------------
+// Attention on fp16 operands in the matrix-core layout (launch_attention_h).
+//
+// Every wave owns one (sequence, query head, block of 32 queries) and works
+// alone: no LDS, no barriers. Its q fragments stay in registers; per key
+// tile of 32 tokens it reads the k fragments straight from the k rows (each
+// lane one 16-byte piece of one key row) and the V^T fragments from the
+// pre-arranged tiles (one 16-byte piece per lane and output block), forms
+// S^T = K Q^T on eight fp16 MFMAs (lane l owns query l % 32 and 16 of the
+// keys), the online softmax in fp32 with one cross-lane exchange, and
+// O^T += V^T P^T on two fp16 MFMAs per 32 output columns. Key tiles are the
+// batch's global 32-token tiles, so a sequence that starts inside a tile
+// masks the tile's leading keys; keys of other sequences and zero-padded
+// rows past the batch enter with probability exactly 0. The next tile's k
+// fragments are loaded while the current tile's probabilities are formed.
+// With KS > 1 (few work items, e.g. one frame) a workgroup of KS waves
+// serves one item: wave w takes key tiles w, w + KS, ..., and wave 0 merges
+// the partial softmax states (running max, sum, O) of the others from LDS,
+// so an item's chain of dependent tile steps is KS times shorter.
+struct AttnHArgs {
+  const f16 *qk;      // [T, ldq]
+  const f16 *vt;      // [ceil(T / 32)][Hkv][HD][32]
+  const f16 *pqk;     // shared prefix rows [P, ldq], or null
+  const f16 *pvt;     // shared prefix V^T tiles [ceil(P / 32)][Hkv][HD][32]
+  f16 *o;             // [T, Hq HD]
+  float sc;           // log2(e) / sqrt(d), times the inverse q and k pre-scales
+  int ldq;            // halfs per qk row, (Hq + Hkv) HD
+  int T, P;
+  int Hq, Hkv, rep;
+  int n_seq, causal;
+  int n_items;        // waves of work in this launch
+  int cu[kMaxSeqPerLaunch + 1];    // absolute token offsets
+  int blk0[kMaxSeqPerLaunch + 1];  // first 32-query block of each sequence
+};
+
+template <int HD, int WPB, int KS>
+__global__ __launch_bounds__(64 * WPB * KS) void k_attn_h(AttnHArgs a) {
+  static_assert(KS == 1 || WPB == 1, "key split: one item per workgroup");
+  constexpr int ND = HD / 32;   // 32-wide output blocks
+  constexpr int NK = HD / 16;   // 16-deep MFMA steps of q . k
+  const int lane = threadIdx.x & 63, lrow = lane & 31, lgrp = lane >> 5;
+  const int kw = KS > 1 ? (int)(threadIdx.x >> 6) : 0;   // key-split wave
+  const int w = KS > 1 ? (int)blockIdx.x : (int)(blockIdx.x * WPB + (threadIdx.x >> 6));
+  // KS = 1: wave-uniform exit, nothing below synchronises waves; KS > 1: the
+  // whole workgroup exits together (one item per workgroup)
+  if (w >= a.n_items) return;
+  const int bi = w / a.Hq, head = w % a.Hq, kvh = head / a.rep;
+  int lo = 0, hi = a.n_seq - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.blk0[mid] <= bi) lo = mid; else hi = mid - 1;
+  }
+  const int s0 = a.cu[lo], L = a.cu[lo + 1] - s0;
+  const int q0 = (bi - a.blk0[lo]) * 32;           // first query of the wave (within the sequence)
+  const int my_q = q0 + lrow;
+  const int q_last = min(q0 + 31, L - 1);
+  const int P = a.P;
+  const int koff = (a.Hq + kvh) * HD + lgrp * 8;   // this lane's 8 d of a key row
+
+  f16x8 qf[NK];
+  {
+    const f16 *qr = a.qk + (size_t)(s0 + min(my_q, L - 1)) * a.ldq + head * HD + lgrp * 8;
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) qf[kk] = *(const f16x8 *)(qr + kk * 16);
+  }
+  f32x16 oacc[ND];
+#pragma unroll
+  for (int n = 0; n < ND; ++n)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[n][r] = 0.f;
+  float m_i = -INFINITY, l_i = 0.f;
+
+  // Key tiles: the prefix's tiles 0 .. np-1, then the batch's global tiles
+  // t_lo .. t_hi holding the sequence's visible keys.
+  const int np = (P + 31) >> 5;
+  const int kend = a.causal ? q_last : L - 1;      // last own key any query of the wave sees
+  const int t_lo = s0 >> 5, t_hi = (s0 + kend) >> 5;
+  const int nt = np + (t_hi - t_lo + 1);
+  auto kload = [&](int u, f16x8 (&kf)[NK]) {
+    const f16 *src;
+    int row;
+    if (u < np) { src = a.pqk; row = min(u * 32 + lrow, P - 1); }
+    else { src = a.qk; row = min((t_lo + u - np) * 32 + lrow, a.T - 1); }
+    const f16 *kr = src + (size_t)row * a.ldq + koff;
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) kf[kk] = *(const f16x8 *)(kr + kk * 16);
+  };
+  f16x8 kf[NK], kn[NK];
+  if (kw < nt) kload(kw, kf);
+  for (int u = kw; u < nt; u += KS) {
+    const bool pre = u < np;
+    const int t = pre ? u : t_lo + u - np;
+    // V^T fragments of this tile (used after the softmax)
+    f16x8 vf[ND][2];
+    {
+      const f16 *vb = (pre ? a.pvt : a.vt) + (((size_t)t * a.Hkv + kvh) * HD + lrow) * 32 + lgrp * 8;
+#pragma unroll
+      for (int n = 0; n < ND; ++n)
+#pragma unroll
+        for (int f = 0; f < 2; ++f) vf[n][f] = *(const f16x8 *)(vb + (size_t)n * 32 * 32 + f * 16);
+    }
+    f32x16 sacc[2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[x][r] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) mfma32(sacc[kk & 1], kf[kk], qf[kk]);
+    if (u + KS < nt) kload(u + KS, kn);
+    f32x16 s = sacc[0] + sacc[1];
+    // key of register r: row 32 t + acc_row(r, lane) of its source
+    float mb = -INFINITY;
+    bool full;
+    if (pre) full = t * 32 + 31 < P;
+    else full = t * 32 >= s0 && t * 32 + 31 <= s0 + (a.causal ? q0 : L - 1) && t * 32 + 31 < s0 + L;
+    if (full) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        s[r] *= a.sc;
+        mb = fmaxf(mb, s[r]);
+      }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int k = t * 32 + acc_row(r, lane);
+        const bool ok = pre ? k < P : (k >= s0 && k < s0 + L && (!a.causal || k - s0 <= my_q));
+        s[r] = ok ? s[r] * a.sc : -INFINITY;
+        mb = fmaxf(mb, s[r]);
+      }
+    }
+    mb = warp_max_xor(mb, 32);
+    const float m_new = fmaxf(m_i, mb);
+    const float m_ref = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = exp2f(m_i - m_ref);
+    m_i = m_new;
+    float p[16], ps = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      p[r] = exp2f(s[r] - m_ref);
+      ps += p[r];
+    }
+    l_i = l_i * alpha + ps;
+    if (__any(alpha != 1.f)) {
+#pragma unroll
+      for (int n = 0; n < ND; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[n][r] *= alpha;
+    }
+    f16x8 pf[2];
+#pragma unroll
+    for (int f = 0; f < 2; ++f)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) pf[f][e] = (f16)p[8 * f + e];
+#pragma unroll
+    for (int f = 0; f < 2; ++f)
+#pragma unroll
+      for (int n = 0; n < ND; ++n) mfma32(oacc[n], vf[n][f], pf[f]);
+    if (u + KS < nt) {
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk) kf[kk] = kn[kk];
+    }
+  }
+  if constexpr (KS > 1) {
+    // waves 1.. hand (m, l, O^T) to wave 0, lane-contiguous (no bank conflicts)
+    constexpr int NV = 2 + ND * 16;
+    __shared__ float red[KS - 1][NV][64];
+    if (kw > 0) {
+      red[kw - 1][0][lane] = m_i;
+      red[kw - 1][1][lane] = l_i;
+#pragma unroll
+      for (int n = 0; n < ND; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) red[kw - 1][2 + n * 16 + r][lane] = oacc[n][r];
+    }
+    __syncthreads();
+    if (kw > 0) return;
+    float mx = m_i;
+#pragma unroll
+    for (int v = 0; v < KS - 1; ++v) mx = fmaxf(mx, red[v][0][lane]);
+    const float mr = mx == -INFINITY ? 0.f : mx;   // wave 0 always saw key 0, so mx is finite
+    const float f0 = exp2f(m_i - mr);
+    l_i *= f0;
+#pragma unroll
+    for (int n = 0; n < ND; ++n)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[n][r] *= f0;
+#pragma unroll
+    for (int v = 0; v < KS - 1; ++v) {
+      const float fv = exp2f(red[v][0][lane] - mr);
+      l_i += fv * red[v][1][lane];
+#pragma unroll
+      for (int n = 0; n < ND; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[n][r] += fv * red[v][2 + n * 16 + r][lane];
+    }
+  }
+  // Output: oacc[n] registers 4c..4c+3 are d = 32 n + 8 c + 4 lgrp + 0..3 of
+  // the lane's query, one 8-byte store each.
+  const float inv = 1.f / (l_i + __shfl_xor(l_i, 32, kWave));
+  if (my_q < L) {
+    f16 *orow = a.o + ((size_t)(s0 + my_q) * a.Hq + head) * HD + 4 * lgrp;
+#pragma unroll
+    for (int n = 0; n < ND; ++n)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        f16x4 h4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) h4[e] = (f16)(oacc[n][4 * c + e] * inv);
+        *(f16x4 *)(orow + n * 32 + 8 * c) = h4;
+      }
+  }
+}
+
+hipError_t launch_attention_h(const f16 *qk, const f16 *vt, const f16 *prefix, const f16 *pvt, int P, f16 *o,
+                              float sc, const int32_t *cu, int batch, int T, int Hq, int Hkv, int d, int causal,
+                              hipStream_t s) {
+  constexpr int WPB = 2;      // work items (waves) per workgroup without key split
+  constexpr int KS = 4;       // waves per work item with key split
+  if (P < 0 || (P > 0 && (!prefix || !pvt)) || (d != 64 && d != 128) || Hq % Hkv || !qk || !vt || !o)
+    return hipErrorInvalidValue;
+  AttnHArgs a;
+  a.qk = qk;
+  a.vt = vt;
+  a.pqk = prefix;
+  a.pvt = pvt;
+  a.o = o;
+  a.sc = sc;
+  a.ldq = (Hq + Hkv) * d;
+  a.T = T;
+  a.P = P;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.rep = Hq / Hkv;
+  a.causal = causal ? 1 : 0;
+  for (int first = 0; first < batch; first += kMaxSeqPerLaunch) {
+    const int n = batch - first < kMaxSeqPerLaunch ? batch - first : kMaxSeqPerLaunch;
+    a.n_seq = n;
+    int blocks = 0;
+    for (int i = 0; i < n; ++i) {
+      a.cu[i] = cu[first + i];
+      a.blk0[i] = blocks;
+      blocks += (cu[first + i + 1] - cu[first + i] + 31) / 32;
+    }
+    a.cu[n] = cu[first + n];
+    a.blk0[n] = blocks;
+    a.n_items = blocks * Hq;
+    if (a.n_items == 0) continue;
+    // Few items (one or two frames) leave most of the chip idle and each
+    // item's tile steps in series: split every item's key tiles over KS waves.
+    if (a.n_items < 256) {
+      if (d == 128) hipLaunchKernelGGL((k_attn_h<128, 1, KS>), dim3(a.n_items), dim3(64 * KS), 0, s, a);
+      else hipLaunchKernelGGL((k_attn_h<64, 1, KS>), dim3(a.n_items), dim3(64 * KS), 0, s, a);
+    } else {
+      dim3 grid((a.n_items + WPB - 1) / WPB);
+      if (d == 128) hipLaunchKernelGGL((k_attn_h<128, WPB, 1>), grid, dim3(64 * WPB), 0, s, a);
+      else hipLaunchKernelGGL((k_attn_h<64, WPB, 1>), grid, dim3(64 * WPB), 0, s, a);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -36,10 +36,11 @@ static bool tile_fits(int id, int N, int K, int esz, int epi, int splits, int co
 static const double kTileRate[kNumTiles] = {959, 944, 895, 850, 850, 884, 850, 850, 800, 819,
                                             640, 777, 860, 600, 700, 650, 550, 450, 600, 600,
                                             921, 850, 850, 714, 766, 800, 1026, 1018, 850, 728,
-                                            803, 950, 950, 1150, 1106, 1084, 940, 1044, 1117};
+                                            803, 950, 950, 1150, 1106, 1084, 940, 1044, 1117,
+                                            300, 300, 300, 300, 300, 300, 300};
 
-// Measured choices (MI355X sweep of every tile and split count, weights
-// rotated through 600 MB so that they stream from HBM; at 96 and 192 rows
+// Measured choices (MI355X sweep of every tile, split count and XCD placement,
+// weights rotated through 600 MB so that they stream from HBM; at 96 and 192 rows
 // timed together with the kernel that consumes the product; the leading
 // candidates then timed again round robin, three times each, since a sweep
 // in fixed order drifts with the clock as the card warms) for the decoder's four
@@ -52,15 +53,16 @@ static const double kTileRate[kNumTiles] = {959, 944, 895, 850, 850, 884, 850, 8
 // that the consuming kernel adds up.
 struct TileChoice {
   int n, k, epi, m, tile, splits;
+  int xcd = 0;   // placement on the XCDs as 100 xa + 10 xb + xc (see GemmArgs), 0: by N tile
 };
 static const TileChoice kChoices[] = {
-    {4096, 2048, EPI_QKV, 96, 13, 4},     {2048, 2048, EPI_RESID, 96, 13, 4},
-    {12288, 2048, EPI_SWIGLU, 96, 12, 2},  {2048, 6144, EPI_RESID, 96, 13, 8},
+    {4096, 2048, EPI_QKV, 96, 42, 4},     {2048, 2048, EPI_RESID, 96, 42, 4},
+    {12288, 2048, EPI_SWIGLU, 96, 42, 1},  {2048, 6144, EPI_RESID, 96, 42, 8},
     {4096, 2048, EPI_QKV, 192, 12, 2},    {2048, 2048, EPI_RESID, 192, 13, 4},
     {12288, 2048, EPI_SWIGLU, 192, 12, 1}, {2048, 6144, EPI_RESID, 192, 14, 8},
-    {4096, 2048, EPI_QKV, 768, 12, 1},    {2048, 2048, EPI_RESID, 768, 12, 2},
+    {4096, 2048, EPI_QKV, 768, 12, 1, 241},    {2048, 2048, EPI_RESID, 768, 12, 2, 222},
     {12288, 2048, EPI_SWIGLU, 768, 3, 1},  {2048, 6144, EPI_RESID, 768, 14, 2},
-    {4096, 2048, EPI_QKV, 1536, 36, 1},   {2048, 2048, EPI_RESID, 1536, 14, 1},
+    {4096, 2048, EPI_QKV, 1536, 36, 1, 421},   {2048, 2048, EPI_RESID, 1536, 14, 1, 181},
     {12288, 2048, EPI_SWIGLU, 1536, 33, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
     {4096, 2048, EPI_QKV, 3072, 38, 1},   {2048, 2048, EPI_RESID, 3072, 8, 1},
     {12288, 2048, EPI_SWIGLU, 3072, 33, 1}, {2048, 6144, EPI_RESID, 3072, 8, 1},
@@ -79,7 +81,7 @@ static const TileChoice kChoicesW8[] = {
     {12288, 2048, EPI_SWIGLU, 96, 14, 1},  {2048, 6144, EPI_RESID, 96, 17, 8},
     {4096, 2048, EPI_QKV, 192, 17, 2},    {2048, 2048, EPI_RESID, 192, 17, 4},
     {12288, 2048, EPI_SWIGLU, 192, 14, 1}, {2048, 6144, EPI_RESID, 192, 12, 8},
-    {4096, 2048, EPI_QKV, 1536, 36, 1},   {2048, 2048, EPI_RESID, 1536, 14, 1},
+    {4096, 2048, EPI_QKV, 1536, 36, 1, 421},   {2048, 2048, EPI_RESID, 1536, 14, 1, 181},
     {12288, 2048, EPI_SWIGLU, 1536, 33, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
 };
 
@@ -113,7 +115,8 @@ static void plan_model(int M, int N, int K, int esz, int epi, int col_align, siz
 }
 
 static void plan(int M, int N, int K, int esz, int epi, int col_align, size_t ws_elems, bool w8,
-                 int *tile, int *splits) {
+                 int *tile, int *splits, int *xcd) {
+  *xcd = 0;
   const TileChoice *best = nullptr;
   double bd = 1e30;
   if (esz == 2) {
@@ -132,6 +135,7 @@ static void plan(int M, int N, int K, int esz, int epi, int col_align, size_t ws
        ((M <= 256 || (M <= 2048 && best->splits == 2)) && (size_t)best->splits * M * N <= ws_elems))) {
     *tile = best->tile;
     *splits = best->splits;
+    *xcd = best->xcd;
     return;
   }
   plan_model(M, N, K, esz, epi, col_align, ws_elems, w8, tile, splits);
@@ -139,10 +143,22 @@ static void plan(int M, int N, int K, int esz, int epi, int col_align, size_t ws
 
 hipError_t launch_mode_f8w(int epi, int tile, int splits, const GemmArgs &a, hipStream_t s);
 
+// Decodes an XCD placement 100 xa + 10 xb + xc into a, or clears it when it
+// does not fit the grid (xa x xb x xc != 8, or a factor not dividing its grid
+// dimension): the placement only permutes tiles, so any grid stays correct.
+static void set_xcd(GemmArgs &a, int code, int gm, int gn, int splits) {
+  const int xa = code / 100, xb = (code / 10) % 10, xc = code % 10;
+  a.xa = a.xb = a.xc = 0;
+  if (code <= 0 || xa * xb * xc != 8 || gm % xa || gn % xb || splits % xc) return;
+  a.xa = xa;
+  a.xb = xb;
+  a.xc = xc;
+}
+
 hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void *A, const void *W,
                             void *C, size_t c_plane, int M, int N, int K, int ldc, float scale,
                             float out_scale, const QkvEpi *qe, hipStream_t s, const float *col_scale,
-                            const float *bias) {
+                            const float *bias, int xcd) {
   if (M <= 0) return hipSuccess;
   const bool w8 = mode == MODE_F8W;
   if (bias && splits > 1) return hipErrorInvalidValue;
@@ -157,7 +173,8 @@ hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void 
       (splits > 1 && epi != EPI_PARTIAL))
     return hipErrorInvalidValue;
   GemmArgs a{(const char *)A, (const char *)W, C, c_plane, M, N, K, ldc, K / splits, scale, out_scale,
-             epi == EPI_QKV ? *qe : QkvEpi{}, w8 ? col_scale : nullptr, bias};
+             epi == EPI_QKV ? *qe : QkvEpi{}, w8 ? col_scale : nullptr, bias, 0, 0, 0};
+  set_xcd(a, xcd, (M + kTiles[tile].bm - 1) / kTiles[tile].bm, N / kTiles[tile].bn, splits);
   if (w8) return launch_mode_f8w(epi, tile, splits, a, s);
   return mode == MODE_F16 ? launch_mode<MODE_F16>(epi, tile, splits, a, s)
                           : launch_mode<MODE_F32>(epi, tile, splits, a, s);
@@ -170,17 +187,17 @@ hipError_t launch_gemm(int mode, int epi, const void *A, const void *W, void *C,
   *splits_out = 0;
   if (M <= 0) return hipSuccess;
   if (epi == EPI_QKV && !qe) return hipErrorInvalidValue;
-  int tile, splits;
+  int tile, splits, xcd;
   plan(M, N, K, mode == MODE_F32 ? 4 : 2, epi, epi == EPI_QKV ? qe->hd : 32, (ws && !bias) ? ws_elems : 0,
-       mode == MODE_F8W, &tile, &splits);
+       mode == MODE_F8W, &tile, &splits, &xcd);
   if (tile < 0) return hipErrorInvalidValue;
   if (splits > 1) {
     *splits_out = splits;
     return launch_gemm_tile(mode, EPI_PARTIAL, tile, splits, A, W, ws, (size_t)M * N, M, N, K, N, scale,
-                            1.f, nullptr, s, col_scale);
+                            1.f, nullptr, s, col_scale, nullptr, xcd);
   }
   return launch_gemm_tile(mode, epi, tile, 1, A, W, C, 0, M, N, K, ldc, scale, out_scale, qe, s, col_scale,
-                          bias);
+                          bias, xcd);
 }
 
 }  // namespace mte

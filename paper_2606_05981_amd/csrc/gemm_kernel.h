@@ -24,9 +24,11 @@
 // wave a (BM/WM) x (BN/WN) block of 32x32 MFMA tiles. Eight waves, or two
 // four-wave workgroups per CU, put two waves on every SIMD, so one wave's
 // LDS reads and waits overlap the other's MFMAs. K is walked in stages of 64
-// or 128 bytes per row, staged through a ring of 2-6 LDS slots (one barrier
+// or 128 bytes per row, staged through a ring of 2-16 LDS slots (one barrier
 // per stage): the loads of the next P stages are in flight while the current
-// one feeds the MFMAs.
+// one feeds the MFMAs. The deep rings serve small M (one frame), where a
+// workgroup's whole K range is a handful of stages: all of them are then in
+// flight at once and the kernel waits for memory once, not once per stage.
 //
 // LDS rows are 128 bytes = 8 chunks of 16 bytes; chunk c of row r is stored
 // at slot c ^ ((r ^ (r >> 3)) & 7), so the 16-byte fragment reads of 8 or 16
@@ -66,6 +68,12 @@ struct GemmArgs {
   QkvEpi qe;          // EPI_QKV
   const float *cs;    // MODE_F8W: per-column (weight row) scales [N]
   const float *bias;  // [N] added to the product before the epilogue (unsplit launches), or null
+  // Placement of tiles on the eight XCDs (workgroup i of a launch runs on XCD
+  // i % 8): xa x xb x xc = 8 with xa | M tiles, xb | N tiles, xc | K splits;
+  // XCD x serves one block of M tiles, one of N tiles and one of splits, so
+  // it fetches only its share of A and W into its L2. xa = 0: workgroup
+  // (x, y, z) serves N tile x, M tile y, split z.
+  int xa, xb, xc;
 };
 
 // tanh-approximated GELU, 0.5 z (1 + tanh(u)) with u = sqrt(2/pi) (z + 0.044715 z^3),
@@ -180,8 +188,9 @@ __host__ __device__ constexpr int acc_row0(int r) { return 8 * (r >> 2) + (r & 3
 // HD/32 column blocks and the 32 lanes that hold the row) and rotate pair
 // (c, c + HD/2), i.e. column blocks (jb, jb + HD/64) of one lane. Gains are
 // read once; the rotary table values of a block of 32 rows are read before
-// they are used. A block wholly inside M is stored at a wave-uniform row
-// address plus a 32-bit lane offset, without per-row tests.
+// they are used. fp32 rows: a block wholly inside M is stored at a
+// wave-uniform row address plus a 32-bit lane offset, without per-row tests.
+// With q.qk the result goes out in the fp16 attention operand layout.
 template <int HD, int TM, int TN>
 __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const GemmArgs &g, int cw,
                                              int mw, int lane) {
@@ -270,7 +279,20 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const 
           v[jp] = w * tc[r][x] + u * ts[r][x];
         }
       }
-      if (full) {
+      if (q.qk) {
+        // attention operand layout: q and k heads as fp16 rows (v below)
+        const int m = mb + acc_row(r, lane);
+        if (m < M) {
+          f16 *qr = q.qk + (size_t)m * q.rot_cols + cw + lrow;
+#pragma unroll
+          for (int h = 0; h < NH; ++h) {
+            if (!rot[h]) continue;
+            const float pre = cw + h * HD < q.nq_cols ? q.q_pre : q.k_pre;
+#pragma unroll
+            for (int jj = 0; jj < HJB; ++jj) qr[(h * HJB + jj) * 32] = (f16)(v[h * HJB + jj] * pre);
+          }
+        }
+      } else if (full) {
         float *p = C + (size_t)(mb + acc_row0(r)) * g.ldc + cw;
 #pragma unroll
         for (int j = 0; j < TN; ++j) at(p, lofs + j * 128u) = v[j];
@@ -279,6 +301,33 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const 
         if (m < M)
 #pragma unroll
           for (int j = 0; j < TN; ++j) C[(size_t)m * g.ldc + cw + j * 32 + lrow] = v[j];
+      }
+    }
+    if (q.qk && mb < M) {
+      // v heads as V^T tiles: the block's 32 rows are one token tile (mb is a
+      // multiple of 32), and a lane's 16 accumulator rows are exactly the
+      // values of its column in the tile's fragment order: registers 0..7 go
+      // to positions 8g.., registers 8..15 to 16 + 8g.. (g = lane / 32).
+      // Rows past M are written as zeros; blocks wholly past M belong to no
+      // tile of the batch and are skipped.
+#pragma unroll
+      for (int h = 0; h < NH; ++h) {
+        if (rot[h]) continue;
+#pragma unroll
+        for (int jj = 0; jj < HJB; ++jj) {
+          const int j = h * HJB + jj;
+          const int dv = cw + j * 32 + lrow - q.rot_cols;
+          f16 *dst = q.vt + (((size_t)(mb >> 5) * q.hkv + dv / HD) * HD + dv % HD) * 32 + lgrp * 8;
+          f16x8 lo, hi;
+          const float sv = g.scale * q.v_pre;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            lo[e] = (f16)(mb + acc_row(e, lane) < M ? acc[i][j][e] * sv : 0.f);
+            hi[e] = (f16)(mb + acc_row(8 + e, lane) < M ? acc[i][j][8 + e] * sv : 0.f);
+          }
+          *(f16x8 *)dst = lo;
+          *(f16x8 *)(dst + 16) = hi;
+        }
       }
     }
   }
@@ -295,7 +344,7 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const 
 // Raw s_barrier (no fence) keeps the compiler from forcing vmcnt(0) at the
 // barrier; the waits are explicit.
 template <int MODE, int BM, int BN, int WM, int WN, int ROWB, int P, int EPI, int OCC>
-__global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_eu(OCC * WM * WN / 4, OCC * WM * WN / 4))) void k_gemm(GemmArgs g) {
+__global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_eu((OCC * WM * WN + 3) / 4, (OCC * WM * WN + 3) / 4))) void k_gemm(GemmArgs g) {
   typedef typename std::conditional<MODE == MODE_F32, float, f16>::type T;
   constexpr bool W8 = MODE == MODE_F8W;           // one-byte weights
   constexpr int KS = ROWB / (int)sizeof(T);       // k elements per stage
@@ -316,20 +365,33 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
   constexpr int AR = (AG + NW - 1) / NW, BR = (BG + NW - 1) / NW;   // DMA instructions per thread
   constexpr int LOADS = AR + BR;                  // per thread per stage
   constexpr int STAGE = ACH + BCH;                // u32x4 slots per stage
-  static_assert(NW == 4 || NW == 8, "4 or 8 waves");
+  static_assert(NW == 4 || NW == 6 || NW == 8, "4, 6 or 8 waves");
   static_assert(WTM % 32 == 0 && WTN % 32 == 0, "wave tile");
-  static_assert(LOADS * (P - 1) < 64 && P >= 2 && P <= 6, "vmcnt range, ring depth");
+  static_assert(LOADS * (P - 1) < 64 && P >= 2 && P <= 16, "vmcnt range, ring depth");
   typedef typename Frag<T>::type frag_t;
 
   extern __shared__ u32x4 lds[];                  // [P][STAGE]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  const int n0 = blockIdx.x * BN, m0 = blockIdx.y * BM;
+  int tn = blockIdx.x, tm = blockIdx.y, tz = blockIdx.z;
+  if (g.xa) {
+    // XCD of this workgroup and its index among that XCD's workgroups
+    const int lin = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+    const int xcd = lin & 7, j = lin >> 3;
+    const int xbc = g.xb * g.xc;
+    const int xi = xcd / xbc, xj = (xcd % xbc) / g.xc, xk = xcd % g.xc;
+    const int sm = gridDim.y / g.xa, sn = gridDim.x / g.xb, ss = gridDim.z / g.xc;
+    const int n = j % sn, t = j / sn;
+    tn = xj * sn + n;
+    tm = xi * sm + t % sm;
+    tz = xk * ss + t / sm;
+  }
+  const int n0 = tn * BN, m0 = tm * BM;
   const int M = g.M;
   const size_t rowb = (size_t)g.K * sizeof(T);    // row pitch in bytes (A; W unless W8)
-  const size_t kb0 = (size_t)blockIdx.z * g.k_chunk * sizeof(T);
+  const size_t kb0 = (size_t)tz * g.k_chunk * sizeof(T);
   const size_t rowbw = W8 ? (size_t)g.K : rowb;
-  const size_t kb0w = W8 ? (size_t)blockIdx.z * g.k_chunk : kb0;
+  const size_t kb0w = W8 ? (size_t)tz * g.k_chunk : kb0;
   const int nk = g.k_chunk / KS;
 
   // DMA sources: instruction c of this thread fills LDS slot q = (c*NW + wave)*64 + lane
@@ -610,7 +672,7 @@ __global__ __launch_bounds__(64 * WM * WN, OCC) __attribute__((amdgpu_waves_per_
   // EPI_STORE / EPI_PARTIAL: C = scale * acc; EPI_RESID: C += scale * acc (one
   // rounding: scale is a power of two), the block's old values all read
   // before the first store so that their latencies overlap.
-  float *C = (float *)g.C + (EPI == EPI_PARTIAL ? (size_t)blockIdx.z * g.c_plane : 0);
+  float *C = (float *)g.C + (EPI == EPI_PARTIAL ? (size_t)tz * g.c_plane : 0);
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
     const int mb = mw + i * 32;
@@ -724,7 +786,14 @@ static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
   X(35, 192, 384, 2, 4, 64, 3, 1, 0)         \
   X(36, 128, 128, 4, 1, 128, 2, 2, 0)        \
   X(37, 192, 128, 2, 2, 128, 2, 1, 0)        \
-  X(38, 256, 256, 4, 2, 128, 2, 1, 0)
+  X(38, 256, 256, 4, 2, 128, 2, 1, 0)        \
+  X(39, 96, 64, 3, 2, 64, 16, 1, 0)          \
+  X(40, 96, 64, 3, 2, 64, 8, 2, 0)           \
+  X(41, 96, 128, 3, 2, 64, 10, 1, 0)         \
+  X(42, 96, 64, 3, 2, 128, 8, 1, 0)          \
+  X(43, 128, 64, 4, 1, 64, 12, 1, 0)         \
+  X(44, 96, 128, 3, 2, 128, 5, 1, 0)         \
+  X(45, 96, 256, 3, 2, 64, 6, 1, 0)
 
 
 template <int MODE, int EPI>

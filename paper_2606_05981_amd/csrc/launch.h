@@ -7,13 +7,17 @@
 
 namespace mte {
 
+typedef _Float16 f16;
+
 // Arithmetic of the matrix-core steps.
 enum Mode {
   MODE_F32 = 0,  // fp32 weights and activations, fp32 MFMA
-  MODE_F16 = 1,  // projections: fp16 operands (weights = bf16 values held exactly as
-                 // power-of-two scaled fp16, activations rounded once to fp16), fp32
-                 // accumulate; attention: fp32 q/k/v/P split into bf16 hi + lo, three
-                 // bf16 MFMAs per product; attention output rounded to fp16
+  MODE_F16 = 1,  // projections: fp16 operands (weights = bf16 values as power-of-two
+                 // scaled fp16, exact down to 2^-31 of the matrix maximum; activations
+                 // rounded once to fp16), fp32 accumulate; decoder attention: q, k, v and
+                 // P as fp16 (power-of-two pre-scales), fp32 accumulate and softmax
+                 // (launch_attention_h); vision attention: q/k split into bf16 hi + lo
+                 // (launch_attention); attention output rounded to fp16
   MODE_F8W = 2,  // projections only: fp16 activations as MODE_F16, weights OCP e4m3 codes
                  // with a power-of-two scale per weight row, widened to fp16 for the MFMAs
 };
@@ -40,10 +44,20 @@ enum Epilogue {
 // (token m) rotates pair (c, c + hd/2) of a head by the angle whose cos / sin
 // are rcos / rsin [m * hd/2 + c]. qn / kn: per-head RMSNorm gains [hd], or
 // both null (no QK-norm).
+// With qk non-null the result is written in the operand layout of
+// launch_attention_h instead of fp32 rows: q and k heads as fp16 rows
+// qk [m, rot_cols] times q_pre / k_pre, and v as fp16 V^T tiles vt (see
+// launch_attention_h) times v_pre, the rows of a 32-token tile past the last
+// token written as zeros. q_pre, k_pre, v_pre: powers of two that keep the
+// values in fp16 range.
 struct QkvEpi {
   const float *rcos, *rsin, *qn, *kn;
   int rot_cols, nq_cols, hd;
   float eps;
+  f16 *qk = nullptr;
+  f16 *vt = nullptr;
+  float q_pre = 1.f, k_pre = 1.f, v_pre = 1.f;
+  int hkv = 0;
 };
 
 // C = A[M, K] * W[N, K]^T, A and W of the mode's operand type (float or
@@ -72,11 +86,14 @@ hipError_t launch_gemm(int mode, int epi, const void *A, const void *W, void *C,
 // The same with an explicit tile configuration (index into the GEMM tile
 // table) and number of K splits (> 1 only with EPI_PARTIAL, partial sums
 // c_plane elements apart); used for tuning. Returns hipErrorInvalidValue if
-// the tile does not fit the shape.
+// the tile does not fit the shape. xcd: placement of the tiles on the eight
+// XCDs, 100 xa + 10 xb + xc with xa x xb x xc = 8 groups of M tiles, N tiles
+// and K splits (each XCD reads only its groups' operands); 0, or a placement
+// that does not divide the grid: workgroup order by N tile.
 hipError_t launch_gemm_tile(int mode, int epi, int tile, int splits, const void *A, const void *W,
                             void *C, size_t c_plane, int M, int N, int K, int ldc, float scale,
                             float out_scale, const QkvEpi *qe, hipStream_t s,
-                            const float *col_scale = nullptr, const float *bias = nullptr);
+                            const float *col_scale = nullptr, const float *bias = nullptr, int xcd = 0);
 int gemm_num_tiles();
 
 // Per-row RMSNorm: out[r, :] = x[r, :] / sqrt(mean(x[r,:]^2) + eps) * g with
@@ -113,7 +130,9 @@ hipError_t launch_rope_table(const int32_t *pos_thw, int T, int half, const Rope
 
 // QKV projection finished from nparts partial sums [T, (Hq+2Hkv)*d]
 // (T*(Hq+2Hkv)*d elements apart, added in order) into qkv, with the q and k
-// heads normalised and rotated as by EPI_QKV (qe; v copied).
+// heads normalised and rotated as by EPI_QKV (qe; v copied). With qe.qk
+// non-null the output goes to qe.qk / qe.vt in the attention operand layout
+// (qkv unused).
 hipError_t launch_qkv_parts(float *qkv, const float *parts, int nparts, int T, int Hq, int Hkv,
                             const QkvEpi &qe, hipStream_t s);
 
@@ -130,6 +149,24 @@ hipError_t launch_qkv_parts(float *qkv, const float *parts, int nparts, int T, i
 hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int P, void *o, float out_scale,
                             const int32_t *cu, int batch, int Hq, int Hkv, int d, hipStream_t s,
                             int causal = 1, int pv_f16 = 0);
+
+// Causal (or bidirectional) GQA attention over packed sequences on fp16
+// operands laid out for the matrix cores by the QKV projection's epilogue:
+//  qk: fp16 [T, (Hq + Hkv) d] rows, q heads then k heads, q times 2^-aq and
+//      k times 2^-ak (sc below undoes both);
+//  vt: fp16 V^T tiles [ceil(T / 32)][Hkv][d][32]: tile t holds tokens
+//      32t .. 32t+31, each d row's 32 values in the order the softmax
+//      probabilities come out of the score MFMA (position 16f + 8g + e holds
+//      token 8 (i / 4) + 4 g + i % 4 of the tile, i = 8 f + e), rows past T
+//      zero; V already times the output's pre-scale.
+//  prefix / pvt: the same two layouts for P rows of a shared prefix (its k
+//      heads and V^T tiles are read), or P = 0.
+// o: fp16 [T, Hq d]. sc = log2(e) / sqrt(d) * 2^(aq + ak). cu: host
+// int32[batch+1] offsets. One wave per (sequence, query head, 32 queries);
+// launches in chunks of <= 256 sequences.
+hipError_t launch_attention_h(const f16 *qk, const f16 *vt, const f16 *prefix, const f16 *pvt, int P, f16 *o,
+                              float sc, const int32_t *cu, int batch, int T, int Hq, int Hkv, int d, int causal,
+                              hipStream_t s);
 
 // Positions of packed sequences (see mte_build_positions).
 hipError_t launch_positions(const int32_t *layouts5, int batch, int32_t *pos_thw, int T,

@@ -240,6 +240,55 @@ __global__ __launch_bounds__(256) void k_qkv_parts(float *__restrict__ qkv, Part
   }
 }
 
+// The same into the attention operand layout (qe.qk / qe.vt): one block per
+// token of the padded range [0, 32 ceil(T / 32)); tokens past T only write
+// their V^T entries, as zeros.
+__global__ __launch_bounds__(256) void k_qkv_parts_h(Parts pt, int T, int Hq, int Hkv, QkvEpi qe) {
+  const int tok = blockIdx.x, tid = threadIdx.x;
+  const int d = qe.hd, half = d >> 1;
+  const int nh = Hq + Hkv, nqkv = (Hq + 2 * Hkv) * d;
+  const bool live = tok < T;
+  const float *prow = pt.p + (size_t)min(tok, T - 1) * nqkv;
+  auto ld = [&](int c) -> float {
+    float q[kMaxParts];
+#pragma unroll
+    for (int k = 0; k < kMaxParts; ++k)
+      if (k < pt.np) q[k] = prow[(size_t)k * pt.stride + c];
+    float v = q[0];
+#pragma unroll
+    for (int k = 1; k < kMaxParts; ++k)
+      if (k < pt.np) v += q[k];
+    return v;
+  };
+  const int it = blockIdx.y * 256 + tid;
+  if (it < nh * half) {
+    if (!live) return;                           // block-uniform
+    const int h = it / half, j = it % half;
+    const int c0 = h * d + j;
+    float u = ld(c0), w = ld(c0 + half);
+    if (qe.qn) {
+      const float *gn = (h < Hq) ? qe.qn : qe.kn;
+      float ss = u * u + w * w;
+      for (int m = half >> 1; m >= 1; m >>= 1) ss = warp_sum_xor(ss, m);
+      const float rs = rsqrtf(ss / (float)d + qe.eps);
+      u = u * rs * gn[j];
+      w = w * rs * gn[j + half];
+    }
+    const float c = qe.rcos[(size_t)tok * half + j], s = qe.rsin[(size_t)tok * half + j];
+    const float pre = h < Hq ? qe.q_pre : qe.k_pre;
+    f16 *row = qe.qk + (size_t)tok * nh * d;
+    row[c0] = (f16)((u * c - w * s) * pre);
+    row[c0 + half] = (f16)((w * c + u * s) * pre);
+  } else if (it < nh * half + Hkv * d) {
+    const int dv = it - nh * half;
+    const float v = live ? ld(nh * d + dv) * qe.v_pre : 0.f;
+    // position of the token in its tile's fragment order
+    const int t = tok & 31, i = 4 * (t >> 3) + (t & 3);
+    const int pos = 16 * (i >> 3) + 8 * ((t >> 2) & 1) + (i & 7);
+    qe.vt[(((size_t)(tok >> 5) * Hkv + dv / d) * d + dv % d) * 32 + pos] = (f16)v;
+  }
+}
+
 hipError_t launch_qkv_parts(float *qkv, const float *parts, int nparts, int T, int Hq, int Hkv,
                             const QkvEpi &qe, hipStream_t s) {
   if (T <= 0) return hipSuccess;
@@ -247,7 +296,13 @@ hipError_t launch_qkv_parts(float *qkv, const float *parts, int nparts, int T, i
   const int d = qe.hd;
   const Parts pt{parts, nparts, (size_t)T * (Hq + 2 * Hkv) * d};
   const int items = (Hq + Hkv) * (d / 2) + Hkv * d;
-  hipLaunchKernelGGL(k_qkv_parts, dim3(T, (items + 255) / 256), dim3(256), 0, s, qkv, pt, Hq, Hkv, qe);
+  if (qe.qk) {
+    if (!qe.vt || qe.hkv != Hkv) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(k_qkv_parts_h, dim3((T + 31) / 32 * 32, (items + 255) / 256), dim3(256), 0, s, pt, T, Hq,
+                       Hkv, qe);
+  } else {
+    hipLaunchKernelGGL(k_qkv_parts, dim3(T, (items + 255) / 256), dim3(256), 0, s, qkv, pt, Hq, Hkv, qe);
+  }
   return hipGetLastError();
 }
 
