@@ -35,6 +35,7 @@
 // activations are. The sequence table (offsets, first tile of each
 // sequence) is passed by value in the kernel arguments, so nothing is read
 // back to the host.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -562,7 +563,9 @@ hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int
 // batch's global 32-token tiles, so a sequence that starts inside a tile
 // masks the tile's leading keys; keys of other sequences and zero-padded
 // rows past the batch enter with probability exactly 0. The next tile's k
-// fragments are loaded while the current tile's probabilities are formed.
+// fragments are loaded while the current tile is computed. Masks are
+// selects on the key index, exponentials the hardware base-2 exponential
+// (v_exp_f32; the arguments are <= 0, exp2(-inf) = 0).
 // With KS > 1 (few work items, e.g. one frame) a workgroup of KS waves
 // serves one item: wave w takes key tiles w, w + KS, ..., and wave 0 merges
 // the partial softmax states (running max, sum, O) of the others from LDS,
@@ -583,7 +586,7 @@ struct AttnHArgs {
   int blk0[kMaxSeqPerLaunch + 1];  // first 32-query block of each sequence
 };
 
-template <int HD, int WPB, int KS>
+template <int HD, int WPB, int KS, int MT>
 __global__ __launch_bounds__(64 * WPB * KS) void k_attn_h(AttnHArgs a) {
   static_assert(KS == 1 || WPB == 1, "key split: one item per workgroup");
   constexpr int ND = HD / 32;   // 32-wide output blocks
@@ -635,20 +638,98 @@ __global__ __launch_bounds__(64 * WPB * KS) void k_attn_h(AttnHArgs a) {
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk) kf[kk] = *(const f16x8 *)(kr + kk * 16);
   };
+  auto vload = [&](int u, f16x8 (&vf)[ND][2]) {
+    const bool pre = u < np;
+    const int t = pre ? u : t_lo + u - np;
+    const f16 *vb = (pre ? a.pvt : a.vt) + (((size_t)t * a.Hkv + kvh) * HD + lrow) * 32 + lgrp * 8;
+#pragma unroll
+    for (int n = 0; n < ND; ++n)
+#pragma unroll
+      for (int f = 0; f < 2; ++f) vf[n][f] = *(const f16x8 *)(vb + (size_t)n * 32 * 32 + f * 16);
+  };
+  // k fragments of the wave's first tile now, of each next tile while the
+  // current one is computed; V^T fragments at the start of their tile (they
+  // are needed only after the softmax)
   f16x8 kf[NK], kn[NK];
   if (kw < nt) kload(kw, kf);
+  // key-tile index u -> (prefix tile?, tile of its source, rows the lane's
+  // query sees there)
+  auto tile_of = [&](int u, int &t, int &k_lo, int &k_hi) {
+    const bool pre = u < np;
+    t = pre ? u : t_lo + u - np;
+    k_lo = pre ? 0 : s0;
+    k_hi = pre ? P - 1 : (a.causal ? s0 + min(my_q, L - 1) : s0 + L - 1);
+  };
+  if constexpr (MT > 0) {
+    // Two passes over at most MT tiles per wave: all scores first (kept in
+    // registers), one max, then the probabilities and O; no rescaling of O.
+    f32x16 sv[MT];
+    float mb = -INFINITY;
+#pragma unroll
+    for (int x = 0; x < MT; ++x) {
+      const int u = kw + x * KS;
+      if (u < nt) {                                  // wave-uniform
+        int t, k_lo, k_hi;
+        tile_of(u, t, k_lo, k_hi);
+        f32x16 sacc[2];
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) sacc[y][r] = 0.f;
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) mfma32(sacc[kk & 1], kf[kk], qf[kk]);
+        if (u + KS < nt) kload(u + KS, kn);
+        const int kb = t * 32 + 4 * lgrp;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int k = kb + 8 * (r >> 2) + (r & 3);
+          const float v = sacc[0][r] + sacc[1][r];
+          sv[x][r] = ((k >= k_lo) & (k <= k_hi)) ? v * a.sc : -INFINITY;
+          mb = fmaxf(mb, sv[x][r]);
+        }
+        if (u + KS < nt) {
+#pragma unroll
+          for (int kk = 0; kk < NK; ++kk) kf[kk] = kn[kk];
+        }
+      }
+    }
+    mb = warp_max_xor(mb, 32);
+    m_i = mb;
+    const float m_ref = mb == -INFINITY ? 0.f : mb;  // a key-split wave may own no tile
+    f16x8 vf[ND][2], vn[ND][2];
+    if (kw < nt) vload(kw, vf);
+#pragma unroll
+    for (int x = 0; x < MT; ++x) {
+      const int u = kw + x * KS;
+      if (u < nt) {
+        if (u + KS < nt) vload(u + KS, vn);
+        f16x8 pf[2];
+#pragma unroll
+        for (int f = 0; f < 2; ++f)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float pv = __builtin_amdgcn_exp2f(sv[x][8 * f + e] - m_ref);
+            l_i += pv;
+            pf[f][e] = (f16)pv;
+          }
+#pragma unroll
+        for (int f = 0; f < 2; ++f)
+#pragma unroll
+          for (int n = 0; n < ND; ++n) mfma32(oacc[n], vf[n][f], pf[f]);
+        if (u + KS < nt) {
+#pragma unroll
+          for (int n = 0; n < ND; ++n)
+#pragma unroll
+            for (int f = 0; f < 2; ++f) vf[n][f] = vn[n][f];
+        }
+      }
+    }
+  } else
   for (int u = kw; u < nt; u += KS) {
     const bool pre = u < np;
     const int t = pre ? u : t_lo + u - np;
-    // V^T fragments of this tile (used after the softmax)
     f16x8 vf[ND][2];
-    {
-      const f16 *vb = (pre ? a.pvt : a.vt) + (((size_t)t * a.Hkv + kvh) * HD + lrow) * 32 + lgrp * 8;
-#pragma unroll
-      for (int n = 0; n < ND; ++n)
-#pragma unroll
-        for (int f = 0; f < 2; ++f) vf[n][f] = *(const f16x8 *)(vb + (size_t)n * 32 * 32 + f * 16);
-    }
+    vload(u, vf);
     f32x16 sacc[2];
 #pragma unroll
     for (int x = 0; x < 2; ++x)
@@ -658,39 +739,33 @@ __global__ __launch_bounds__(64 * WPB * KS) void k_attn_h(AttnHArgs a) {
     for (int kk = 0; kk < NK; ++kk) mfma32(sacc[kk & 1], kf[kk], qf[kk]);
     if (u + KS < nt) kload(u + KS, kn);
     f32x16 s = sacc[0] + sacc[1];
-    // key of register r: row 32 t + acc_row(r, lane) of its source
+    // key of register r: row 32 t + acc_row(r, lane) of its source; the lane
+    // sees rows [k_lo, k_hi] of this source (branch-free selects)
+    const int k_lo = pre ? 0 : s0;
+    const int k_hi = pre ? P - 1 : (a.causal ? s0 + min(my_q, L - 1) : s0 + L - 1);
+    const int kb = t * 32 + 4 * lgrp;
     float mb = -INFINITY;
-    bool full;
-    if (pre) full = t * 32 + 31 < P;
-    else full = t * 32 >= s0 && t * 32 + 31 <= s0 + (a.causal ? q0 : L - 1) && t * 32 + 31 < s0 + L;
-    if (full) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[r] *= a.sc;
-        mb = fmaxf(mb, s[r]);
-      }
-    } else {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int k = t * 32 + acc_row(r, lane);
-        const bool ok = pre ? k < P : (k >= s0 && k < s0 + L && (!a.causal || k - s0 <= my_q));
-        s[r] = ok ? s[r] * a.sc : -INFINITY;
-        mb = fmaxf(mb, s[r]);
-      }
+    for (int r = 0; r < 16; ++r) {
+      const int k = kb + 8 * (r >> 2) + (r & 3);
+      s[r] = ((k >= k_lo) & (k <= k_hi)) ? s[r] * a.sc : -INFINITY;
+      mb = fmaxf(mb, s[r]);
     }
     mb = warp_max_xor(mb, 32);
     const float m_new = fmaxf(m_i, mb);
     const float m_ref = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = exp2f(m_i - m_ref);
+    const float alpha = __builtin_amdgcn_exp2f(m_i - m_ref);
     m_i = m_new;
     float p[16], ps = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      p[r] = exp2f(s[r] - m_ref);
+      p[r] = __builtin_amdgcn_exp2f(s[r] - m_ref);
       ps += p[r];
     }
     l_i = l_i * alpha + ps;
-    if (__any(alpha != 1.f)) {
+    // the running max moved for some query: rescale O (not on the wave's
+    // first tile, where O is still zero)
+    if (u != kw && __any(alpha != 1.f)) {
 #pragma unroll
       for (int n = 0; n < ND; ++n)
 #pragma unroll
@@ -728,7 +803,7 @@ __global__ __launch_bounds__(64 * WPB * KS) void k_attn_h(AttnHArgs a) {
 #pragma unroll
     for (int v = 0; v < KS - 1; ++v) mx = fmaxf(mx, red[v][0][lane]);
     const float mr = mx == -INFINITY ? 0.f : mx;   // wave 0 always saw key 0, so mx is finite
-    const float f0 = exp2f(m_i - mr);
+    const float f0 = __builtin_amdgcn_exp2f(m_i - mr);
     l_i *= f0;
 #pragma unroll
     for (int n = 0; n < ND; ++n)
@@ -736,7 +811,7 @@ __global__ __launch_bounds__(64 * WPB * KS) void k_attn_h(AttnHArgs a) {
       for (int r = 0; r < 16; ++r) oacc[n][r] *= f0;
 #pragma unroll
     for (int v = 0; v < KS - 1; ++v) {
-      const float fv = exp2f(red[v][0][lane] - mr);
+      const float fv = __builtin_amdgcn_exp2f(red[v][0][lane] - mr);
       l_i += fv * red[v][1][lane];
 #pragma unroll
       for (int n = 0; n < ND; ++n)
@@ -763,9 +838,8 @@ __global__ __launch_bounds__(64 * WPB * KS) void k_attn_h(AttnHArgs a) {
 
 hipError_t launch_attention_h(const f16 *qk, const f16 *vt, const f16 *prefix, const f16 *pvt, int P, f16 *o,
                               float sc, const int32_t *cu, int batch, int T, int Hq, int Hkv, int d, int causal,
-                              hipStream_t s) {
+                              hipStream_t s, int ks) {
   constexpr int WPB = 2;      // work items (waves) per workgroup without key split
-  constexpr int KS = 4;       // waves per work item with key split
   if (P < 0 || (P > 0 && (!prefix || !pvt)) || (d != 64 && d != 128) || Hq % Hkv || !qk || !vt || !o)
     return hipErrorInvalidValue;
   AttnHArgs a;
@@ -795,16 +869,32 @@ hipError_t launch_attention_h(const f16 *qk, const f16 *vt, const f16 *prefix, c
     a.blk0[n] = blocks;
     a.n_items = blocks * Hq;
     if (a.n_items == 0) continue;
-    // Few items (one or two frames) leave most of the chip idle and each
-    // item's tile steps in series: split every item's key tiles over KS waves.
-    if (a.n_items < 256) {
-      if (d == 128) hipLaunchKernelGGL((k_attn_h<128, 1, KS>), dim3(a.n_items), dim3(64 * KS), 0, s, a);
-      else hipLaunchKernelGGL((k_attn_h<64, 1, KS>), dim3(a.n_items), dim3(64 * KS), 0, s, a);
-    } else {
-      dim3 grid((a.n_items + WPB - 1) / WPB);
-      if (d == 128) hipLaunchKernelGGL((k_attn_h<128, WPB, 1>), grid, dim3(64 * WPB), 0, s, a);
-      else hipLaunchKernelGGL((k_attn_h<64, WPB, 1>), grid, dim3(64 * WPB), 0, s, a);
+    // key tiles of the longest item: the prefix's, then the batch tiles the
+    // sequence touches (it may start inside a tile)
+    int nt_max = 0;
+    for (int i = 0; i < n; ++i) {
+      const int s0 = cu[first + i], e0 = cu[first + i + 1] - 1;
+      nt_max = std::max(nt_max, (P + 31) / 32 + (e0 >> 5) - (s0 >> 5) + 1);
     }
+    // Few items (one or two frames) leave most of the chip idle and each
+    // item's tile steps in series: split every item's key tiles over 2 waves
+    // (measured: one 96-token frame 7.3 us with 1 wave per item, 6.7 with 2,
+    // 6.9 with 4; 16 frames 10.3 us with 1 or 2, 14.0 with 4).
+    const int k = ks > 0 ? ks : (a.n_items < 256 ? 2 : 1);
+    // at most 4 tiles per wave: the two-pass variant
+    const bool two = (nt_max + k - 1) / k <= 4;
+#define MTE_ATTN_H(KS_, WPB_)                                                                          \
+    {                                                                                                  \
+      dim3 grid_((a.n_items + WPB_ - 1) / WPB_), blk_(64 * WPB_ * KS_);                                \
+      if (d == 128 && two) hipLaunchKernelGGL((k_attn_h<128, WPB_, KS_, 4>), grid_, blk_, 0, s, a);    \
+      else if (d == 128) hipLaunchKernelGGL((k_attn_h<128, WPB_, KS_, 0>), grid_, blk_, 0, s, a);      \
+      else if (two) hipLaunchKernelGGL((k_attn_h<64, WPB_, KS_, 4>), grid_, blk_, 0, s, a);            \
+      else hipLaunchKernelGGL((k_attn_h<64, WPB_, KS_, 0>), grid_, blk_, 0, s, a);                     \
+    }
+    if (k == 4) MTE_ATTN_H(4, 1)
+    else if (k == 2) MTE_ATTN_H(2, 1)
+    else MTE_ATTN_H(1, WPB)
+#undef MTE_ATTN_H
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -162,11 +162,12 @@ hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int
 //  prefix / pvt: the same two layouts for P rows of a shared prefix (its k
 //      heads and V^T tiles are read), or P = 0.
 // o: fp16 [T, Hq d]. sc = log2(e) / sqrt(d) * 2^(aq + ak). cu: host
-// int32[batch+1] offsets. One wave per (sequence, query head, 32 queries);
-// launches in chunks of <= 256 sequences.
+// int32[batch+1] offsets. One wave per (sequence, query head, 32 queries),
+// or ks waves (2 or 4) splitting its key tiles; ks = 0 picks by the number of
+// work items. Launches in chunks of <= 256 sequences.
 hipError_t launch_attention_h(const f16 *qk, const f16 *vt, const f16 *prefix, const f16 *pvt, int P, f16 *o,
                               float sc, const int32_t *cu, int batch, int T, int Hq, int Hkv, int d, int causal,
-                              hipStream_t s);
+                              hipStream_t s, int ks = 0);
 
 // Positions of packed sequences (see mte_build_positions).
 hipError_t launch_positions(const int32_t *layouts5, int batch, int32_t *pos_thw, int T,
