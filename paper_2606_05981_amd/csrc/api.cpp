@@ -563,8 +563,8 @@ hipError_t run_layers(mte_encoder *e, const Work &wk, float *h, const int32_t *c
                                    use ? (const f16 *)(lc + cq) : nullptr, use ? pre->P : 0, (f16 *)wk.attn,
                                    W.att_sc, cu, batch, T, Hq, Hkv, d, 1, s));
       else
-        MTE_TRY(launch_attention(mode, wk.qkv, use ? (const float *)lc : nullptr, use ? pre->P : 0, wk.attn,
-                                 W.o_pre, cu, batch, Hq, Hkv, d, s));
+        MTE_TRY(launch_attention(wk.qkv, use ? (const float *)lc : nullptr, use ? pre->P : 0, (float *)wk.attn,
+                                 cu, batch, Hq, Hkv, d, s));
     }
     {
       Timer t(e, 2, s);

@@ -5,11 +5,11 @@
 // with k, v taken from kv head h / (Hq / Hkv) and j ranging over the same
 // sequence only (q and k arrive normalised and rotated).
 //
-// Two kernels. k_attn_h (at the end of this file) is the decoder's with bf16
-// storage: fp16 operands that the QKV projection already wrote in the
-// matrix-core layout, one wave per work item and no LDS. k_attn below serves
-// fp32 storage (fp32 operands) and the vision tower (fp32 q/k/v split into
-// bf16 hi + lo for the scores):
+// Three kernels. With bf16 storage (decoder and vision tower) q, k and v
+// arrive as fp16 operands that the QKV projection already wrote in the
+// matrix-core layout: k_attn_s stages a workgroup's key range in LDS when it
+// fits, k_attn_h streams it from global memory (both at the end of this
+// file). k_attn below serves fp32 storage, on the fp32 matrix cores:
 //
 // One workgroup (4 waves) serves one kv head, one tile of query rows of one
 // sequence and the query heads of that kv head assigned to it; every wave
@@ -22,19 +22,9 @@
 //   exchange (lane ^ 32)
 //   O^T += V^T P^T  (32x32 MFMA; again query l%32 per lane, so the
 //   rescaling of O by the running-max correction is a per-lane scalar).
-//
-// q, k, v arrive in fp32 (the packed QKV projection). MODE_F32 multiplies
-// them on the fp32 matrix cores and writes fp32. MODE_F16 splits every
-// operand x into bf16 hi + lo (lo = bf16(x - hi)) and forms each product
-// from three bf16 MFMAs, hi*hi + lo*hi + hi*lo (the lo*lo term is below fp32
-// accumulation noise), and writes o times a power-of-two pre-scale as fp16,
-// the operand type of the output projection. With PVH (fp16 PV, MODE_F16
-// only) the scores are formed the same way but P and V enter one fp16 MFMA:
-// P in [0, 1] and V times the output pre-scale (a static bound keeps it, and
-// hence o, in fp16 range) are rounded once to fp16, as the projections'
-// activations are. The sequence table (offsets, first tile of each
-// sequence) is passed by value in the kernel arguments, so nothing is read
-// back to the host.
+// q, k, v arrive as fp32 rows of the packed QKV projection; o is written in
+// fp32. The sequence table (offsets, first tile of each sequence) is passed
+// by value in the kernel arguments, so nothing is read back to the host.
 #include <algorithm>
 #include <type_traits>
 
@@ -49,8 +39,7 @@ struct AttnArgs {
   const float *qkv;   // [T, ld_qkv] fp32
   const float *pre;   // [P, ld_qkv] fp32: keys / values of a shared prefix every sequence sees, or null
   int P;              // prefix length (0: none)
-  char *o;
-  float o_scale;   // output multiplier (MODE_F16)
+  float *o;
   int ld_qkv;      // floats per token row of qkv
   int Hq, Hkv, rep;
   int wph;         // waves per query head (query rows per workgroup = 32 * wph)
@@ -68,16 +57,6 @@ __device__ __forceinline__ int kswz(int r, int c) {
   else return c ^ ((r ^ (r >> 3)) & 7);
 }
 
-// Splits EC fp32 values into NP planes of element type T (NP = 1: plain).
-template <typename T, int NP, int EC>
-__device__ __forceinline__ void split_vals(const float *x, T (&out)[NP][EC]) {
-#pragma unroll
-  for (int e = 0; e < EC; ++e) {
-    T hi = from_f32<T>(x[e]);
-    out[0][e] = hi;
-    if constexpr (NP == 2) out[1][e] = from_f32<T>(x[e] - to_f32(hi));
-  }
-}
 
 // Position of key k (0..31) of a tile in a row of the transposed V stage:
 // the P fragment f of lane group g holds the probabilities of keys
@@ -94,35 +73,25 @@ __device__ __forceinline__ int vt_pos(int k) {
 // the next one in flight in registers (any length); NB > 1 loads all of a
 // workgroup's tiles up front (sequences of at most NB * 32 tokens), so the
 // whole key/value range costs one global-load latency and one barrier.
-template <int MODE, int HD, int NB, bool PVH>
+template <int HD, int NB>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
-  static_assert(!PVH || MODE == MODE_F16, "fp16 PV with fp16 operands only");
-  // q, k: type T in NP planes; v and p: type TV in NPV planes
-  typedef typename std::conditional<MODE == MODE_F32, float, bf16>::type T;
-  typedef typename std::conditional<PVH, f16, T>::type TV;
-  constexpr int NP = (MODE == MODE_F16) ? 2 : 1;   // bf16 planes of q and k
-  constexpr int NPV = PVH ? 1 : NP;                // planes of v and p
   constexpr int KV = 32;
-  constexpr int EC = 16 / (int)sizeof(T);        // elements per 16-byte chunk
+  constexpr int EC = 4;                          // fp32 elements per 16-byte chunk
   constexpr int NCH = HD / EC;                   // chunks per head row
-  constexpr int EPF = Frag<TV>::kElems;          // values per P / V fragment
+  constexpr int EPF = Frag<float>::kElems;       // values per P / V fragment
   constexpr int NFP = 16 / EPF;                  // P fragments per 32-kv tile
-  constexpr int VTP = KV + 16 / (int)sizeof(TV); // V^T row pitch: 16-byte aligned, conflict-free
+  constexpr int VTP = KV + 4;                    // V^T row pitch: 16-byte aligned, conflict-free
   constexpr int ND = HD / 32;                    // 32-wide d blocks
-  static_assert(EC == Frag<T>::kElems && (int)sizeof(T) == (int)sizeof(TV), "chunk = fragment");
-  typedef typename Frag<T>::type frag_t;
-  typedef typename Frag<TV>::type vfrag_t;
-  // PVH: V is staged times the output pre-scale, so o comes out scaled
-  const float v_scale = PVH ? a.o_scale : 1.f;
+  typedef f32x4 frag_t;
 
-  constexpr int K_BYTES = NP * KV * NCH * 16;
-  constexpr int V_BYTES = NPV * HD * VTP * (int)sizeof(TV);
+  constexpr int K_BYTES = KV * NCH * 16;
+  constexpr int V_BYTES = HD * VTP * 4;
   constexpr int ST_BYTES = K_BYTES + V_BYTES;             // one staged tile
   constexpr int SMEM = NB * ST_BYTES;
   __shared__ __attribute__((aligned(16))) char smem[SMEM];
-  // tile b: K [NP][KV * NCH] at smem + b * ST_BYTES, V^T [NPV][HD * VTP] after it
+  // tile b: K [KV * NCH] at smem + b * ST_BYTES, V^T [HD * VTP] after it
   auto sK_of = [&](int b) { return (u32x4 *)(smem + b * ST_BYTES); };
-  auto sVt_of = [&](int b) { return (TV *)(smem + b * ST_BYTES + K_BYTES); };
+  auto sVt_of = [&](int b) { return (float *)(smem + b * ST_BYTES + K_BYTES); };
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int lrow = lane & 31, lgrp = lane >> 5;
@@ -162,24 +131,12 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   // past the sequence read its last row (their outputs are not stored).
   // Loaded after the first key/value tiles' loads are issued, so that the
   // two global-load round trips overlap.
-  frag_t qf[NP][NCH / 2];
+  frag_t qf[NCH / 2];
   auto load_q = [&]() {
     const int qi = min(qw + lrow, L - 1);
 #pragma unroll
-    for (int kk = 0; kk < NCH / 2; ++kk) {
-      float x[EC];
-#pragma unroll
-      for (int e = 0; e < EC; e += 4) {
-        const f32x4 v = *(const f32x4 *)(a.qkv + base + (size_t)qi * ld + head * HD + (kk * 2 + lgrp) * EC + e);
-        x[e] = v[0]; x[e + 1] = v[1]; x[e + 2] = v[2]; x[e + 3] = v[3];
-      }
-      T sp[NP][EC];
-      split_vals<T, NP, EC>(x, sp);
-#pragma unroll
-      for (int p = 0; p < NP; ++p)
-#pragma unroll
-        for (int e = 0; e < EC; ++e) qf[p][kk][e] = sp[p][e];
-    }
+    for (int kk = 0; kk < NCH / 2; ++kk)
+      qf[kk] = *(const f32x4 *)(a.qkv + base + (size_t)qi * ld + head * HD + (kk * 2 + lgrp) * EC);
   };
   // Scores are kept in log2 units: s * log2(e) / sqrt(d).
   const float sc = 1.4426950408889634f * rsqrtf((float)HD);
@@ -267,75 +224,39 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     }
   };
   // Register slot b -> LDS tile sKb / sVtb.
-  auto lstore = [&](int b, u32x4 *sKb, TV *sVtb) {
+  auto lstore = [&](int b, u32x4 *sKb, float *sVtb) {
 #pragma unroll
     for (int t = 0; t < KCH; ++t) {
       const int idx = tid + t * 256, r = idx / NCH, c = idx % NCH;
-      T sp[NP][EC];
-      split_vals<T, NP, EC>(kx[b][t], sp);
-#pragma unroll
-      for (int p = 0; p < NP; ++p) {
-        u32x4 w;
-        __builtin_memcpy(&w, sp[p], 16);
-        sKb[p * KV * NCH + r * NCH + kswz<NCH>(r, c)] = w;
-      }
+      u32x4 w;
+      __builtin_memcpy(&w, kx[b][t], 16);
+      sKb[r * NCH + kswz<NCH>(r, c)] = w;
     }
 #pragma unroll
     for (int t = 0; t < VCH; ++t) {
       const int idx = tid + t * 256, d = idx % HD, v = idx / HD;
-      TV vs[NPV][EC];
-      if constexpr (PVH) {
-#pragma unroll
-        for (int e = 0; e < EC; ++e) vs[0][e] = from_f32<TV>(vx[b][t][e] * v_scale);
-      } else {
-        split_vals<TV, NPV, EC>(vx[b][t], vs);
-      }
-#pragma unroll
-      for (int p = 0; p < NPV; ++p) {
-        TV *row = sVtb + p * HD * VTP + d * VTP;
-        // keys v*EC .. v*EC+EC-1 land in runs of 4 consecutive positions
-#pragma unroll
-        for (int e = 0; e < EC; e += 4) {
-          const int pos = vt_pos<EPF>(v * EC + e);
-          if constexpr (sizeof(TV) == 2) {
-            u32x2 w;
-            __builtin_memcpy(&w, &vs[p][e], 8);
-            *(u32x2 *)(row + pos) = w;
-          } else {
-            u32x4 w;
-            __builtin_memcpy(&w, &vs[p][e], 16);
-            *(u32x4 *)(row + pos) = w;
-          }
-        }
-      }
+      // keys v*EC .. v*EC+3 land in a run of 4 consecutive positions
+      u32x4 w;
+      __builtin_memcpy(&w, vx[b][t], 16);
+      *(u32x4 *)(sVtb + d * VTP + vt_pos<EPF>(v * EC)) = w;
     }
   };
   // One key/value tile for this wave: scores, online softmax, O update.
-  auto compute = [&](int kv0, const u32x4 *sK, const TV *sVt) {
+  auto compute = [&](int kv0, const u32x4 *sK, const float *sVt) {
     if (!(qw < L && kv0 <= (a.causal ? P + wave_last : P + L - 1))) return;
-    // Independent accumulators (one per split product, or per k parity
-    // for fp32) so consecutive MFMAs do not wait on each other's results.
-    constexpr int NS = (NP == 2) ? 3 : 2;
-    f32x16 sacc[NS];
+    // Two accumulators (by k parity) so consecutive MFMAs do not wait on
+    // each other's results.
+    f32x16 sacc[2];
 #pragma unroll
-    for (int u = 0; u < NS; ++u)
+    for (int u = 0; u < 2; ++u)
 #pragma unroll
       for (int r = 0; r < 16; ++r) sacc[u][r] = 0.f;
 #pragma unroll
     for (int kk = 0; kk < NCH / 2; ++kk) {
       const int slot = lrow * NCH + kswz<NCH>(lrow, kk * 2 + lgrp);
-      const frag_t k0 = __builtin_bit_cast(frag_t, sK[slot]);
-      if constexpr (NP == 2) {
-        const frag_t k1 = __builtin_bit_cast(frag_t, sK[KV * NCH + slot]);
-        mfma32(sacc[0], k0, qf[0][kk]);
-        mfma32(sacc[1], k1, qf[0][kk]);
-        mfma32(sacc[2], k0, qf[1][kk]);
-      } else {
-        mfma32(sacc[kk & 1], k0, qf[0][kk]);
-      }
+      mfma32(sacc[kk & 1], __builtin_bit_cast(frag_t, sK[slot]), qf[kk]);
     }
     f32x16 s = sacc[0] + sacc[1];
-    if constexpr (NS == 3) s += sacc[2];
     float mb = -INFINITY;
     // a tile every query of the wave sees in full needs no mask
     const bool full = kv0 + KV <= P + L && (!a.causal || kv0 + KV - 1 <= P + qw);
@@ -376,38 +297,15 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         for (int r = 0; r < 16; ++r) oacc[n][r] *= alpha;
     }
     // P fragments: element e of fragment f is P value i = EPF*f + e.
-    vfrag_t pf[NPV][NFP];
-#pragma unroll
-    for (int f = 0; f < NFP; ++f) {
-      TV sp[NPV][EPF];
-      if constexpr (PVH) {
-#pragma unroll
-        for (int e = 0; e < EPF; ++e) sp[0][e] = from_f32<TV>(p[EPF * f + e]);
-      } else {
-        split_vals<TV, NPV, EPF>(p + EPF * f, sp);
-      }
-#pragma unroll
-      for (int q = 0; q < NPV; ++q)
-#pragma unroll
-        for (int e = 0; e < EPF; ++e) pf[q][f][e] = sp[q][e];
-    }
     // Consecutive MFMAs go to the ND different output blocks.
 #pragma unroll
     for (int f = 0; f < NFP; ++f) {
-      vfrag_t vf[ND][NPV];
+      const frag_t pf = {p[EPF * f], p[EPF * f + 1], p[EPF * f + 2], p[EPF * f + 3]};
+      frag_t vf[ND];
 #pragma unroll
-      for (int n = 0; n < ND; ++n)
+      for (int n = 0; n < ND; ++n) vf[n] = *(const frag_t *)(sVt + (n * 32 + lrow) * VTP + (2 * f + lgrp) * EPF);
 #pragma unroll
-        for (int q = 0; q < NPV; ++q)
-          vf[n][q] = *(const vfrag_t *)(sVt + q * HD * VTP + (n * 32 + lrow) * VTP + (2 * f + lgrp) * EPF);
-#pragma unroll
-      for (int n = 0; n < ND; ++n) mfma32(oacc[n], vf[n][0], pf[0][f]);
-      if constexpr (NPV == 2) {
-#pragma unroll
-        for (int n = 0; n < ND; ++n) mfma32(oacc[n], vf[n][1], pf[0][f]);
-#pragma unroll
-        for (int n = 0; n < ND; ++n) mfma32(oacc[n], vf[n][0], pf[1][f]);
-      }
+      for (int n = 0; n < ND; ++n) mfma32(oacc[n], vf[n], pf);
     }
   };
   if constexpr (NB == 1) {
@@ -468,46 +366,34 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 
   // Output. oacc[n] holds rows d = 32 n + acc_row(r, lane) of O^T for the
   // lane's query: accumulator registers 4c..4c+3 are four consecutive d, so
-  // each lane writes them as one 8-byte (fp16) or 16-byte (fp32) store into
-  // its query's row, and the two lane groups fill 16 (32) contiguous bytes.
-  const float lt = l_i + __shfl_xor(l_i, 32, kWave);
-  // MODE_F16: o times its pre-scale (with PVH the pre-scale came with V)
-  const float inv = ((MODE == MODE_F32 || PVH) ? 1.f : a.o_scale) / lt;
+  // each lane writes them as one 16-byte store into its query's row, and the
+  // two lane groups fill 32 contiguous bytes.
+  const float inv = 1.f / (l_i + __shfl_xor(l_i, 32, kWave));
   if (my_q < L && !helper) {
     const size_t orow = ((size_t)(s0 + my_q) * a.Hq + head) * HD + 4 * lgrp;
 #pragma unroll
     for (int n = 0; n < ND; ++n)
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        const int d = n * 32 + 8 * c;
-        if constexpr (MODE == MODE_F32) {
-          f32x4 y;
+        f32x4 y;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) y[e] = oacc[n][4 * c + e] * inv;
-          *(f32x4 *)((float *)a.o + orow + d) = y;
-        } else {
-          f16x4 h;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) h[e] = (f16)(oacc[n][4 * c + e] * inv);
-          *(f16x4 *)((f16 *)a.o + orow + d) = h;
-        }
+        for (int e = 0; e < 4; ++e) y[e] = oacc[n][4 * c + e] * inv;
+        *(f32x4 *)(a.o + orow + n * 32 + 8 * c) = y;
       }
   }
 }
 
-hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int P, void *o, float out_scale,
-                            const int32_t *cu, int batch, int Hq, int Hkv, int d, hipStream_t s, int causal,
-                            int pv_f16) {
+hipError_t launch_attention(const float *qkv, const float *prefix, int P, float *o, const int32_t *cu, int batch,
+                            int Hq, int Hkv, int d, hipStream_t s, int causal) {
   const int rep = Hq / Hkv;
-  if (P < 0 || (P > 0 && !prefix)) return hipErrorInvalidValue;
+  if (P < 0 || (P > 0 && !prefix) || (d != 64 && d != 128) || Hq % Hkv) return hipErrorInvalidValue;
   AttnArgs a;
   a.causal = causal ? 1 : 0;
   a.qkv = qkv;
   a.pre = prefix;
   a.P = P;
   a.ld_qkv = (Hq + 2 * Hkv) * d;
-  a.o = (char *)o;
-  a.o_scale = out_scale;
+  a.o = o;
   a.Hq = Hq;
   a.Hkv = Hkv;
   a.rep = rep;
@@ -532,17 +418,10 @@ hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int
     // Sequences of at most 128 tokens: every workgroup stages all of its
     // (at most 4) key/value tiles at once.
     const bool all = P + max_len <= 4 * 32;
-#define MTE_ATTN(M_, D_, H_)                                                             \
-    if (all) hipLaunchKernelGGL((k_attn<M_, D_, 4, H_>), grid, dim3(256), 0, s, a);      \
-    else hipLaunchKernelGGL((k_attn<M_, D_, 1, H_>), grid, dim3(256), 0, s, a);
-    if (mode == MODE_F16 && pv_f16) {
-      if (d == 128) { MTE_ATTN(MODE_F16, 128, true) } else { MTE_ATTN(MODE_F16, 64, true) }
-    } else if (mode == MODE_F16) {
-      if (d == 128) { MTE_ATTN(MODE_F16, 128, false) } else { MTE_ATTN(MODE_F16, 64, false) }
-    } else {
-      if (d == 128) { MTE_ATTN(MODE_F32, 128, false) } else { MTE_ATTN(MODE_F32, 64, false) }
-    }
-#undef MTE_ATTN
+    if (d == 128 && all) hipLaunchKernelGGL((k_attn<128, 4>), grid, dim3(256), 0, s, a);
+    else if (d == 128) hipLaunchKernelGGL((k_attn<128, 1>), grid, dim3(256), 0, s, a);
+    else if (all) hipLaunchKernelGGL((k_attn<64, 4>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((k_attn<64, 1>), grid, dim3(256), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -836,12 +715,307 @@ __global__ __launch_bounds__(64 * WPB * KS) void k_attn_h(AttnHArgs a) {
   }
 }
 
+// Staged variant of k_attn_h for key ranges that fit in LDS. A workgroup
+// serves one kv head and a chunk of `qbw` 32-query blocks of one sequence,
+// one wave per (query head of the group, query block). All waves first copy
+// every key tile the chunk sees (its k rows and V^T rows for this kv head)
+// from global memory straight into LDS (global_load_lds, 16 bytes a lane,
+// all copies in flight at once), wait for them once, and then compute from
+// LDS only: the chain of dependent global loads of the register-streaming
+// kernel becomes one load latency. The LDS cap (64 KB: two workgroups a CU)
+// holds at most 4 tiles of head size 128 and 8 of 64, so the softmax is
+// always the two-pass form: every tile's scores in registers, one maximum,
+// then the probabilities and O, in straight-line code per tile count. Same
+// arithmetic as k_attn_h (fp16 operands, fp32 scores and softmax in base 2,
+// masks as selects) on the same global 32-token key tiles.
+// LDS per tile: k rows [32][HD] then V^T rows [HD][32], 16-byte chunks
+// placed by an XOR of the row so that the 16 lanes of a quarter-wave that
+// read one chunk column of 16 rows hit 16 distinct 16-byte bank groups.
+struct AttnSArgs {
+  const f16 *qk, *vt, *pqk, *pvt;
+  f16 *o;
+  float sc;
+  int ldq, T, P;
+  int Hq, Hkv, rep;
+  int n_seq, causal;
+  int qbw;             // 32-query blocks per workgroup
+  int cu[kMaxSeqPerLaunch + 1];   // absolute token offsets
+  int ch0[kMaxSeqPerLaunch + 1];  // first query chunk of each sequence
+};
+
+// slot of 16-byte chunk c of k row r (HD / 8 chunks a row), and of chunk c
+// of V^T row r (4 chunks a row); each is its own inverse
+template <int HD>
+__device__ __forceinline__ int kslot(int r, int c) {
+  if constexpr (HD == 128) return c ^ (r & 15);
+  else return c ^ ((r >> 1) & 7);
+}
+__device__ __forceinline__ int vslot(int r, int c) { return c ^ ((r >> 2) & 3); }
+
+constexpr int kAttnSMaxWaves = 8;
+constexpr int kAttnSCap = 64 * 1024;   // LDS bytes per workgroup: two workgroups a CU
+
+// Where a wave's staged tiles come from and which keys its lane's query sees.
+struct STile {
+  const char *lb;      // LDS base
+  int np, t_lo, P, s0, kq_hi;
+  float sc;
+  int lgrp;
+};
+
+// All N staged tiles of one wave, two passes: the scores of every tile (kept
+// in registers), one maximum per query, then the probabilities and O. No
+// rescaling, and no branch between tiles, so the loads and MFMAs of
+// different tiles overlap.
+template <int HD, int N>
+__device__ __forceinline__ void s_tiles(const STile &st, const uint32_t (&ka)[HD / 16],
+                                        const uint32_t (&va)[HD / 32][2], const f16x8 (&qf)[HD / 16],
+                                        f32x16 (&oacc)[HD / 32], float &l_i) {
+  constexpr int ND = HD / 32, NK = HD / 16, TB = 128 * HD;
+  f32x16 sv[N];
+  float mb = -INFINITY;
+#pragma unroll
+  for (int x = 0; x < N; ++x) {
+    const char *tb = st.lb + x * TB;
+    f16x8 kf[NK];
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) kf[kk] = *(const f16x8 *)(tb + ka[kk]);
+    f32x16 sacc[2];
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[y][r] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) mfma32(sacc[kk & 1], kf[kk], qf[kk]);
+    const bool pre = x < st.np;
+    const int t = pre ? x : st.t_lo + x - st.np;
+    const int k_lo = pre ? 0 : st.s0, k_hi = pre ? st.P - 1 : st.kq_hi;
+    const int kb = t * 32 + 4 * st.lgrp;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int k = kb + 8 * (r >> 2) + (r & 3);
+      const float v = sacc[0][r] + sacc[1][r];
+      sv[x][r] = ((k >= k_lo) & (k <= k_hi)) ? v * st.sc : -INFINITY;
+      mb = fmaxf(mb, sv[x][r]);
+    }
+  }
+  mb = warp_max_xor(mb, 32);                   // finite: every query sees its own key
+#pragma unroll
+  for (int x = 0; x < N; ++x) {
+    const char *tb = st.lb + x * TB;
+    f16x8 vf[ND][2];
+#pragma unroll
+    for (int n = 0; n < ND; ++n)
+#pragma unroll
+      for (int f = 0; f < 2; ++f) vf[n][f] = *(const f16x8 *)(tb + va[n][f]);
+    f16x8 pf[2];
+#pragma unroll
+    for (int f = 0; f < 2; ++f)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float p = __builtin_amdgcn_exp2f(sv[x][8 * f + e] - mb);
+        l_i += p;
+        pf[f][e] = (f16)p;
+      }
+#pragma unroll
+    for (int f = 0; f < 2; ++f)
+#pragma unroll
+      for (int n = 0; n < ND; ++n) mfma32(oacc[n], vf[n][f], pf[f]);
+  }
+}
+
+template <int HD>
+__global__ __launch_bounds__(64 * kAttnSMaxWaves) void k_attn_s(AttnSArgs a) {
+  constexpr int ND = HD / 32, NK = HD / 16, NCH = HD / 8;
+  constexpr int MT = kAttnSCap / (128 * HD);   // tiles that fit the LDS cap
+  constexpr int KB = 64 * HD;                  // bytes of k rows (and of V^T rows) per tile
+  constexpr int TB = 2 * KB;                   // bytes per staged tile
+  constexpr int GPT = TB / 1024;               // 64-lane copies per tile
+  extern __shared__ u32x4 lds[];
+  const int lane = threadIdx.x & 63, lrow = lane & 31, lgrp = lane >> 5;
+  const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int nwv = (int)(blockDim.x >> 6);
+  const int chunk = (int)blockIdx.x / a.Hkv, kvh = (int)blockIdx.x % a.Hkv;
+  int lo = 0, hi = a.n_seq - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.ch0[mid] <= chunk) lo = mid; else hi = mid - 1;
+  }
+  const int s0 = a.cu[lo], L = a.cu[lo + 1] - s0;
+  const int qc0 = (chunk - a.ch0[lo]) * a.qbw * 32;   // first query of the chunk
+  const int P = a.P, np = (P + 31) >> 5;
+  const int t_lo = s0 >> 5;
+  // key tiles of the chunk: the prefix's, then the batch tiles up to the last
+  // key its last query sees
+  const int kend_c = a.causal ? min(qc0 + a.qbw * 32, L) - 1 : L - 1;
+  const int nt = np + ((s0 + kend_c) >> 5) - t_lo + 1;
+
+  // this wave's query head and 32 queries
+  const int head = kvh * a.rep + wv % a.rep;
+  const int q0 = qc0 + (wv / a.rep) * 32;
+  const bool live = q0 < L;                    // wave-uniform
+  const int my_q = q0 + lrow;
+  f16x8 qf[NK];
+  if (live) {
+    const f16 *qr = a.qk + (size_t)(s0 + min(my_q, L - 1)) * a.ldq + head * HD + lgrp * 8;
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) qf[kk] = *(const f16x8 *)(qr + kk * 16);
+  }
+  // copies: wave w takes copies w, w + nwv, ... of the nt * GPT
+  const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
+  const uint32_t kcol = (uint32_t)((a.Hq + kvh) * HD) * 2u;
+  for (int j = wv, cnt = 1; j < nt * GPT; j += nwv, ++cnt) {
+    if ((cnt & 31) == 0) wait_vm<32>();        // at most 63 loads in flight
+    const int u = j / GPT, g = j % GPT;
+    const bool pre = u < np;
+    const int t = pre ? u : t_lo + u - np;
+    const uint32_t dst = lds0 + (uint32_t)(u * TB + g * 1024);
+    if (g < GPT / 2) {
+      const int x = g * 64 + lane, r = x / NCH, c = kslot<HD>(r, x % NCH);
+      const int row = pre ? min(u * 32 + r, P - 1) : min(t * 32 + r, a.T - 1);
+      dma16(pre ? a.pqk : a.qk, (uint32_t)row * (uint32_t)a.ldq * 2u + kcol + (uint32_t)c * 16u, dst);
+    } else {
+      const int x = (g - GPT / 2) * 64 + lane, r = x >> 2, c = vslot(r, x & 3);
+      dma16(pre ? a.pvt : a.vt, (uint32_t)(((t * a.Hkv + kvh) * HD + r) * 64 + c * 16), dst);
+    }
+  }
+  wait_vm<0>();
+  __syncthreads();
+  if (!live) return;
+
+  const char *lb = (const char *)lds;
+  uint32_t ka[NK], va[ND][2];
+#pragma unroll
+  for (int kk = 0; kk < NK; ++kk) ka[kk] = (uint32_t)(lrow * NCH + kslot<HD>(lrow, 2 * kk + lgrp)) * 16u;
+#pragma unroll
+  for (int n = 0; n < ND; ++n)
+#pragma unroll
+    for (int f = 0; f < 2; ++f) {
+      const int r = n * 32 + lrow;
+      va[n][f] = (uint32_t)KB + (uint32_t)(r * 4 + vslot(r, 2 * f + lgrp)) * 16u;
+    }
+  // tiles this wave sees, and the keys its lane's query sees in each source
+  const int kend = a.causal ? min(q0 + 31, L - 1) : L - 1;
+  const int ntw = np + ((s0 + kend) >> 5) - t_lo + 1;
+  const int kq_hi = a.causal ? s0 + min(my_q, L - 1) : s0 + L - 1;
+  const STile st{lb, np, t_lo, P, s0, kq_hi, a.sc, lgrp};
+  f32x16 oacc[ND];
+#pragma unroll
+  for (int n = 0; n < ND; ++n)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[n][r] = 0.f;
+  float l_i = 0.f;
+  // straight-line code for the wave's tile count (1 .. MT: the host checks
+  // that every sequence's tiles fit)
+  switch (ntw) {
+#define MTE_S_CASE(N_) \
+  case N_:             \
+    if constexpr (N_ <= MT) s_tiles<HD, N_>(st, ka, va, qf, oacc, l_i); \
+    break;
+    MTE_S_CASE(1) MTE_S_CASE(2) MTE_S_CASE(3) MTE_S_CASE(4)
+    MTE_S_CASE(5) MTE_S_CASE(6) MTE_S_CASE(7) MTE_S_CASE(8)
+#undef MTE_S_CASE
+    default: break;
+  }
+  const float inv = 1.f / (l_i + __shfl_xor(l_i, 32, kWave));
+  if (my_q < L) {
+    f16 *orow = a.o + ((size_t)(s0 + my_q) * a.Hq + head) * HD + 4 * lgrp;
+#pragma unroll
+    for (int n = 0; n < ND; ++n)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        f16x4 h4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) h4[e] = (f16)(oacc[n][4 * c + e] * inv);
+        *(f16x4 *)(orow + n * 32 + 8 * c) = h4;
+      }
+  }
+}
+
+// Launches k_attn_s when every chunk's key tiles fit the LDS cap (returns
+// hipErrorNotSupported, launching nothing, when they do not).
+static hipError_t launch_attention_s(const AttnSArgs &base, const int32_t *cu, int batch, int d, int qbw,
+                                     hipStream_t s) {
+  constexpr int kCap = kAttnSCap;
+  if (qbw < 1 || base.rep * qbw > kAttnSMaxWaves) return hipErrorInvalidValue;
+  const int tb = 128 * d;
+  const int np = (base.P + 31) / 32;
+  // the key tiles of every sequence's last chunk (all its tiles) must fit
+  // before anything is launched
+  for (int i = 0; i < batch; ++i) {
+    const int s0 = cu[i], L = cu[i + 1] - cu[i];
+    if (L > 0 && (np + ((s0 + L - 1) >> 5) - (s0 >> 5) + 1) * tb > kCap) return hipErrorNotSupported;
+  }
+  AttnSArgs a = base;
+  a.qbw = qbw;
+  for (int first = 0; first < batch; first += kMaxSeqPerLaunch) {
+    const int n = batch - first < kMaxSeqPerLaunch ? batch - first : kMaxSeqPerLaunch;
+    a.n_seq = n;
+    int chunks = 0, nt_max = 0;
+    for (int i = 0; i < n; ++i) {
+      const int s0 = cu[first + i], L = cu[first + i + 1] - s0;
+      a.cu[i] = s0;
+      a.ch0[i] = chunks;
+      const int nch = (L + 32 * qbw - 1) / (32 * qbw);
+      chunks += nch;
+      if (L > 0) nt_max = std::max(nt_max, np + ((s0 + L - 1) >> 5) - (s0 >> 5) + 1);
+    }
+    a.cu[n] = cu[first + n];
+    a.ch0[n] = chunks;
+    if (chunks == 0) continue;
+    const int lds = nt_max * tb;
+    dim3 grid(chunks * a.Hkv), blk(64 * a.rep * qbw);
+#define MTE_ATTN_S(HD_)                                                                            \
+    {                                                                                              \
+      auto kern = k_attn_s<HD_>;                                                                   \
+      static const hipError_t attr =                                                               \
+          hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, kCap); \
+      if (attr != hipSuccess) return attr;                                                         \
+      hipLaunchKernelGGL(kern, grid, blk, lds, s, a);                                              \
+    }
+    if (d == 128) MTE_ATTN_S(128)
+    else MTE_ATTN_S(64)
+#undef MTE_ATTN_S
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 hipError_t launch_attention_h(const f16 *qk, const f16 *vt, const f16 *prefix, const f16 *pvt, int P, f16 *o,
                               float sc, const int32_t *cu, int batch, int T, int Hq, int Hkv, int d, int causal,
-                              hipStream_t s, int ks) {
+                              hipStream_t s, int ks, int qbw) {
   constexpr int WPB = 2;      // work items (waves) per workgroup without key split
   if (P < 0 || (P > 0 && (!prefix || !pvt)) || (d != 64 && d != 128) || Hq % Hkv || !qk || !vt || !o)
     return hipErrorInvalidValue;
+  // the staged kernel addresses k rows and V^T tiles by 32-bit byte offsets
+  const bool small = (uint64_t)std::max(T, P) * (uint64_t)(Hq + Hkv) * d * 2 < (1ull << 32);
+  if (qbw >= 0 && ks == 0 && small) {
+    AttnSArgs b;
+    b.qk = qk;
+    b.vt = vt;
+    b.pqk = prefix;
+    b.pvt = pvt;
+    b.o = o;
+    b.sc = sc;
+    b.ldq = (Hq + Hkv) * d;
+    b.T = T;
+    b.P = P;
+    b.Hq = Hq;
+    b.Hkv = Hkv;
+    b.rep = Hq / Hkv;
+    b.causal = causal ? 1 : 0;
+    // Default chunk: 2 query blocks of both query heads per kv head (4 waves)
+    // for causal attention with two query heads per kv head, 8 query blocks
+    // of one head (8 waves) for the bidirectional vision tower. Measured in
+    // isolation, 16 x 96 tokens: 10.1 / 8.0 / 9.1 us with 1 / 2 / 3 blocks
+    // (10.3 streaming), 16 x 128: 12.5 / 10.0 / 11.0 with 1 / 2 / 4 (12.9);
+    // one frame 6.8 (6.7 streaming, two-wave key split); 16 images of 256
+    // patches: 25.0 / 14.0 / 12.9 us with 2 / 4 / 8 blocks (19.5 streaming).
+    const int q = qbw > 0 ? qbw : std::max(1, (causal ? 4 : 8) / b.rep);
+    const hipError_t e = launch_attention_s(b, cu, batch, d, q, s);
+    if (e != hipErrorNotSupported || qbw > 0) return e;
+  }
   AttnHArgs a;
   a.qk = qk;
   a.vt = vt;

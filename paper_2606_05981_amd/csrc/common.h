@@ -73,4 +73,41 @@ __device__ __forceinline__ float warp_sum_xor(float v, int mask) {
   return v + __shfl_xor(v, mask, kWave);
 }
 
+// Waits until at most n vector-memory operations of this wave are pending.
+template <int n>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((n & 0xF) | (0x7 << 4) | (0xF << 8) | ((n >> 4) << 14));
+}
+// The same, and until every LDS access of this wave has completed.
+template <int n>
+__device__ __forceinline__ void wait_vm_lds0() {
+  static_assert(n >= 0 && n < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((n & 0xF) | (0x7 << 4) | (0x0 << 8) | ((n >> 4) << 14));
+}
+
+// 16-byte global -> LDS copy without a register round trip: lane i of the
+// wave writes lds_base + 16*i, lds_base wave-uniform. Written as inline asm
+// on purpose: the compiler's waitcnt pass treats the builtin form as LDS
+// traffic and then drains every outstanding LDS read (lgkmcnt(0)) before
+// the MFMAs that follow a stage's loads. The asm form is invisible to that
+// pass; the kernel orders these loads itself with explicit vmcnt waits and
+// barriers, and waits for all of them before it ends.
+// The source is a wave-uniform base (SGPRs) plus a 32-bit lane offset, so
+// each load needs one VGPR instead of a 64-bit address.
+// M0 is saved and restored around the load (the compiler reserves it), and
+// one wait state separates the M0 write from the load that reads it.
+__device__ __forceinline__ void dma16(const void *base, uint32_t off, uint32_t lds_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %3\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(off), "s"(base), "s"(lds_base)
+      : "memory");
+}
+
 }  // namespace mte

@@ -14,10 +14,9 @@ enum Mode {
   MODE_F32 = 0,  // fp32 weights and activations, fp32 MFMA
   MODE_F16 = 1,  // projections: fp16 operands (weights = bf16 values as power-of-two
                  // scaled fp16, exact down to 2^-31 of the matrix maximum; activations
-                 // rounded once to fp16), fp32 accumulate; decoder attention: q, k, v and
-                 // P as fp16 (power-of-two pre-scales), fp32 accumulate and softmax
-                 // (launch_attention_h); vision attention: q/k split into bf16 hi + lo
-                 // (launch_attention); attention output rounded to fp16
+                 // rounded once to fp16), fp32 accumulate; attention (decoder and vision
+                 // tower): q, k, v and P as fp16 (power-of-two pre-scales), fp32
+                 // accumulate and softmax (launch_attention_h), output rounded to fp16
   MODE_F8W = 2,  // projections only: fp16 activations as MODE_F16, weights OCP e4m3 codes
                  // with a power-of-two scale per weight row, widened to fp16 for the MFMAs
 };
@@ -136,19 +135,16 @@ hipError_t launch_rope_table(const int32_t *pos_thw, int T, int half, const Rope
 hipError_t launch_qkv_parts(float *qkv, const float *parts, int nparts, int T, int Hq, int Hkv,
                             const QkvEpi &qe, hipStream_t s);
 
-// Causal GQA attention over packed sequences. qkv: fp32 [T, (Hq+2Hkv)*d],
-// q heads first, then k, then v (q and k already normalised and rotated).
-// prefix: fp32 [P, (Hq+2Hkv)*d] rows of a shared prefix (same layout; its k
-// and v columns are read) that every sequence attends to in full before
-// its own keys, or P = 0. o: [T, Hq*d], float (MODE_F32) or fp16
-// (MODE_F16) times out_scale. cu: host int32[batch+1] sequence offsets.
-// Launches in chunks of <= 256 sequences. causal = 0: bidirectional (every
-// query attends to all keys of its own sequence). pv_f16 (MODE_F16): P and V
-// rounded once to fp16 for one fp16 MFMA instead of the three-product bf16
-// split (scores keep the split either way).
-hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int P, void *o, float out_scale,
-                            const int32_t *cu, int batch, int Hq, int Hkv, int d, hipStream_t s,
-                            int causal = 1, int pv_f16 = 0);
+// Causal GQA attention over packed sequences in fp32 (MODE_F32). qkv: fp32
+// [T, (Hq+2Hkv)*d], q heads first, then k, then v (q and k already
+// normalised and rotated). prefix: fp32 [P, (Hq+2Hkv)*d] rows of a shared
+// prefix (same layout; its k and v columns are read) that every sequence
+// attends to in full before its own keys, or P = 0. o: fp32 [T, Hq*d]. cu:
+// host int32[batch+1] sequence offsets. Launches in chunks of <= 256
+// sequences. causal = 0: bidirectional (every query attends to all keys of
+// its own sequence).
+hipError_t launch_attention(const float *qkv, const float *prefix, int P, float *o, const int32_t *cu, int batch,
+                            int Hq, int Hkv, int d, hipStream_t s, int causal = 1);
 
 // Causal (or bidirectional) GQA attention over packed sequences on fp16
 // operands laid out for the matrix cores by the QKV projection's epilogue:
@@ -162,12 +158,17 @@ hipError_t launch_attention(int mode, const float *qkv, const float *prefix, int
 //  prefix / pvt: the same two layouts for P rows of a shared prefix (its k
 //      heads and V^T tiles are read), or P = 0.
 // o: fp16 [T, Hq d]. sc = log2(e) / sqrt(d) * 2^(aq + ak). cu: host
-// int32[batch+1] offsets. One wave per (sequence, query head, 32 queries),
-// or ks waves (2 or 4) splitting its key tiles; ks = 0 picks by the number of
-// work items. Launches in chunks of <= 256 sequences.
+// int32[batch+1] offsets. Launches in chunks of <= 256 sequences.
+// Two kernels: when every sequence's key tiles (and the prefix's) for one kv
+// head fit in 64 KB of LDS, workgroups of qbw 32-query blocks x the query
+// heads of a kv head stage them in LDS once (qbw = 0: the default); else one
+// wave per (sequence, query head, 32 queries) streams them from global
+// memory, or ks waves (2 or 4) split its key tiles (ks = 0 picks by the
+// number of work items). qbw < 0 or ks > 0 selects the streaming kernel;
+// qbw > 0 requires the staged one (hipErrorNotSupported if it does not fit).
 hipError_t launch_attention_h(const f16 *qk, const f16 *vt, const f16 *prefix, const f16 *pvt, int P, f16 *o,
                               float sc, const int32_t *cu, int batch, int T, int Hq, int Hkv, int d, int causal,
-                              hipStream_t s, int ks = 0);
+                              hipStream_t s, int ks = 0, int qbw = 0);
 
 // Positions of packed sequences (see mte_build_positions).
 hipError_t launch_positions(const int32_t *layouts5, int batch, int32_t *pos_thw, int T,

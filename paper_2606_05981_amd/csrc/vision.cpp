@@ -32,6 +32,9 @@ struct VLayer {
   void *w_qkv, *w_o, *w_fc1, *w_fc2;
   float *ln1_g, *ln1_b, *ln2_g, *ln2_b, *b_qkv, *b_o, *b_fc1, *b_fc2;
   float s_qkv = 1.f, s_o = 1.f, s_fc1 = 1.f, s_fc2 = 1.f, o_pre = 1.f, y_pre = 1.f;
+  // fp16 attention operands (bf16 storage): q and k times q_pre / k_pre,
+  // att_sc = log2(e) / sqrt(d) / (q_pre k_pre)
+  float q_pre = 1.f, k_pre = 1.f, att_sc = 1.f;
 };
 
 size_t v_esize(int dtype) { return dtype == MTE_BF16 ? 2 : 4; }
@@ -53,7 +56,7 @@ struct mte_vision {
   void *patches = nullptr;  // [T, C p p] operand type
   float *h = nullptr;       // [T, D] residual stream
   void *xn = nullptr;       // [T, D] LayerNorm output (viewed [T/mm, mm D] for the merger)
-  float *qkv = nullptr;     // [T, 3D]
+  float *qkv = nullptr;     // [T, 3D] fp32 (fp32 storage), or fp16 q/k rows [T, 2D] then V^T tiles
   void *attn = nullptr;     // [T, D]
   void *act = nullptr;      // [T, F]
   void *mact = nullptr;     // [T/mm, mm D]
@@ -141,7 +144,7 @@ int mte_vision_create(const mte_vision_config *cfg, const mte_vision_weights *w,
   const size_t per = (size_t)(c.max_side / c.patch) * (c.max_side / c.patch);
   const size_t T = (size_t)c.max_images * per;
   if (hipMalloc(&e->patches, T * KP * es) != hipSuccess || hipMalloc((void **)&e->h, T * D * 4) != hipSuccess ||
-      hipMalloc(&e->xn, T * D * es) != hipSuccess || hipMalloc((void **)&e->qkv, T * 3 * D * 4) != hipSuccess ||
+      hipMalloc(&e->xn, T * D * es) != hipSuccess || hipMalloc((void **)&e->qkv, std::max(T * 3 * D * 4, ((T * 2 * D * 2 + 255) & ~(size_t)255) + (T + 31) / 32 * 32 * D * 2)) != hipSuccess ||
       hipMalloc(&e->attn, T * D * es) != hipSuccess || hipMalloc(&e->act, T * F * es) != hipSuccess ||
       hipMalloc(&e->mact, T * D * es) != hipSuccess || hipMalloc((void **)&e->mout, (T / mm + 1) * DO * 4) != hipSuccess ||
       hipMalloc((void **)&e->pos, 3 * T * 4) != hipSuccess ||
@@ -153,7 +156,7 @@ int mte_vision_create(const mte_vision_config *cfg, const mte_vision_weights *w,
   hipError_t he = hipSuccess;
   // Range analysis (bf16): max |.| of every matrix and vector, and the
   // largest row norms of Wv (rows 2D..3D of w_qkv), W_fc1 and W_m1.
-  enum { Q_QKV, Q_V, Q_O, Q_FC1, Q_FC2, Q_G1, Q_B1, Q_G2, Q_B2, Q_BQKV, Q_BFC1, Q_N };
+  enum { Q_QKV, Q_V, Q_O, Q_FC1, Q_FC2, Q_G1, Q_B1, Q_G2, Q_B2, Q_BQKV, Q_BFC1, Q_Q, Q_K, Q_N };
   enum { G_PATCH, G_M1, G_M2, G_MG, G_MB, G_BM1, G_N };
   std::vector<float> sth;
   const size_t nst = 2 * ((size_t)c.depth * Q_N + G_N);
@@ -168,7 +171,7 @@ int mte_vision_create(const mte_vision_config *cfg, const mte_vision_weights *w,
       const struct { const void *p; size_t rows, cols; } m[Q_N] = {
           {L.w_qkv, 3 * D, D}, {(const char *)L.w_qkv + 2 * D * D * eb, D, D}, {L.w_o, D, D}, {L.w_fc1, F, D},
           {L.w_fc2, D, F}, {L.ln1_g, 1, D}, {L.ln1_b, 1, D}, {L.ln2_g, 1, D}, {L.ln2_b, 1, D}, {L.b_qkv, 1, 3 * D},
-          {L.b_fc1, 1, F}};
+          {L.b_fc1, 1, F}, {L.w_qkv, D, D}, {(const char *)L.w_qkv + D * D * eb, D, D}};
       for (int k = 0; k < Q_N && he == hipSuccess; ++k)
         he = launch_matrix_stats(sf, m[k].p, (int)m[k].rows, (int)m[k].cols, sl + 2 * k, stream);
     }
@@ -208,7 +211,7 @@ int mte_vision_create(const mte_vision_config *cfg, const mte_vision_weights *w,
     o.w_fc2 = take_w(D * F);
     o.ln1_g = take_f(D); o.ln1_b = take_f(D); o.ln2_g = take_f(D); o.ln2_b = take_f(D);
     o.b_qkv = take_f(3 * D); o.b_o = take_f(D); o.b_fc1 = take_f(F); o.b_fc2 = take_f(D);
-    int wq = 0, wo = 0, w1 = 0, w2 = 0, k1 = 0, k2 = 0, ko = 0, ky = 0;
+    int wq = 0, wo = 0, w1 = 0, w2 = 0, k1 = 0, k2 = 0, ko = 0, ky = 0, kq = 0, kk = 0;
     if (f16) {
       const float *s = &sth[2 * (size_t)l * Q_N];
       auto mx = [&](int k) { return (double)s[2 * k]; };
@@ -222,6 +225,9 @@ int mte_vision_create(const mte_vision_config *cfg, const mte_vision_weights *w,
       k2 = v_act_shift(n2);
       ko = v_act_shift(n1 * rn(Q_V) + mx(Q_BQKV));
       ky = v_act_shift(n2 * rn(Q_FC1) + mx(Q_BFC1));
+      // q and k likewise, times sqrt(2) for the rotation of each pair
+      kq = v_act_shift(std::sqrt(2.0) * (n1 * rn(Q_Q) + mx(Q_BQKV)));
+      kk = v_act_shift(std::sqrt(2.0) * (n1 * rn(Q_K) + mx(Q_BQKV)));
     }
     o.s_qkv = std::ldexp(1.f, k1 - wq);
     o.s_o = std::ldexp(1.f, ko - wo);
@@ -229,6 +235,9 @@ int mte_vision_create(const mte_vision_config *cfg, const mte_vision_weights *w,
     o.s_fc2 = std::ldexp(1.f, ky - w2);
     o.o_pre = std::ldexp(1.f, -ko);
     o.y_pre = std::ldexp(1.f, -ky);
+    o.q_pre = std::ldexp(1.f, -kq);
+    o.k_pre = std::ldexp(1.f, -kk);
+    o.att_sc = (float)(1.4426950408889634 / std::sqrt((double)c.head_dim) * std::ldexp(1.0, kq + kk));
     he = conv_w(L.w_qkv, o.w_qkv, 3 * D, D, wq);
     if (he == hipSuccess) he = conv_w(L.w_o, o.w_o, D, D, wo);
     if (he == hipSuccess) he = conv_w(L.w_fc1, o.w_fc1, F, D, w1);
@@ -326,11 +335,26 @@ int mte_vision_encode_strided(mte_vision *e, const void *pixels, int32_t n, int3
                       nullptr, s, nullptr, e->b_patch));
   for (int l = 0; l < c.depth; ++l) {
     const VLayer &L = e->layers[l];
-    const QkvEpi qe{e->rcos, e->rsin, nullptr, nullptr, 2 * D, D, hd, c.ln_eps};
+    QkvEpi qe{e->rcos, e->rsin, nullptr, nullptr, 2 * D, D, hd, c.ln_eps};
+    // bf16 storage: fp16 attention operands in the matrix-core layout (q/k
+    // rows [T, 2D], then V^T tiles), in the qkv region
+    const bool half = mode != MODE_F32;
+    if (half) {
+      qe.qk = (f16 *)e->qkv;
+      qe.vt = (f16 *)((char *)e->qkv + (((size_t)T * 2 * D * 2 + 255) & ~(size_t)255));
+      qe.q_pre = L.q_pre;
+      qe.k_pre = L.k_pre;
+      qe.v_pre = L.o_pre;
+      qe.hkv = nh;
+    }
     MTE_TRY(launch_layernorm(e->h, L.ln1_g, L.ln1_b, af, e->xn, T, D, c.ln_eps, s));
     MTE_TRY(launch_gemm(mode, EPI_QKV, e->xn, L.w_qkv, e->qkv, T, 3 * D, D, 3 * D, L.s_qkv, 1.f, nullptr, 0, &sp,
                         &qe, s, nullptr, L.b_qkv));
-    MTE_TRY(launch_attention(mode, e->qkv, nullptr, 0, e->attn, L.o_pre, cu.data(), n, nh, nh, hd, s, 0, 1));
+    if (half)
+      MTE_TRY(launch_attention_h(qe.qk, qe.vt, nullptr, nullptr, 0, (f16 *)e->attn, L.att_sc, cu.data(), n, T, nh, nh,
+                                 hd, 0, s));
+    else
+      MTE_TRY(launch_attention(e->qkv, nullptr, 0, (float *)e->attn, cu.data(), n, nh, nh, hd, s, 0));
     MTE_TRY(launch_gemm(mode, EPI_RESID, e->attn, L.w_o, e->h, T, D, D, D, L.s_o, 1.f, nullptr, 0, &sp, nullptr, s,
                         nullptr, L.b_o));
     MTE_TRY(launch_layernorm(e->h, L.ln2_g, L.ln2_b, af, e->xn, T, D, c.ln_eps, s));

@@ -308,7 +308,9 @@ def test_stack_batched_sampled_sequences(torch, full_enc, name, sample):
 
 
 # Ragged lengths through the measured bf16 path (fp16 operands, K-split small-M tiles,
-# the bf16 hi/lo attention): 1, 2, the 32-row tile edges, 64/65 and 129.
+# fp16 attention operands): 1, 2, the 32-row tile edges, 64/65 and 129. Packed, the
+# 129-token sequence sends the batch to the register-streaming attention kernel; one
+# at a time, every length but 129 runs the LDS-staged one.
 RAGGED = (W.SeqLayout(1, 0, 0, 0, 0), W.SeqLayout(0, 1, 1, 1, 1), W.SeqLayout(0, 1, 4, 4, 15),
           W.SeqLayout(0, 1, 4, 4, 16), W.SeqLayout(0, 1, 4, 4, 17), W.SeqLayout(0, 1, 6, 5, 34),
           W.SeqLayout(0, 1, 8, 8, 1), W.SeqLayout(0, 1, 8, 8, 65), W.SeqLayout(5, 1, 8, 8, 27))
