@@ -23,17 +23,38 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gate_up_gemm_b16_traffic.json")
+STEP_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "te_prefill_28L_b1_L96_step_traffic.json")
 KERNEL_SOURCES = ["paper_2606_05981_amd/csrc/gemm_kernel.h", "paper_2606_05981_amd/csrc/gemm.hip",
                   "paper_2606_05981_amd/csrc/common.h", "paper_2606_05981_amd/csrc/launch.h"]
 
 
-def kernel_source_hash():
+def kernel_source_hash(files=None):
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in files or KERNEL_SOURCES:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
+
+
+def all_kernel_sources():
+    """Every source file of the library (a whole step's traffic depends on all of them)."""
+    d = os.path.join(ROOT, "paper_2606_05981_amd", "csrc")
+    return [os.path.join("paper_2606_05981_amd", "csrc", f) for f in sorted(os.listdir(d))]
+
+
+def measured_step_traffic():
+    """HBM-side bytes of one single-frame step (every kernel of positions + 28 layers +
+    final norm) from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE passes, each divided by
+    its copy-kernel calibration factor; None when missing or the sources changed since."""
+    try:
+        with open(STEP_TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("source_sha256") != kernel_source_hash(all_kernel_sources()):
+        return None
+    return t["hbm_bytes_per_step"]
 
 
 def measured_traffic():
@@ -803,7 +824,7 @@ def main():
                          "hbm_roofline": {"bound": "hbm", "achieved": round(wbytes / t1 / 1e9, 1),
                                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
                                           "frac": round(wbytes / t1 / 1e9 / PEAK_HBM_GBS, 4),
-                                          "bytes_per_step": wbytes,
+                                          "bytes_per_step": wbytes, "traffic": measured_step_traffic(),
                                           "frac_of_measured_copy": round(wbytes / t1 / 1e9 / res["hbm_copy_gbs_measured"], 4),
                                           "kernels": kernel_table(dims, b1["lens"], b1["kern"])}}
     if not args.no_regimes:

@@ -865,7 +865,7 @@ __global__ __launch_bounds__(64 * kAttnSMaxWaves) void k_attn_s(AttnSArgs a) {
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
   const uint32_t kcol = (uint32_t)((a.Hq + kvh) * HD) * 2u;
   for (int j = wv, cnt = 1; j < nt * GPT; j += nwv, ++cnt) {
-    if ((cnt & 31) == 0) wait_vm<32>();        // at most 63 loads in flight
+    if ((cnt & 31) == 0) wait_vm<31>();        // <= 31 pending, then 32 more: at most 63 in flight
     const int u = j / GPT, g = j % GPT;
     const bool pre = u < np;
     const int t = pre ? u : t_lo + u - np;
