@@ -737,10 +737,9 @@ struct AttnSArgs {
   float sc;
   int ldq, T, P;
   int Hq, Hkv, rep;
-  int n_seq, causal;
+  int causal;
   int qbw;             // 32-query blocks per workgroup
   int cu[kMaxSeqPerLaunch + 1];   // absolute token offsets
-  int ch0[kMaxSeqPerLaunch + 1];  // first query chunk of each sequence
 };
 
 // slot of 16-byte chunk c of k row r (HD / 8 chunks a row), and of chunk c
@@ -752,7 +751,6 @@ __device__ __forceinline__ int kslot(int r, int c) {
 }
 __device__ __forceinline__ int vslot(int r, int c) { return c ^ ((r >> 2) & 3); }
 
-constexpr int kAttnSMaxWaves = 8;
 constexpr int kAttnSCap = 64 * 1024;   // LDS bytes per workgroup: two workgroups a CU
 
 // Where a wave's staged tiles come from and which keys its lane's query sees.
@@ -824,8 +822,12 @@ __device__ __forceinline__ void s_tiles(const STile &st, const uint32_t (&ka)[HD
   }
 }
 
-template <int HD>
-__global__ __launch_bounds__(64 * kAttnSMaxWaves) void k_attn_s(AttnSArgs a) {
+// Grid: x = (chunk of the sequence, kv head), y = sequence; workgroups past a
+// sequence's last chunk leave at once. NWV waves (4 or 8), each copying a
+// fixed block of GPT / NWV copies of every tile: all k rows or all V^T rows,
+// the same per-lane offsets for every tile.
+template <int HD, int NWV>
+__global__ __launch_bounds__(64 * NWV) void k_attn_s(AttnSArgs a) {
   constexpr int ND = HD / 32, NK = HD / 16, NCH = HD / 8;
   constexpr int MT = kAttnSCap / (128 * HD);   // tiles that fit the LDS cap
   constexpr int KB = 64 * HD;                  // bytes of k rows (and of V^T rows) per tile
@@ -834,15 +836,10 @@ __global__ __launch_bounds__(64 * kAttnSMaxWaves) void k_attn_s(AttnSArgs a) {
   extern __shared__ u32x4 lds[];
   const int lane = threadIdx.x & 63, lrow = lane & 31, lgrp = lane >> 5;
   const int wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  const int nwv = (int)(blockDim.x >> 6);
   const int chunk = (int)blockIdx.x / a.Hkv, kvh = (int)blockIdx.x % a.Hkv;
-  int lo = 0, hi = a.n_seq - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (a.ch0[mid] <= chunk) lo = mid; else hi = mid - 1;
-  }
-  const int s0 = a.cu[lo], L = a.cu[lo + 1] - s0;
-  const int qc0 = (chunk - a.ch0[lo]) * a.qbw * 32;   // first query of the chunk
+  const int s0 = a.cu[blockIdx.y], L = a.cu[blockIdx.y + 1] - s0;
+  const int qc0 = chunk * a.qbw * 32;          // first query of the chunk
+  if (qc0 >= L) return;                        // the whole workgroup, before any barrier
   const int P = a.P, np = (P + 31) >> 5;
   const int t_lo = s0 >> 5;
   // key tiles of the chunk: the prefix's, then the batch tiles up to the last
@@ -861,23 +858,41 @@ __global__ __launch_bounds__(64 * kAttnSMaxWaves) void k_attn_s(AttnSArgs a) {
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk) qf[kk] = *(const f16x8 *)(qr + kk * 16);
   }
-  // copies: wave w takes copies w, w + nwv, ... of the nt * GPT
+  // Copy g of a tile (0 <= g < GPT) fills its 1 KB group g: groups below
+  // GPT / 2 hold k rows (lane l: row 64 g / NCH + l / NCH, chunk slot l % NCH),
+  // the rest V^T rows (lane l: row 16 g' + l / 4, chunk slot l % 4).
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
   const uint32_t kcol = (uint32_t)((a.Hq + kvh) * HD) * 2u;
-  for (int j = wv, cnt = 1; j < nt * GPT; j += nwv, ++cnt) {
-    if ((cnt & 31) == 0) wait_vm<31>();        // <= 31 pending, then 32 more: at most 63 in flight
-    const int u = j / GPT, g = j % GPT;
+  const uint32_t ldq2 = (uint32_t)a.ldq * 2u;
+  auto kcopy = [&](int u, int g) {
+    const bool pre = u < np;
+    const int rb = pre ? u * 32 : (t_lo + u - np) * 32;
+    const int r = g * (64 / NCH) + lane / NCH;
+    const int row = min(rb + r, pre ? P - 1 : a.T - 1);
+    dma16(pre ? a.pqk : a.qk, (uint32_t)row * ldq2 + kcol + (uint32_t)kslot<HD>(r, lane % NCH) * 16u,
+          lds0 + (uint32_t)(u * TB + g * 1024));
+  };
+  // V^T: the chunk slot of lane l is the same for every group
+  const uint32_t voff = (uint32_t)((lane >> 2) * 64 + (((lane & 3) ^ ((lane >> 4) & 3)) * 16));
+  auto vcopy = [&](int u, int g) {
     const bool pre = u < np;
     const int t = pre ? u : t_lo + u - np;
-    const uint32_t dst = lds0 + (uint32_t)(u * TB + g * 1024);
-    if (g < GPT / 2) {
-      const int x = g * 64 + lane, r = x / NCH, c = kslot<HD>(r, x % NCH);
-      const int row = pre ? min(u * 32 + r, P - 1) : min(t * 32 + r, a.T - 1);
-      dma16(pre ? a.pqk : a.qk, (uint32_t)row * (uint32_t)a.ldq * 2u + kcol + (uint32_t)c * 16u, dst);
-    } else {
-      const int x = (g - GPT / 2) * 64 + lane, r = x >> 2, c = vslot(r, x & 3);
-      dma16(pre ? a.pvt : a.vt, (uint32_t)(((t * a.Hkv + kvh) * HD + r) * 64 + c * 16), dst);
-    }
+    const char *vb = (const char *)(pre ? a.pvt : a.vt) + ((size_t)(t * a.Hkv + kvh) * HD) * 64 + g * 1024;
+    dma16(vb, voff, lds0 + (uint32_t)(u * TB + KB + g * 1024));
+  };
+  constexpr int CPW = GPT / NWV;               // copies per wave and tile
+  static_assert((NWV == 4 || NWV == 8) && GPT % NWV == 0 && (GPT / 2) % CPW == 0,
+                "a wave's block is all k or all V^T");
+  static_assert(MT * CPW + NK < 64, "vmcnt range: every copy and q load in flight at once");
+  const int c0 = wv * CPW;
+  if (c0 < GPT / 2) {
+    for (int u = 0; u < nt; ++u)
+#pragma unroll
+      for (int i = 0; i < CPW; ++i) kcopy(u, c0 + i);
+  } else {
+    for (int u = 0; u < nt; ++u)
+#pragma unroll
+      for (int i = 0; i < CPW; ++i) vcopy(u, c0 - GPT / 2 + i);
   }
   wait_vm<0>();
   __syncthreads();
@@ -937,7 +952,8 @@ __global__ __launch_bounds__(64 * kAttnSMaxWaves) void k_attn_s(AttnSArgs a) {
 static hipError_t launch_attention_s(const AttnSArgs &base, const int32_t *cu, int batch, int d, int qbw,
                                      hipStream_t s) {
   constexpr int kCap = kAttnSCap;
-  if (qbw < 1 || base.rep * qbw > kAttnSMaxWaves) return hipErrorInvalidValue;
+  if (qbw < 1) return hipErrorInvalidValue;
+  if (base.rep * qbw != 4 && base.rep * qbw != 8) return hipErrorNotSupported;   // 4 or 8 waves
   const int tb = 128 * d;
   const int np = (base.P + 31) / 32;
   // the key tiles of every sequence's last chunk (all its tiles) must fit
@@ -948,33 +964,32 @@ static hipError_t launch_attention_s(const AttnSArgs &base, const int32_t *cu, i
   }
   AttnSArgs a = base;
   a.qbw = qbw;
+  const int nwv = a.rep * qbw;
   for (int first = 0; first < batch; first += kMaxSeqPerLaunch) {
     const int n = batch - first < kMaxSeqPerLaunch ? batch - first : kMaxSeqPerLaunch;
-    a.n_seq = n;
-    int chunks = 0, nt_max = 0;
+    int nch_max = 0, nt_max = 0;
     for (int i = 0; i < n; ++i) {
       const int s0 = cu[first + i], L = cu[first + i + 1] - s0;
       a.cu[i] = s0;
-      a.ch0[i] = chunks;
-      const int nch = (L + 32 * qbw - 1) / (32 * qbw);
-      chunks += nch;
+      nch_max = std::max(nch_max, (L + 32 * qbw - 1) / (32 * qbw));
       if (L > 0) nt_max = std::max(nt_max, np + ((s0 + L - 1) >> 5) - (s0 >> 5) + 1);
     }
     a.cu[n] = cu[first + n];
-    a.ch0[n] = chunks;
-    if (chunks == 0) continue;
+    if (nch_max == 0) continue;
     const int lds = nt_max * tb;
-    dim3 grid(chunks * a.Hkv), blk(64 * a.rep * qbw);
-#define MTE_ATTN_S(HD_)                                                                            \
+    dim3 grid(nch_max * a.Hkv, n), blk(64 * nwv);
+#define MTE_ATTN_S(HD_, NWV_)                                                                      \
     {                                                                                              \
-      auto kern = k_attn_s<HD_>;                                                                   \
+      auto kern = k_attn_s<HD_, NWV_>;                                                             \
       static const hipError_t attr =                                                               \
           hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, kCap); \
       if (attr != hipSuccess) return attr;                                                         \
       hipLaunchKernelGGL(kern, grid, blk, lds, s, a);                                              \
     }
-    if (d == 128) MTE_ATTN_S(128)
-    else MTE_ATTN_S(64)
+    if (d == 128 && nwv == 4) MTE_ATTN_S(128, 4)
+    else if (d == 128) MTE_ATTN_S(128, 8)
+    else if (nwv == 4) MTE_ATTN_S(64, 4)
+    else MTE_ATTN_S(64, 8)
 #undef MTE_ATTN_S
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

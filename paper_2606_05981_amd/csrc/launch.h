@@ -165,7 +165,8 @@ hipError_t launch_attention(const float *qkv, const float *prefix, int P, float 
 // wave per (sequence, query head, 32 queries) streams them from global
 // memory, or ks waves (2 or 4) split its key tiles (ks = 0 picks by the
 // number of work items). qbw < 0 or ks > 0 selects the streaming kernel;
-// qbw > 0 requires the staged one (hipErrorNotSupported if it does not fit).
+// qbw > 0 requires the staged one (hipErrorNotSupported if it does not fit or
+// a workgroup of qbw blocks x Hq / Hkv heads would not be 4 or 8 waves).
 hipError_t launch_attention_h(const f16 *qk, const f16 *vt, const f16 *prefix, const f16 *pvt, int P, f16 *o,
                               float sc, const int32_t *cu, int batch, int T, int Hq, int Hkv, int d, int causal,
                               hipStream_t s, int ks = 0, int qbw = 0);
