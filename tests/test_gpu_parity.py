@@ -393,6 +393,43 @@ def test_no_leak_between_sequences_bit_exact(torch, enc_2l):
                 np.testing.assert_array_equal(out[sl[j]], base[sl[j]], err_msg=f"{i} -> {j}")
 
 
+# Ragged lengths that all stay within four 32-token key tiles at their packed offsets
+# (0, 96, 129, 194, 284, 285, 381): the batch takes the LDS-staged attention kernel with
+# sequences starting inside a tile, where the packed-edge batch above takes the streaming one.
+RAGGED_STAGED = (W.FRAME_96, W.SeqLayout(0, 1, 4, 4, 17), W.SeqLayout(0, 1, 8, 8, 1),
+                 W.SeqLayout(2, 1, 8, 8, 24), W.SeqLayout(1, 0, 0, 0, 0), W.FRAME_96,
+                 W.SeqLayout(0, 1, 4, 4, 15))
+
+
+def test_bf16_ragged_staged_attention(torch, enc_2l):
+    """Packed lengths 96, 33, 65, 90, 1, 96, 31: every sequence against the oracle at both bars,
+    and replacing a sequence that starts inside a key tile leaves every other one
+    bit-identical."""
+    dims, layouts = DIMS_2L, RAGGED_STAGED
+    lens = W.seq_lens(layouts)
+    assert lens == [96, 33, 65, 90, 1, 96, 31]
+    starts = np.cumsum([0] + lens[:-1])
+    assert all(((s0 + L - 1) >> 5) - (s0 >> 5) + 1 <= 4 for s0, L in zip(starts, lens))
+    emb = W.embeddings(dims, layouts)
+    got = _gpu_encode(torch, enc_2l, dims, emb, layouts)
+    ref, kept = _oracle_batch_with_layer_inputs(dims, emb, layouts, (0, 1))
+    sl = seq_slices(layouts)
+    for i in range(len(layouts)):
+        e = rel_err(got[sl[i]], ref[sl[i]])
+        _say(f"  L={lens[i]} at {starts[i]}: {e:.3e}")
+        assert e <= TOL_STACK, (lens[i], e)
+    _per_layer(torch, enc_2l, dims, layouts, kept, (0, 1), "ragged staged")
+    for i in (2, 3):
+        alt = emb.copy()
+        alt[sl[i]] = W.round_to_bf16(np.random.default_rng(70 + i).standard_normal(
+            alt[sl[i]].shape).astype(np.float32) * np.float32(0.02))
+        out = _gpu_encode(torch, enc_2l, dims, alt, layouts)
+        assert not np.array_equal(out[sl[i]], got[sl[i]])
+        for j in range(len(layouts)):
+            if j != i:
+                np.testing.assert_array_equal(out[sl[j]], got[sl[j]], err_msg=f"{i} -> {j}")
+
+
 def test_stack_wide_range_inputs(torch, full_enc):
     """Embeddings with std 37 and +-1160 outliers (the trained encoder's activation range)."""
     wl = W.workload("stack_b1")
