@@ -20,9 +20,10 @@ pytestmark = pytest.mark.gpu
 TOL_STACK = 3e-2
 
 
-# (24, 4, 4): 20 own tokens after 24 prefix keys, so that in the all-tiles-staged attention the
-# second key tile (keys 32..43) goes to the otherwise idle wave, and own queries 0..7 see none
-# of its keys (their partial softmax state is empty and must merge as zero).
+# Attention kernels: with an 80-token prefix (3 prefix tiles + 3 own) the streaming kernel;
+# with a 16-token prefix (1 + 3 tiles) and with (24, 4, 4) (20 own tokens after 24 prefix
+# keys: one prefix tile and one own tile) the LDS-staged one, both key sources in one staged
+# range.
 @pytest.mark.parametrize("prefix,hw,after,frames,n_layers",
                          [(80, 8, 32, 3, 4), (16, 8, 32, 2, 4), (80, 8, 32, 1, 28), (24, 4, 4, 2, 2)])
 def test_prefixed_equals_full_sequences(prefix, hw, after, frames, n_layers):
