@@ -145,6 +145,48 @@ class TextEncoder:
             pass
 
 
+class TECache:
+    """The optional text-encoder caching modes for streams whose instruction is fixed
+    (Sec. III-B, optional TE caching modes), around a TextEncoder:
+
+    - batch_one: encode only the batch's first frame (its rows 0 .. seq_lens[0] - 1) and
+      hand every frame that frame's hidden states, as a [B, L0, D] broadcast view (no copy);
+    - refresh_every = N: keep the result for N consecutive calls, encoding on the first of
+      every N (counting from the first call).
+
+    Both are approximations the caller opts into (the conditioning drifts from the frames it
+    stands for); with neither, every call encodes the whole packed batch and returns [T, D].
+    The cached tensor is returned as is until the next refresh."""
+
+    def __init__(self, encoder: "TextEncoder", batch_one: bool = False, refresh_every: int = 1):
+        if int(refresh_every) < 1:
+            raise ValueError("refresh_every must be >= 1")
+        self.encoder = encoder
+        self.batch_one = bool(batch_one)
+        self.refresh_every = int(refresh_every)
+        self.calls = 0
+        self.encodes = 0
+        self._cached: Optional[torch.Tensor] = None
+
+    def __call__(self, embeds: torch.Tensor, pos_thw: torch.Tensor, seq_lens: Sequence[int],
+                 stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+        lens = [int(x) for x in seq_lens]
+        _total(lens)
+        refresh = self._cached is None or self.calls % self.refresh_every == 0
+        self.calls += 1
+        if not refresh:
+            return self._cached
+        if self.batch_one:
+            l0 = lens[0]
+            one = self.encoder.encode(embeds[:l0], pos_thw[:, :l0].contiguous(), [l0], stream=stream)
+            out = one.unsqueeze(0).expand(len(lens), l0, one.shape[1])
+        else:
+            out = self.encoder.encode(embeds, pos_thw, lens, stream=stream)
+        self.encodes += 1
+        self._cached = out
+        return out
+
+
 def build_positions(layouts: Sequence[Sequence[int]], device="cuda",
                     stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
     """(t, h, w) positions of packed sequences, built on the device -> int32 [3, T]."""
