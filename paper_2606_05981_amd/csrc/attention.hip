@@ -7,9 +7,10 @@
 //
 // Three kernels. With bf16 storage (decoder and vision tower) q, k and v
 // arrive as fp16 operands that the QKV projection already wrote in the
-// matrix-core layout: k_attn_s stages a workgroup's key range in LDS when it
-// fits, k_attn_h streams it from global memory (both at the end of this
-// file). k_attn below serves fp32 storage, on the fp32 matrix cores:
+// matrix-core layout: k_attn_s stages a workgroup's key range in LDS (in
+// rounds when it is long), k_attn_h streams it from global memory for shapes
+// the staged kernel's 4- or 8-wave workgroups do not cover (both at the end
+// of this file). k_attn below serves fp32 storage, on the fp32 matrix cores:
 //
 // One workgroup (4 waves) serves one kv head, one tile of query rows of one
 // sequence and the query heads of that kv head assigned to it; every wave
@@ -722,12 +723,13 @@ __global__ __launch_bounds__(64 * WPB * KS) void k_attn_h(AttnHArgs a) {
 // from global memory straight into LDS (global_load_lds, 16 bytes a lane,
 // all copies in flight at once), wait for them once, and then compute from
 // LDS only: the chain of dependent global loads of the register-streaming
-// kernel becomes one load latency. The LDS cap (64 KB: two workgroups a CU)
-// holds at most 4 tiles of head size 128 and 8 of 64, so the softmax is
-// always the two-pass form: every tile's scores in registers, one maximum,
-// then the probabilities and O, in straight-line code per tile count. Same
-// arithmetic as k_attn_h (fp16 operands, fp32 scores and softmax in base 2,
-// masks as selects) on the same global 32-token key tiles.
+// kernel becomes one load latency per round. A round fills the LDS cap (64
+// KB: two workgroups a CU), 4 tiles of head size 128 or 8 of 64; within it
+// the softmax is two-pass (every tile's scores in registers, one maximum,
+// then the probabilities and O, in straight-line code per tile count), and
+// longer ranges carry the running maximum, sum and O from round to round.
+// Same arithmetic as k_attn_h (fp16 operands, fp32 scores and softmax in
+// base 2, masks as selects) on the same global 32-token key tiles.
 // LDS per tile: k rows [32][HD] then V^T rows [HD][32], 16-byte chunks
 // placed by an XOR of the row so that the 16 lanes of a quarter-wave that
 // read one chunk column of 16 rows hit 16 distinct 16-byte bank groups.
@@ -761,14 +763,16 @@ struct STile {
   int lgrp;
 };
 
-// All N staged tiles of one wave, two passes: the scores of every tile (kept
-// in registers), one maximum per query, then the probabilities and O. No
-// rescaling, and no branch between tiles, so the loads and MFMAs of
-// different tiles overlap.
+// The N tiles of one wave in one staged round (LDS slots 0 .. N-1 hold key
+// tiles ub .. ub+N-1 of its range), two passes: the scores of every tile
+// (kept in registers), one maximum per query, then the probabilities and O,
+// with no branch between tiles, so the loads and MFMAs of different tiles
+// overlap. Across rounds the running maximum m_i, sum l_i and O carry over
+// (rescaled when the maximum moves); a range of one round is plain two-pass.
 template <int HD, int N>
-__device__ __forceinline__ void s_tiles(const STile &st, const uint32_t (&ka)[HD / 16],
+__device__ __forceinline__ void s_tiles(const STile &st, int ub, const uint32_t (&ka)[HD / 16],
                                         const uint32_t (&va)[HD / 32][2], const f16x8 (&qf)[HD / 16],
-                                        f32x16 (&oacc)[HD / 32], float &l_i) {
+                                        f32x16 (&oacc)[HD / 32], float &m_i, float &l_i) {
   constexpr int ND = HD / 32, NK = HD / 16, TB = 128 * HD;
   f32x16 sv[N];
   float mb = -INFINITY;
@@ -785,8 +789,9 @@ __device__ __forceinline__ void s_tiles(const STile &st, const uint32_t (&ka)[HD
       for (int r = 0; r < 16; ++r) sacc[y][r] = 0.f;
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk) mfma32(sacc[kk & 1], kf[kk], qf[kk]);
-    const bool pre = x < st.np;
-    const int t = pre ? x : st.t_lo + x - st.np;
+    const int u = ub + x;
+    const bool pre = u < st.np;
+    const int t = pre ? u : st.t_lo + u - st.np;
     const int k_lo = pre ? 0 : st.s0, k_hi = pre ? st.P - 1 : st.kq_hi;
     const int kb = t * 32 + 4 * st.lgrp;
 #pragma unroll
@@ -797,7 +802,22 @@ __device__ __forceinline__ void s_tiles(const STile &st, const uint32_t (&ka)[HD
       mb = fmaxf(mb, sv[x][r]);
     }
   }
-  mb = warp_max_xor(mb, 32);                   // finite: every query sees its own key
+  mb = warp_max_xor(mb, 32);
+  // a query with no visible key yet (impossible in a range's first round,
+  // which holds a key every query sees) exponentiates against 0: exact zeros
+  const float m_new = fmaxf(m_i, mb);
+  const float m_ref = m_new == -INFINITY ? 0.f : m_new;
+  if (ub > 0) {                                // wave-uniform: rounds after the first
+    const float alpha = __builtin_amdgcn_exp2f(m_i - m_ref);
+    l_i *= alpha;
+    if (__any(alpha != 1.f)) {
+#pragma unroll
+      for (int n = 0; n < ND; ++n)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[n][r] *= alpha;
+    }
+  }
+  m_i = m_new;
 #pragma unroll
   for (int x = 0; x < N; ++x) {
     const char *tb = st.lb + x * TB;
@@ -811,7 +831,7 @@ __device__ __forceinline__ void s_tiles(const STile &st, const uint32_t (&ka)[HD
     for (int f = 0; f < 2; ++f)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float p = __builtin_amdgcn_exp2f(sv[x][8 * f + e] - mb);
+        const float p = __builtin_amdgcn_exp2f(sv[x][8 * f + e] - m_ref);
         l_i += p;
         pf[f][e] = (f16)p;
       }
@@ -825,9 +845,12 @@ __device__ __forceinline__ void s_tiles(const STile &st, const uint32_t (&ka)[HD
 // Grid: x = (chunk of the sequence, kv head), y = sequence; workgroups past a
 // sequence's last chunk leave at once. NWV waves (4 or 8), each copying a
 // fixed block of GPT / NWV copies of every tile: all k rows or all V^T rows,
-// the same per-lane offsets for every tile.
-template <int HD, int NWV>
-__global__ __launch_bounds__(64 * NWV) void k_attn_s(AttnSArgs a) {
+// the same per-lane offsets for every tile. Registers are held to two waves
+// per SIMD (two 4-wave workgroups, or one 8-wave workgroup, per CU). MR:
+// the launch has ranges longer than one round (without it the round loop is
+// compiled out, which leaves the one-round kernel fewer registers).
+template <int HD, int NWV, bool MR>
+__global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_attn_s(AttnSArgs a) {
   constexpr int ND = HD / 32, NK = HD / 16, NCH = HD / 8;
   constexpr int MT = kAttnSCap / (128 * HD);   // tiles that fit the LDS cap
   constexpr int KB = 64 * HD;                  // bytes of k rows (and of V^T rows) per tile
@@ -864,39 +887,44 @@ __global__ __launch_bounds__(64 * NWV) void k_attn_s(AttnSArgs a) {
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;
   const uint32_t kcol = (uint32_t)((a.Hq + kvh) * HD) * 2u;
   const uint32_t ldq2 = (uint32_t)a.ldq * 2u;
-  auto kcopy = [&](int u, int g) {
+  auto kcopy = [&](int u, int slot, int g) {
     const bool pre = u < np;
     const int rb = pre ? u * 32 : (t_lo + u - np) * 32;
     const int r = g * (64 / NCH) + lane / NCH;
     const int row = min(rb + r, pre ? P - 1 : a.T - 1);
     dma16(pre ? a.pqk : a.qk, (uint32_t)row * ldq2 + kcol + (uint32_t)kslot<HD>(r, lane % NCH) * 16u,
-          lds0 + (uint32_t)(u * TB + g * 1024));
+          lds0 + (uint32_t)(slot * TB + g * 1024));
   };
   // V^T: the chunk slot of lane l is the same for every group
   const uint32_t voff = (uint32_t)((lane >> 2) * 64 + (((lane & 3) ^ ((lane >> 4) & 3)) * 16));
-  auto vcopy = [&](int u, int g) {
+  auto vcopy = [&](int u, int slot, int g) {
     const bool pre = u < np;
     const int t = pre ? u : t_lo + u - np;
     const char *vb = (const char *)(pre ? a.pvt : a.vt) + ((size_t)(t * a.Hkv + kvh) * HD) * 64 + g * 1024;
-    dma16(vb, voff, lds0 + (uint32_t)(u * TB + KB + g * 1024));
+    dma16(vb, voff, lds0 + (uint32_t)(slot * TB + KB + g * 1024));
   };
   constexpr int CPW = GPT / NWV;               // copies per wave and tile
   static_assert((NWV == 4 || NWV == 8) && GPT % NWV == 0 && (GPT / 2) % CPW == 0,
                 "a wave's block is all k or all V^T");
   static_assert(MT * CPW + NK < 64, "vmcnt range: every copy and q load in flight at once");
   const int c0 = wv * CPW;
-  if (c0 < GPT / 2) {
-    for (int u = 0; u < nt; ++u)
+  // this wave's block of the copies of key tiles [ub, ue) into slots 0 ..
+  auto copies = [&](int ub, int ue) {
+    if (c0 < GPT / 2) {
+      for (int u = ub; u < ue; ++u)
 #pragma unroll
-      for (int i = 0; i < CPW; ++i) kcopy(u, c0 + i);
-  } else {
-    for (int u = 0; u < nt; ++u)
+        for (int i = 0; i < CPW; ++i) kcopy(u, u - ub, c0 + i);
+    } else {
+      for (int u = ub; u < ue; ++u)
 #pragma unroll
-      for (int i = 0; i < CPW; ++i) vcopy(u, c0 - GPT / 2 + i);
-  }
-  wait_vm<0>();
-  __syncthreads();
-  if (!live) return;
+        for (int i = 0; i < CPW; ++i) vcopy(u, u - ub, c0 - GPT / 2 + i);
+    }
+  };
+  // Rounds of at most MT tiles (one round when the range fits the cap). The
+  // first round's copies go out before anything else; its fragment offsets
+  // are computed while they land.
+  const int nrounds = (nt + MT - 1) / MT;      // workgroup-uniform
+  copies(0, min(nt, MT));
 
   const char *lb = (const char *)lds;
   uint32_t ka[NK], va[ND][2];
@@ -919,19 +947,37 @@ __global__ __launch_bounds__(64 * NWV) void k_attn_s(AttnSArgs a) {
   for (int n = 0; n < ND; ++n)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[n][r] = 0.f;
-  float l_i = 0.f;
-  // straight-line code for the wave's tile count (1 .. MT: the host checks
-  // that every sequence's tiles fit)
-  switch (ntw) {
-#define MTE_S_CASE(N_) \
-  case N_:             \
-    if constexpr (N_ <= MT) s_tiles<HD, N_>(st, ka, va, qf, oacc, l_i); \
-    break;
-    MTE_S_CASE(1) MTE_S_CASE(2) MTE_S_CASE(3) MTE_S_CASE(4)
-    MTE_S_CASE(5) MTE_S_CASE(6) MTE_S_CASE(7) MTE_S_CASE(8)
-#undef MTE_S_CASE
-    default: break;
+  float m_i = -INFINITY, l_i = 0.f;
+  // the round's tiles of this wave's own range, in straight-line code per
+  // count (waves with no queries, or whose range ended, skip)
+#define MTE_S_ROUND(UB_, UE_)                                                        \
+  switch (live ? min(ntw, (UE_)) - (UB_) : 0) {                                     \
+    case 1: s_tiles<HD, 1>(st, (UB_), ka, va, qf, oacc, m_i, l_i); break;           \
+    case 2: if constexpr (MT >= 2) s_tiles<HD, 2>(st, (UB_), ka, va, qf, oacc, m_i, l_i); break; \
+    case 3: if constexpr (MT >= 3) s_tiles<HD, 3>(st, (UB_), ka, va, qf, oacc, m_i, l_i); break; \
+    case 4: if constexpr (MT >= 4) s_tiles<HD, 4>(st, (UB_), ka, va, qf, oacc, m_i, l_i); break; \
+    case 5: if constexpr (MT >= 5) s_tiles<HD, 5>(st, (UB_), ka, va, qf, oacc, m_i, l_i); break; \
+    case 6: if constexpr (MT >= 6) s_tiles<HD, 6>(st, (UB_), ka, va, qf, oacc, m_i, l_i); break; \
+    case 7: if constexpr (MT >= 7) s_tiles<HD, 7>(st, (UB_), ka, va, qf, oacc, m_i, l_i); break; \
+    case 8: if constexpr (MT >= 8) s_tiles<HD, 8>(st, (UB_), ka, va, qf, oacc, m_i, l_i); break; \
+    default: break;                                                                 \
   }
+  wait_vm<0>();
+  __syncthreads();
+  MTE_S_ROUND(0, min(nt, MT))
+  // further rounds: every wave is done with the slots before they are refilled
+  if constexpr (MR) {
+    for (int rd = 1; rd < nrounds; ++rd) {
+      const int ub = rd * MT, ue = min(nt, ub + MT);
+      __syncthreads();
+      copies(ub, ue);
+      wait_vm<0>();
+      __syncthreads();
+      MTE_S_ROUND(ub, ue)
+    }
+  }
+#undef MTE_S_ROUND
+  if (!live) return;
   const float inv = 1.f / (l_i + __shfl_xor(l_i, 32, kWave));
   if (my_q < L) {
     f16 *orow = a.o + ((size_t)(s0 + my_q) * a.Hq + head) * HD + 4 * lgrp;
@@ -947,8 +993,8 @@ __global__ __launch_bounds__(64 * NWV) void k_attn_s(AttnSArgs a) {
   }
 }
 
-// Launches k_attn_s when every chunk's key tiles fit the LDS cap (returns
-// hipErrorNotSupported, launching nothing, when they do not).
+// Launches k_attn_s (hipErrorNotSupported, launching nothing, when a
+// workgroup would not have 4 or 8 waves).
 static hipError_t launch_attention_s(const AttnSArgs &base, const int32_t *cu, int batch, int d, int qbw,
                                      hipStream_t s) {
   constexpr int kCap = kAttnSCap;
@@ -956,12 +1002,6 @@ static hipError_t launch_attention_s(const AttnSArgs &base, const int32_t *cu, i
   if (base.rep * qbw != 4 && base.rep * qbw != 8) return hipErrorNotSupported;   // 4 or 8 waves
   const int tb = 128 * d;
   const int np = (base.P + 31) / 32;
-  // the key tiles of every sequence's last chunk (all its tiles) must fit
-  // before anything is launched
-  for (int i = 0; i < batch; ++i) {
-    const int s0 = cu[i], L = cu[i + 1] - cu[i];
-    if (L > 0 && (np + ((s0 + L - 1) >> 5) - (s0 >> 5) + 1) * tb > kCap) return hipErrorNotSupported;
-  }
   AttnSArgs a = base;
   a.qbw = qbw;
   const int nwv = a.rep * qbw;
@@ -976,20 +1016,21 @@ static hipError_t launch_attention_s(const AttnSArgs &base, const int32_t *cu, i
     }
     a.cu[n] = cu[first + n];
     if (nch_max == 0) continue;
-    const int lds = nt_max * tb;
+    const int lds = std::min(nt_max * tb, kCap);   // one round's tiles
     dim3 grid(nch_max * a.Hkv, n), blk(64 * nwv);
-#define MTE_ATTN_S(HD_, NWV_)                                                                      \
+#define MTE_ATTN_S(HD_, NWV_, MR_)                                                                 \
     {                                                                                              \
-      auto kern = k_attn_s<HD_, NWV_>;                                                             \
+      auto kern = k_attn_s<HD_, NWV_, MR_>;                                                        \
       static const hipError_t attr =                                                               \
           hipFuncSetAttribute((const void *)kern, hipFuncAttributeMaxDynamicSharedMemorySize, kCap); \
       if (attr != hipSuccess) return attr;                                                         \
       hipLaunchKernelGGL(kern, grid, blk, lds, s, a);                                              \
     }
-    if (d == 128 && nwv == 4) MTE_ATTN_S(128, 4)
-    else if (d == 128) MTE_ATTN_S(128, 8)
-    else if (nwv == 4) MTE_ATTN_S(64, 4)
-    else MTE_ATTN_S(64, 8)
+    const bool mr = nt_max * tb > kCap;         // some range needs more than one round
+    if (d == 128 && nwv == 4) { if (mr) MTE_ATTN_S(128, 4, true) else MTE_ATTN_S(128, 4, false) }
+    else if (d == 128) { if (mr) MTE_ATTN_S(128, 8, true) else MTE_ATTN_S(128, 8, false) }
+    else if (nwv == 4) { if (mr) MTE_ATTN_S(64, 4, true) else MTE_ATTN_S(64, 4, false) }
+    else { if (mr) MTE_ATTN_S(64, 8, true) else MTE_ATTN_S(64, 8, false) }
 #undef MTE_ATTN_S
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -159,14 +159,14 @@ hipError_t launch_attention(const float *qkv, const float *prefix, int P, float 
 //      heads and V^T tiles are read), or P = 0.
 // o: fp16 [T, Hq d]. sc = log2(e) / sqrt(d) * 2^(aq + ak). cu: host
 // int32[batch+1] offsets. Launches in chunks of <= 256 sequences.
-// Two kernels: when every sequence's key tiles (and the prefix's) for one kv
-// head fit in 64 KB of LDS, workgroups of qbw 32-query blocks x the query
-// heads of a kv head stage them in LDS once (qbw = 0: the default); else one
-// wave per (sequence, query head, 32 queries) streams them from global
-// memory, or ks waves (2 or 4) split its key tiles (ks = 0 picks by the
-// number of work items). qbw < 0 or ks > 0 selects the streaming kernel;
-// qbw > 0 requires the staged one (hipErrorNotSupported if it does not fit or
-// a workgroup of qbw blocks x Hq / Hkv heads would not be 4 or 8 waves).
+// Two kernels: workgroups of qbw 32-query blocks x the query heads of a kv
+// head copy their key tiles (and the prefix's) into LDS, 64 KB per round,
+// and compute from there (qbw = 0: the default chunk), when such a workgroup
+// is 4 or 8 waves; otherwise one wave per (sequence, query head, 32 queries)
+// streams the tiles from global memory, or ks waves (2 or 4) split its key
+// tiles (ks = 0 picks by the number of work items). qbw < 0 or ks > 0
+// selects the streaming kernel; qbw > 0 requires the staged one
+// (hipErrorNotSupported if qbw blocks x Hq / Hkv heads is not 4 or 8 waves).
 hipError_t launch_attention_h(const f16 *qk, const f16 *vt, const f16 *prefix, const f16 *pvt, int P, f16 *o,
                               float sc, const int32_t *cu, int batch, int T, int Hq, int Hkv, int d, int causal,
                               hipStream_t s, int ks = 0, int qbw = 0);

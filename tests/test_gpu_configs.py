@@ -1,7 +1,8 @@
 """Parity of supported model shapes beyond the default Qwen3-VL-2B layer, in bf16 storage
 (fp16 matrix-core operands): head_dim 64, plain multi-head attention (one query head per kv
-head), wider query groups (4 and 8 query heads per kv head), and the interleaved M-RoPE
-layout with QK-norm off at full width. Each runs one layer from the oracle's input (per-layer
+head), wider query groups (4, 8 and 16 query heads per kv head; 16 is beyond the LDS-staged
+attention's 4- or 8-wave workgroups and takes the register-streaming kernel, with its key
+split at this small batch), and the interleaved M-RoPE layout with QK-norm off at full width. Each runs one layer from the oracle's input (per-layer
 bar) and a two-layer stack (stack bar) over a ragged packed batch."""
 import sys
 
@@ -23,6 +24,7 @@ CASES = {
     "mha": W.Dims(n_layers=2, hidden=1024, n_q_heads=8, n_kv_heads=8, head_dim=128, ffn=2048),
     "gqa4": W.Dims(n_layers=2, hidden=2048, n_q_heads=16, n_kv_heads=4, head_dim=128, ffn=4096),
     "gqa8": W.Dims(n_layers=2, hidden=2048, n_q_heads=16, n_kv_heads=2, head_dim=128, ffn=4096),
+    "gqa16": W.Dims(n_layers=2, hidden=2048, n_q_heads=16, n_kv_heads=1, head_dim=128, ffn=4096),
     "interleaved_noqknorm": W.DIMS_FULL.with_(n_layers=2, mrope_layout=1, qk_norm=0),
 }
 LAYOUTS = (W.FRAME_96, W.SeqLayout(0, 1, 6, 5, 21), W.SeqLayout(3, 1, 9, 8, 40))
@@ -54,8 +56,8 @@ def test_shape_variants(case):
 
 def test_long_sequences_one_layer():
     """Long sequences at full width, one layer from the oracle's input: a 2048-token sequence
-    (a 32x32 image grid and 1024 text tokens; 64 causal query tiles, keys staged tile by tile)
-    packed with a 1003-token one whose last key tile is partial."""
+    (a 32x32 image grid and 1024 text tokens; 64 causal query tiles, keys staged in LDS in 16
+    rounds of four tiles) packed with a 1003-token one whose last key tile is partial."""
     import torch
     from paper_2606_05981_amd.encoder import build_positions
     assert torch.cuda.is_available(), "no GPU"

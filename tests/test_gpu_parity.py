@@ -309,8 +309,8 @@ def test_stack_batched_sampled_sequences(torch, full_enc, name, sample):
 
 # Ragged lengths through the measured bf16 path (fp16 operands, K-split small-M tiles,
 # fp16 attention operands): 1, 2, the 32-row tile edges, 64/65 and 129. Packed, the
-# 129-token sequence sends the batch to the register-streaming attention kernel; one
-# at a time, every length but 129 runs the LDS-staged one.
+# 129-token sequence's later query chunks see more than four key tiles, so the staged
+# attention takes two LDS rounds there; one at a time, every length but 129 fits one.
 RAGGED = (W.SeqLayout(1, 0, 0, 0, 0), W.SeqLayout(0, 1, 1, 1, 1), W.SeqLayout(0, 1, 4, 4, 15),
           W.SeqLayout(0, 1, 4, 4, 16), W.SeqLayout(0, 1, 4, 4, 17), W.SeqLayout(0, 1, 6, 5, 34),
           W.SeqLayout(0, 1, 8, 8, 1), W.SeqLayout(0, 1, 8, 8, 65), W.SeqLayout(5, 1, 8, 8, 27))
@@ -394,8 +394,8 @@ def test_no_leak_between_sequences_bit_exact(torch, enc_2l):
 
 
 # Ragged lengths that all stay within four 32-token key tiles at their packed offsets
-# (0, 96, 129, 194, 284, 285, 381): the batch takes the LDS-staged attention kernel with
-# sequences starting inside a tile, where the packed-edge batch above takes the streaming one.
+# (0, 96, 129, 194, 284, 285, 381): every key range is one LDS round of the staged attention,
+# with sequences starting inside a tile (the packed-edge batch above needs two rounds).
 RAGGED_STAGED = (W.FRAME_96, W.SeqLayout(0, 1, 4, 4, 17), W.SeqLayout(0, 1, 8, 8, 1),
                  W.SeqLayout(2, 1, 8, 8, 24), W.SeqLayout(1, 0, 0, 0, 0), W.FRAME_96,
                  W.SeqLayout(0, 1, 4, 4, 15))

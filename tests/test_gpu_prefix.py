@@ -20,10 +20,9 @@ pytestmark = pytest.mark.gpu
 TOL_STACK = 3e-2
 
 
-# Attention kernels: with an 80-token prefix (3 prefix tiles + 3 own) the streaming kernel;
-# with a 16-token prefix (1 + 3 tiles) and with (24, 4, 4) (20 own tokens after 24 prefix
-# keys: one prefix tile and one own tile) the LDS-staged one, both key sources in one staged
-# range.
+# Staged attention: an 80-token prefix (3 prefix tiles + 3 own) takes two LDS rounds, the
+# first all prefix; a 16-token prefix (1 + 3 tiles) and (24, 4, 4) (20 own tokens after 24
+# prefix keys: one prefix tile and one own tile) one round holding both key sources.
 @pytest.mark.parametrize("prefix,hw,after,frames,n_layers",
                          [(80, 8, 32, 3, 4), (16, 8, 32, 2, 4), (80, 8, 32, 1, 28), (24, 4, 4, 2, 2)])
 def test_prefixed_equals_full_sequences(prefix, hw, after, frames, n_layers):
