@@ -450,6 +450,37 @@ hipError_t launch_attention(const float *qkv, const float *prefix, int P, float 
 // serves one item: wave w takes key tiles w, w + KS, ..., and wave 0 merges
 // the partial softmax states (running max, sum, O) of the others from LDS,
 // so an item's chain of dependent tile steps is KS times shorter.
+// A wave's output for its lanes' queries: registers 4c..4c+3 of oacc[n] are
+// d = 32 n + 8 c + 4 g + 0..3 of the lane's query (g = lane / 32). For each
+// pair (2p, 2p+1) one v_permlane32_swap gives lane g = 0 the d 16p + 0..7 and
+// lane g = 1 the d 16p + 8..15 of block n, so each lane stores 16 contiguous
+// bytes (half the stores of 8-byte pieces, each to another row). `row`: the
+// query's first output value plus 8 g; every lane of the wave takes part,
+// lanes with `valid` false store nothing.
+template <int HD>
+__device__ __forceinline__ void store_o(const f32x16 (&oacc)[HD / 32], float inv, f16 *row, bool valid) {
+#pragma unroll
+  for (int n = 0; n < HD / 32; ++n)
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      f16x4 lo, hi;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        lo[e] = (f16)(oacc[n][8 * p + e] * inv);
+        hi[e] = (f16)(oacc[n][8 * p + 4 + e] * inv);
+      }
+      u32x2 x = __builtin_bit_cast(u32x2, lo), y = __builtin_bit_cast(u32x2, hi);
+#pragma unroll
+      for (int w = 0; w < 2; ++w) {
+        // the upper 32 lanes' x and the lower 32 lanes' y trade places
+        const auto r = __builtin_amdgcn_permlane32_swap(x[w], y[w], false, false);
+        x[w] = r[0];
+        y[w] = r[1];
+      }
+      if (valid) *(u32x4 *)(row + n * 32 + 16 * p) = u32x4{x[0], x[1], y[0], y[1]};
+    }
+}
+
 struct AttnHArgs {
   const f16 *qk;      // [T, ldq]
   const f16 *vt;      // [ceil(T / 32)][Hkv][HD][32]
@@ -699,21 +730,8 @@ __global__ __launch_bounds__(64 * WPB * KS) void k_attn_h(AttnHArgs a) {
         for (int r = 0; r < 16; ++r) oacc[n][r] += fv * red[v][2 + n * 16 + r][lane];
     }
   }
-  // Output: oacc[n] registers 4c..4c+3 are d = 32 n + 8 c + 4 lgrp + 0..3 of
-  // the lane's query, one 8-byte store each.
   const float inv = 1.f / (l_i + __shfl_xor(l_i, 32, kWave));
-  if (my_q < L) {
-    f16 *orow = a.o + ((size_t)(s0 + my_q) * a.Hq + head) * HD + 4 * lgrp;
-#pragma unroll
-    for (int n = 0; n < ND; ++n)
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        f16x4 h4;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) h4[e] = (f16)(oacc[n][4 * c + e] * inv);
-        *(f16x4 *)(orow + n * 32 + 8 * c) = h4;
-      }
-  }
+  store_o<HD>(oacc, inv, a.o + ((size_t)(s0 + min(my_q, L - 1)) * a.Hq + head) * HD + 8 * lgrp, my_q < L);
 }
 
 // Staged variant of k_attn_h for key ranges that fit in LDS. A workgroup
@@ -979,18 +997,7 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(2, 2))
 #undef MTE_S_ROUND
   if (!live) return;
   const float inv = 1.f / (l_i + __shfl_xor(l_i, 32, kWave));
-  if (my_q < L) {
-    f16 *orow = a.o + ((size_t)(s0 + my_q) * a.Hq + head) * HD + 4 * lgrp;
-#pragma unroll
-    for (int n = 0; n < ND; ++n)
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        f16x4 h4;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) h4[e] = (f16)(oacc[n][4 * c + e] * inv);
-        *(f16x4 *)(orow + n * 32 + 8 * c) = h4;
-      }
-  }
+  store_o<HD>(oacc, inv, a.o + ((size_t)(s0 + min(my_q, L - 1)) * a.Hq + head) * HD + 8 * lgrp, my_q < L);
 }
 
 // Launches k_attn_s (hipErrorNotSupported, launching nothing, when a
