@@ -66,12 +66,12 @@ static const TileChoice kChoices[] = {
     {12288, 2048, EPI_SWIGLU, 1536, 33, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
     {4096, 2048, EPI_QKV, 3072, 38, 1},   {2048, 2048, EPI_RESID, 3072, 8, 1},
     {12288, 2048, EPI_SWIGLU, 3072, 33, 1}, {2048, 6144, EPI_RESID, 3072, 8, 1},
-    {4096, 2048, EPI_QKV, 10240, 38, 1},  {2048, 2048, EPI_RESID, 10240, 36, 1},
-    {12288, 2048, EPI_SWIGLU, 10240, 33, 1}, {2048, 6144, EPI_RESID, 10240, 12, 1},
+    {4096, 2048, EPI_QKV, 10240, 38, 1, 421},  {2048, 2048, EPI_RESID, 10240, 36, 1, 421},
+    {12288, 2048, EPI_SWIGLU, 10240, 33, 1}, {2048, 6144, EPI_RESID, 10240, 12, 1, 421},
     // vision tower (width 1024, MLP 4096, 768-value patches, 2x2 merger to 2048):
     // 16 images of 256 patches, merger at 1024 rows
-    {3072, 1024, EPI_QKV, 4096, 38, 1},   {1024, 1024, EPI_RESID, 4096, 12, 1},
-    {4096, 1024, EPI_GELU, 4096, 38, 1},  {1024, 4096, EPI_RESID, 4096, 12, 1},
+    {3072, 1024, EPI_QKV, 4096, 38, 1},   {1024, 1024, EPI_RESID, 4096, 12, 1, 421},
+    {4096, 1024, EPI_GELU, 4096, 38, 1},  {1024, 4096, EPI_RESID, 4096, 12, 1, 421},
     {1024, 768, EPI_STORE, 4096, 12, 1},  {4096, 4096, EPI_GELU, 1024, 30, 1},
     {2048, 4096, EPI_STORE, 1024, 18, 1},
 };
