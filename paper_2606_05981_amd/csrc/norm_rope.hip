@@ -80,29 +80,38 @@ __global__ __launch_bounds__(256) void k_rmsnorm_vec(const TI *in, float *copy_t
   __shared__ float red[4];
   const int row = blockIdx.x, tid = threadIdx.x;
   const size_t rb = (size_t)row * D;
-  f32x4 v[NV];
+  f32x4 v[NV], gv[NV];
   float ss = 0.f;
+  // Every load first (input, gains, then the partial sums), so that one
+  // memory latency covers them all; then the adds, in split order.
 #pragma unroll
   for (int i = 0; i < NV; ++i) {
     const int c = (i * 256 + tid) * 4;
+    gv[i] = *(const f32x4 *)(gain + c);
     if constexpr (std::is_same<TI, float>::value) {
       v[i] = *(const f32x4 *)(in + rb + c);
     } else {
       const bf16x4 b = *(const bf16x4 *)(in + rb + c);
       v[i] = (f32x4){(float)b[0], (float)b[1], (float)b[2], (float)b[3]};
     }
-    f32x4 q[kMaxParts];
+  }
+  f32x4 q[kMaxParts][NV];
 #pragma unroll
-    for (int k = 0; k < kMaxParts; ++k)     // all loads first, then the adds in split order
-      if (k < pt.np) q[k] = *(const f32x4 *)(pt.p + (size_t)k * pt.stride + rb + c);
+  for (int k = 0; k < kMaxParts; ++k)
+    if (k < pt.np)
 #pragma unroll
-    for (int k = 0; k < kMaxParts; ++k)
-      if (k < pt.np)
+      for (int i = 0; i < NV; ++i) q[k][i] = *(const f32x4 *)(pt.p + (size_t)k * pt.stride + rb + (i * 256 + tid) * 4);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[i][e] += q[k][e];
+  for (int k = 0; k < kMaxParts; ++k)
+    if (k < pt.np)
+#pragma unroll
+      for (int i = 0; i < NV; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[i][e] += q[k][i][e];
+#pragma unroll
+  for (int i = 0; i < NV; ++i)
 #pragma unroll
     for (int e = 0; e < 4; ++e) ss += v[i][e] * v[i][e];
-  }
 #pragma unroll
   for (int m = 32; m >= 1; m >>= 1) ss = warp_sum_xor(ss, m);
   if ((tid & 63) == 0) red[tid >> 6] = ss;
@@ -112,10 +121,9 @@ __global__ __launch_bounds__(256) void k_rmsnorm_vec(const TI *in, float *copy_t
   for (int i = 0; i < NV; ++i) {
     const int c = (i * 256 + tid) * 4;
     if (copy_to) *(f32x4 *)(copy_to + rb + c) = v[i];
-    const f32x4 g = *(const f32x4 *)(gain + c);
     f32x4 y;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) y[e] = v[i][e] * rs * g[e];
+    for (int e = 0; e < 4; ++e) y[e] = v[i][e] * rs * gv[i][e];
     if constexpr (OUT_FMT == FMT_F32) {
       *(f32x4 *)((float *)out + rb + c) = y;
     } else if constexpr (OUT_FMT == FMT_BF16) {
@@ -222,16 +230,33 @@ __global__ __launch_bounds__(256) void k_qkv_parts(float *__restrict__ qkv, Part
   if (it < nh * half) {
     const int h = it / half, j = it % half;
     const int c0 = h * d + j;
-    float u = ld(c0), w = ld(c0 + half);
+    // every load first (the pair's partial sums, gains and rotary table entry),
+    // so that one memory latency covers them all
+    float qa[kMaxParts], qb[kMaxParts];
+#pragma unroll
+    for (int k = 0; k < kMaxParts; ++k)
+      if (k < pt.np) {
+        qa[k] = prow[(size_t)k * pt.stride + c0];
+        qb[k] = prow[(size_t)k * pt.stride + c0 + half];
+      }
+    const float *gn = (h < Hq) ? qe.qn : qe.kn;
+    const float ga = qe.qn ? gn[j] : 1.f, gb = qe.qn ? gn[j + half] : 1.f;
+    const float c = qe.rcos[(size_t)tok * half + j], s = qe.rsin[(size_t)tok * half + j];
+    asm volatile("" ::"v"(ga), "v"(gb), "v"(c), "v"(s) : "memory");   // keeps these loads up here
+    float u = qa[0], w = qb[0];
+#pragma unroll
+    for (int k = 1; k < kMaxParts; ++k)
+      if (k < pt.np) {
+        u += qa[k];
+        w += qb[k];
+      }
     if (qe.qn) {
-      const float *gn = (h < Hq) ? qe.qn : qe.kn;
       float ss = u * u + w * w;
       for (int m = half >> 1; m >= 1; m >>= 1) ss = warp_sum_xor(ss, m);
       const float rs = rsqrtf(ss / (float)d + qe.eps);
-      u = u * rs * gn[j];
-      w = w * rs * gn[j + half];
+      u = u * rs * ga;
+      w = w * rs * gb;
     }
-    const float c = qe.rcos[(size_t)tok * half + j], s = qe.rsin[(size_t)tok * half + j];
     row[c0] = u * c - w * s;
     row[c0 + half] = w * c + u * s;
   } else if (it < nh * half + Hkv * d) {
@@ -265,16 +290,33 @@ __global__ __launch_bounds__(256) void k_qkv_parts_h(Parts pt, int T, int Hq, in
     if (!live) return;                           // block-uniform
     const int h = it / half, j = it % half;
     const int c0 = h * d + j;
-    float u = ld(c0), w = ld(c0 + half);
+    // every load first (the pair's partial sums, gains and rotary table entry),
+    // so that one memory latency covers them all
+    float qa[kMaxParts], qb[kMaxParts];
+#pragma unroll
+    for (int k = 0; k < kMaxParts; ++k)
+      if (k < pt.np) {
+        qa[k] = prow[(size_t)k * pt.stride + c0];
+        qb[k] = prow[(size_t)k * pt.stride + c0 + half];
+      }
+    const float *gn = (h < Hq) ? qe.qn : qe.kn;
+    const float ga = qe.qn ? gn[j] : 1.f, gb = qe.qn ? gn[j + half] : 1.f;
+    const float c = qe.rcos[(size_t)tok * half + j], s = qe.rsin[(size_t)tok * half + j];
+    asm volatile("" ::"v"(ga), "v"(gb), "v"(c), "v"(s) : "memory");   // keeps these loads up here
+    float u = qa[0], w = qb[0];
+#pragma unroll
+    for (int k = 1; k < kMaxParts; ++k)
+      if (k < pt.np) {
+        u += qa[k];
+        w += qb[k];
+      }
     if (qe.qn) {
-      const float *gn = (h < Hq) ? qe.qn : qe.kn;
       float ss = u * u + w * w;
       for (int m = half >> 1; m >= 1; m >>= 1) ss = warp_sum_xor(ss, m);
       const float rs = rsqrtf(ss / (float)d + qe.eps);
-      u = u * rs * gn[j];
-      w = w * rs * gn[j + half];
+      u = u * rs * ga;
+      w = w * rs * gb;
     }
-    const float c = qe.rcos[(size_t)tok * half + j], s = qe.rsin[(size_t)tok * half + j];
     const float pre = h < Hq ? qe.q_pre : qe.k_pre;
     f16 *row = qe.qk + (size_t)tok * nh * d;
     row[c0] = (f16)((u * c - w * s) * pre);
