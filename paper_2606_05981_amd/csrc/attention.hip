@@ -744,10 +744,12 @@ __global__ __launch_bounds__(64 * WPB * KS) void k_attn_h(AttnHArgs a) {
 // kernel becomes one load latency per round. A round fills the LDS cap (64
 // KB: two workgroups a CU), 4 tiles of head size 128 or 8 of 64; within it
 // the softmax is two-pass (every tile's scores in registers, one maximum,
-// then the probabilities and O, in straight-line code per tile count), and
-// longer ranges carry the running maximum, sum and O from round to round.
-// Same arithmetic as k_attn_h (fp16 operands, fp32 scores and softmax in
-// base 2, masks as selects) on the same global 32-token key tiles.
+// then the probabilities and O, code specialised per tile count; masks only
+// in the tiles that need them), and longer ranges carry the running maximum,
+// sum and O from round to round. The arithmetic of k_attn_h (fp16 operands,
+// fp32 scores and softmax in base 2, masks as selects) on the same global
+// 32-token key tiles, but for the scale: one fma before exp2 here, a multiply
+// and a subtract there (one rounding apart).
 // LDS per tile: k rows [32][HD] then V^T rows [HD][32], 16-byte chunks
 // placed by an XOR of the row so that the 16 lanes of a quarter-wave that
 // read one chunk column of 16 rows hit 16 distinct 16-byte bank groups.
@@ -777,50 +779,58 @@ constexpr int kAttnSCap = 64 * 1024;   // LDS bytes per workgroup: two workgroup
 struct STile {
   const char *lb;      // LDS base
   int np, t_lo, P, s0, kq_hi;
+  int kw_hi;           // the smallest kq_hi of the wave's lanes (wave-uniform)
   float sc;
   int lgrp;
 };
 
 // The N tiles of one wave in one staged round (LDS slots 0 .. N-1 hold key
-// tiles ub .. ub+N-1 of its range), two passes: the scores of every tile
-// (kept in registers), one maximum per query, then the probabilities and O,
-// with no branch between tiles, so the loads and MFMAs of different tiles
-// overlap. Across rounds the running maximum m_i, sum l_i and O carry over
-// (rescaled when the maximum moves); a range of one round is plain two-pass.
+// tiles ub .. ub+N-1 of its range), in three passes: the raw scores q.k of
+// every tile (one MFMA chain per tile, all kept in registers; straight-line
+// code, so the loads and MFMAs of different tiles overlap), then the mask --
+// only in a tile that some query of the wave does not see whole, a
+// wave-uniform test -- and one maximum per query, then the probabilities
+// 2^(sc s - m) (one fma per score: sc > 0 scales the maximum exactly as it
+// scales each score) and O. Across rounds the running maximum m_i (scaled),
+// sum l_i and O carry over (rescaled when the maximum moves); a range of one
+// round is plain two-pass.
 template <int HD, int N>
 __device__ __forceinline__ void s_tiles(const STile &st, int ub, const uint32_t (&ka)[HD / 16],
                                         const uint32_t (&va)[HD / 32][2], const f16x8 (&qf)[HD / 16],
                                         f32x16 (&oacc)[HD / 32], float &m_i, float &l_i) {
   constexpr int ND = HD / 32, NK = HD / 16, TB = 128 * HD;
   f32x16 sv[N];
-  float mb = -INFINITY;
 #pragma unroll
   for (int x = 0; x < N; ++x) {
     const char *tb = st.lb + x * TB;
     f16x8 kf[NK];
 #pragma unroll
     for (int kk = 0; kk < NK; ++kk) kf[kk] = *(const f16x8 *)(tb + ka[kk]);
-    f32x16 sacc[2];
 #pragma unroll
-    for (int y = 0; y < 2; ++y)
+    for (int r = 0; r < 16; ++r) sv[x][r] = 0.f;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) sacc[y][r] = 0.f;
+    for (int kk = 0; kk < NK; ++kk) mfma32(sv[x], kf[kk], qf[kk]);
+  }
+  float mb = -INFINITY;
 #pragma unroll
-    for (int kk = 0; kk < NK; ++kk) mfma32(sacc[kk & 1], kf[kk], qf[kk]);
+  for (int x = 0; x < N; ++x) {
     const int u = ub + x;
     const bool pre = u < st.np;
-    const int t = pre ? u : st.t_lo + u - st.np;
-    const int k_lo = pre ? 0 : st.s0, k_hi = pre ? st.P - 1 : st.kq_hi;
-    const int kb = t * 32 + 4 * st.lgrp;
+    const int kt0 = pre ? u * 32 : (st.t_lo + u - st.np) * 32;   // the tile's first key
+    const int k_lo = pre ? 0 : st.s0;
+    if (kt0 < k_lo || kt0 + 31 > (pre ? st.P - 1 : st.kw_hi)) {    // wave-uniform
+      const int k_hi = pre ? st.P - 1 : st.kq_hi;
+      const int kb = kt0 + 4 * st.lgrp;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int k = kb + 8 * (r >> 2) + (r & 3);
-      const float v = sacc[0][r] + sacc[1][r];
-      sv[x][r] = ((k >= k_lo) & (k <= k_hi)) ? v * st.sc : -INFINITY;
-      mb = fmaxf(mb, sv[x][r]);
+      for (int r = 0; r < 16; ++r) {
+        const int k = kb + 8 * (r >> 2) + (r & 3);
+        sv[x][r] = ((k >= k_lo) & (k <= k_hi)) ? sv[x][r] : -INFINITY;
+      }
     }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mb = fmaxf(mb, sv[x][r]);
   }
-  mb = warp_max_xor(mb, 32);
+  mb = warp_max_xor(mb, 32) * st.sc;
   // a query with no visible key yet (impossible in a range's first round,
   // which holds a key every query sees) exponentiates against 0: exact zeros
   const float m_new = fmaxf(m_i, mb);
@@ -849,7 +859,7 @@ __device__ __forceinline__ void s_tiles(const STile &st, int ub, const uint32_t 
     for (int f = 0; f < 2; ++f)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float p = __builtin_amdgcn_exp2f(sv[x][8 * f + e] - m_ref);
+        const float p = __builtin_amdgcn_exp2f(fmaf(sv[x][8 * f + e], st.sc, -m_ref));
         l_i += p;
         pf[f][e] = (f16)p;
       }
@@ -959,7 +969,8 @@ __global__ __launch_bounds__(64 * NWV) __attribute__((amdgpu_waves_per_eu(2, 2))
   const int kend = a.causal ? min(q0 + 31, L - 1) : L - 1;
   const int ntw = np + ((s0 + kend) >> 5) - t_lo + 1;
   const int kq_hi = a.causal ? s0 + min(my_q, L - 1) : s0 + L - 1;
-  const STile st{lb, np, t_lo, P, s0, kq_hi, a.sc, lgrp};
+  const int kw_hi = a.causal ? s0 + min(q0, L - 1) : s0 + L - 1;
+  const STile st{lb, np, t_lo, P, s0, kq_hi, kw_hi, a.sc, lgrp};
   f32x16 oacc[ND];
 #pragma unroll
   for (int n = 0; n < ND; ++n)
