@@ -115,6 +115,25 @@ def test_vision_bf16_512_source(torch):
     assert err <= TOL_SHORT
 
 
+def test_vision_bf16_unaligned_patch_counts(torch):
+    """Images whose patch counts are not multiples of the 32-key attention tile (224x224:
+    196 patches, 49 image tokens each): every image after the first starts its key range
+    inside a tile and every range ends inside one, so the LDS-staged attention masks the
+    first and last tiles of each range, which the aligned sizes above never need."""
+    v = SV.VDIMS_FULL.with_(depth=2)
+    img = SV.images(v, 3, 224, 224)
+    _say("vision bf16, 2 blocks, 3 images of 224x224")
+    enc = _encoder(v)
+    got = _run(torch, enc, v, img)
+    enc.close()
+    ref = _oracle(v, img)
+    assert got.shape == (3 * 49, v.out_hidden)
+    for i in range(3):
+        err = rel_err(got[49 * i:49 * (i + 1)], ref[49 * i:49 * (i + 1)])
+        _say("  image", i, "err", err)
+        assert err <= TOL_SHORT
+
+
 def test_vision_bf16_full_depth(torch):
     v = SV.VDIMS_FULL
     img = SV.images(v, 1, 256, 256)
