@@ -37,7 +37,7 @@ static const double kTileRate[kNumTiles] = {959, 944, 895, 850, 850, 884, 850, 8
                                             640, 777, 860, 600, 700, 650, 550, 450, 600, 600,
                                             921, 850, 850, 714, 766, 800, 1026, 1018, 850, 728,
                                             803, 950, 950, 1150, 1106, 1084, 940, 1044, 1117,
-                                            300, 300, 300, 300, 300, 300, 300};
+                                            300, 300, 300, 300, 300, 300, 300, 800, 800};
 
 // Measured choices (MI355X sweep of every tile, split count and XCD placement,
 // weights rotated through 600 MB so that they stream from HBM; at 96 and 192 rows
@@ -47,7 +47,10 @@ static const double kTileRate[kNumTiles] = {959, 944, 895, 850, 850, 884, 850, 8
 // projections (D 2048 / FFN 6144 / 16+8+8 heads of 128) at 96 ... 10240 rows. A K split is only
 // kept where it still wins after the consumer's extra pass over the fp32
 // partial sums (at 1536 rows two QKV partials cost 16 us to add up, more than
-// the split saves). Other row counts take the entry of the nearest row
+// the split saves; the 1536-row QKV product runs on six-wave 192x128 tiles,
+// one workgroup per CU, in 34 us against 37.6 for 128x128 tiles, which put
+// two workgroups on half of the CUs and one on the rest). Other row counts
+// take the entry of the nearest row
 // count (log scale) for the same N, K and epilogue. `epi` is the epilogue of
 // the finished product; splits > 1 means the K splits write partial sums
 // that the consuming kernel adds up.
@@ -62,7 +65,7 @@ static const TileChoice kChoices[] = {
     {12288, 2048, EPI_SWIGLU, 192, 12, 1}, {2048, 6144, EPI_RESID, 192, 14, 8},
     {4096, 2048, EPI_QKV, 768, 12, 1, 241},    {2048, 2048, EPI_RESID, 768, 12, 2, 222},
     {12288, 2048, EPI_SWIGLU, 768, 3, 1},  {2048, 6144, EPI_RESID, 768, 14, 2},
-    {4096, 2048, EPI_QKV, 1536, 36, 1, 421},   {2048, 2048, EPI_RESID, 1536, 14, 1, 181},
+    {4096, 2048, EPI_QKV, 1536, 47, 1, 241},   {2048, 2048, EPI_RESID, 1536, 14, 1, 181},
     {12288, 2048, EPI_SWIGLU, 1536, 33, 1}, {2048, 6144, EPI_RESID, 1536, 8, 2},
     {4096, 2048, EPI_QKV, 3072, 38, 1},   {2048, 2048, EPI_RESID, 3072, 8, 1},
     {12288, 2048, EPI_SWIGLU, 3072, 33, 1}, {2048, 6144, EPI_RESID, 3072, 8, 1},

@@ -756,7 +756,9 @@ static hipError_t run(const GemmArgs &a, int splits, hipStream_t s) {
   X(42, 96, 64, 3, 2, 128, 8, 1, 0)          \
   X(43, 128, 64, 4, 1, 64, 12, 1, 0)         \
   X(44, 96, 128, 3, 2, 128, 5, 1, 0)         \
-  X(45, 96, 256, 3, 2, 64, 6, 1, 0)
+  X(45, 96, 256, 3, 2, 64, 6, 1, 0)          \
+  X(46, 192, 128, 6, 1, 128, 2, 1, 0)        \
+  X(47, 192, 128, 6, 1, 128, 3, 1, 0)
 
 
 template <int MODE, int EPI>
