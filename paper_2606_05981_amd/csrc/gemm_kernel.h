@@ -159,19 +159,19 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const 
                                              int mw, int lane) {
   constexpr int HJB = HD / 32;                    // column blocks per head
   constexpr int NH = TN / HJB;                    // heads of the wave
-  constexpr int NR = NH * HJB / 2;                // rotary blocks per row
   static_assert(TN % HJB == 0, "whole heads per wave");
   const QkvEpi &q = g.qe;
   const int lrow = lane & 31, lgrp = lane >> 5;
   const int M = g.M;
   float *C = (float *)g.C;
   const uint32_t lofs = (uint32_t)(4 * lgrp * g.ldc + lrow) * 4u;   // bytes
-  bool rot[NH];
+  bool rot[NH], anyrot = false;
   float gsc[TN];
 #pragma unroll
   for (int h = 0; h < NH; ++h) {
     const int cb = cw + h * HD;
     rot[h] = cb < q.rot_cols;                     // wave-uniform
+    anyrot |= rot[h];
     const float *gn = cb < q.nq_cols ? q.qn : q.kn;
 #pragma unroll
     for (int jj = 0; jj < HJB; ++jj) gsc[h * HJB + jj] = (rot[h] && gn) ? gn[jj * 32 + lrow] : 1.f;
@@ -180,39 +180,37 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const 
   for (int i = 0; i < TM; ++i) {
     const int mb = mw + i * 32;
     const bool full = mb + 32 <= M;               // wave-uniform
-    float tc[16][NR], ts[16][NR];
+    // the rotary entries of a row depend on the pair index only: one set of
+    // HJB / 2 blocks serves every head of the wave
+    float tc[16][HJB / 2], ts[16][HJB / 2];
 #pragma unroll
     for (int r = 0; r < 16; ++r)
 #pragma unroll
-      for (int x = 0; x < NR; ++x) {
-        tc[r][x] = 1.f;
-        ts[r][x] = 0.f;
+      for (int jj = 0; jj < HJB / 2; ++jj) {
+        tc[r][jj] = 1.f;
+        ts[r][jj] = 0.f;
       }
     // table row mb + acc_row(r, lane), clamped to M - 1 in a partial block
-    if (full) {
-      const uint32_t to = (uint32_t)(4 * lgrp * (HD / 2) + lrow) * 4u;
+    if (anyrot) {
+      if (full) {
+        const uint32_t to = (uint32_t)(4 * lgrp * (HD / 2) + lrow) * 4u;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const size_t rb = (size_t)(mb + acc_row0(r)) * (HD / 2);
+        for (int r = 0; r < 16; ++r) {
+          const size_t rb = (size_t)(mb + acc_row0(r)) * (HD / 2);
 #pragma unroll
-        for (int x = 0; x < NR; ++x) {
-          const int h = x / (HJB / 2), jj = x % (HJB / 2);
-          if (rot[h]) {
-            tc[r][x] = at(q.rcos + rb, to + jj * 128u);
-            ts[r][x] = at(q.rsin + rb, to + jj * 128u);
+          for (int jj = 0; jj < HJB / 2; ++jj) {
+            tc[r][jj] = at(q.rcos + rb, to + jj * 128u);
+            ts[r][jj] = at(q.rsin + rb, to + jj * 128u);
           }
         }
-      }
-    } else {
+      } else {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const size_t rb = (size_t)min(mb + acc_row(r, lane), M - 1) * (HD / 2);
+        for (int r = 0; r < 16; ++r) {
+          const size_t rb = (size_t)min(mb + acc_row(r, lane), M - 1) * (HD / 2);
 #pragma unroll
-        for (int x = 0; x < NR; ++x) {
-          const int h = x / (HJB / 2), jj = x % (HJB / 2);
-          if (rot[h]) {
-            tc[r][x] = q.rcos[rb + jj * 32 + lrow];
-            ts[r][x] = q.rsin[rb + jj * 32 + lrow];
+          for (int jj = 0; jj < HJB / 2; ++jj) {
+            tc[r][jj] = q.rcos[rb + jj * 32 + lrow];
+            ts[r][jj] = q.rsin[rb + jj * 32 + lrow];
           }
         }
       }
@@ -236,10 +234,10 @@ __device__ __forceinline__ void qkv_epilogue(const f32x16 (&acc)[TM][TN], const 
         }
 #pragma unroll
         for (int jj = 0; jj < HJB / 2; ++jj) {
-          const int j = h * HJB + jj, jp = j + HJB / 2, x = h * (HJB / 2) + jj;
+          const int j = h * HJB + jj, jp = j + HJB / 2;
           const float u = v[j], w = v[jp];
-          v[j] = u * tc[r][x] - w * ts[r][x];
-          v[jp] = w * tc[r][x] + u * ts[r][x];
+          v[j] = u * tc[r][jj] - w * ts[r][jj];
+          v[jp] = w * tc[r][jj] + u * ts[r][jj];
         }
       }
       if (q.qk) {
