@@ -215,10 +215,10 @@ def run_workload(torch, name, steps, warmup, timing_classes=(), use_graph=True, 
 
 
 def cpu_baseline():
-    """The fp64 oracle on the host cores, once over each workload of the survey's
-    configurations 0-3: the tiny fp32 decoder (32 tokens), one full-width layer (96
-    tokens) and the 28-layer stack at one frame (96 tokens), 8 frames and 16 frames
-    (packed batches of 96-token frames). `value` is the 16-frame rate, the benchmark's
+    """The fp64 oracle on the host cores, once over each of the small and medium
+    workloads: the tiny fp32 decoder (32 tokens), one full-width layer (96 tokens)
+    and the 28-layer stack at one frame (96 tokens), 8 frames and 16 frames (packed
+    batches of 96-token frames). `value` is the 16-frame rate, the benchmark's
     own workload; about 15 s of host time in all."""
     from oracle import te_oracle as O
     from synth import workloads as W
