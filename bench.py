@@ -86,8 +86,9 @@ KERNEL_CLASSES = {0: "qkv_gemm", 1: "attention", 2: "o_gemm", 3: "gate_up_gemm",
 def kernel_work(dims, lens):
     """Algorithmic flops and bytes of one launch of each timed kernel class at these
     sequence lengths (one layer): the projections read their fp16 weights and fp16 input
-    once and write their output (QKV fp32; SwiGLU fp16; the residual projections read
-    and write the fp32 residual stream); attention reads fp32 q/k/v and writes fp16 o.
+    once and write their output (QKV: fp16 attention operands; SwiGLU fp16; the residual
+    projections read and write the fp32 residual stream); attention reads fp16 q/k/v and
+    writes fp16 o.
     With a K split the timed launch is the split GEMM alone (its partial sums are added
     by the next kernel); its bytes are still counted as the finished product's."""
     T = sum(lens)
@@ -96,8 +97,8 @@ def kernel_work(dims, lens):
     g = gemm_flops(dims, T)
     att = sum(4 * hq * d * L * (L + 1) // 2 for L in lens)
     return {
-        0: (g["qkv"], 2 * nqkv * D + 2 * T * D + 4 * T * nqkv),
-        1: (att, 4 * T * nqkv + 2 * T * hq * d),
+        0: (g["qkv"], 2 * nqkv * D + 2 * T * D + 2 * T * nqkv),
+        1: (att, 2 * T * nqkv + 2 * T * hq * d),
         2: (g["o"], 2 * D * hq * d + 2 * T * hq * d + 8 * T * D),
         3: (g["gate_up"], 2 * 2 * F * D + 2 * T * D + 2 * T * F),
         4: (g["down"], 2 * D * F + 2 * T * F + 8 * T * D),
