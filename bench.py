@@ -733,6 +733,8 @@ def main():
                     help="skip the vision-tower run (16 images of 256x256)")
     ap.add_argument("--profile-pass", action="store_true",
                     help="only the main workload's warm-up and timed steps (for counter runs under rocprofv3)")
+    ap.add_argument("--e4m3-weights", action="store_true",
+                    help="with --profile-pass: the encoder holds e4m3 weights")
     ap.add_argument("--no-overlap", action="store_true",
                     help="skip the encoder on a side stream beside a main-stream GEMM load")
     args = ap.parse_args()
@@ -751,9 +753,9 @@ def main():
         return
 
     if args.profile_pass:
-        r = run_workload(torch, args.workload, args.steps, args.warmup)
-        print(json.dumps({"profile_pass": args.workload, "ms_per_step": round(r["wall_s"] * 1e3 / args.steps, 4)}),
-              flush=True)
+        r = run_workload(torch, args.workload, args.steps, args.warmup, weight_format=1 if args.e4m3_weights else 0)
+        print(json.dumps({"profile_pass": args.workload, "e4m3_weights": args.e4m3_weights,
+                          "ms_per_step": round(r["wall_s"] * 1e3 / args.steps, 4)}), flush=True)
         return
     main_run = run_workload(torch, args.workload, args.steps, args.warmup, timing_classes=(0, 1, 2, 3, 4))
     dims, T = main_run["dims"], main_run["T"]
